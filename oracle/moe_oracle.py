@@ -1,0 +1,423 @@
+"""Plain CPU oracle of the resident-expert MoE layer (fp64 NumPy).
+
+TEST INFRASTRUCTURE.  Only tests/, the package's smoke() entry and bench.py's
+cpu_baseline leg may import this module.  It shares no code with the HIP path
+and imports nothing from it.  It is written to be read against the paper, not
+to be fast: no blocking, no fusion, no reordering beyond what the definitions
+state.
+
+What it computes (arxiv 2606.19025):
+
+* The layer output is the gate-weighted sum of the selected experts' outputs,
+  y = sum_{i in T(x)} s_i(x) E_i(x), with T(x) the top-k of the router scores
+  (App. A, "MoE architectures and scaling", the two displayed equations;
+  App. B.3 "Sigmoid Routing").
+* Skip-token (Sec. 3.3 "Ghost Experts and Skip-Token"; Fig. "skipped-token"):
+  the router is NOT partitioned, so T(x) is chosen over all E experts; a route
+  whose expert is not resident on this worker (a "ghost expert") is dropped
+  from the local computation graph.  It contributes nothing to y and receives
+  no gradient through an expert path.  The gate weights of the surviving
+  routes are NOT renormalised over the surviving routes (App. B.3: the
+  unavailability of an expert must not skew the distribution over the
+  remaining ones).
+* The worker holds a resident subset S_m of the experts (Sec. 3.3.1/3.3.2 and
+  Alg. 1); routing is strictly local (Sec. 3.3.2 "System context and routing
+  logic"), so the dispatch groups routes only by resident expert.
+* Expert FFN: SwiGLU without biases, hidden H (the workloads' choice; the
+  paper's own expert is a single projection followed by SiLU, App. B.3.1).
+  Shared experts are dense, always active, weight 1 (Sec. 3.2).
+* Round boundary (Alg. 2 "Simplified View"; Sec. 3.4): the expert-wise
+  pseudo-gradient delta theta_start - theta_now of each resident expert,
+  averaged over the expert's replica group.
+
+Readings where the paper is silent (each is a convention of this build):
+  gate "softmax_topk" = softmax over all E experts renormalised over the global
+  top-k (before masking), so the k weights sum to 1; "softmax" = raw softmax
+  probabilities of the selected experts; "sigmoid" = the paper's sigma-MoE gate.
+  Selection is on the logits; ties go to the lower expert id.  Router
+  temperature enters as z = (x W_r^T + b) * inv_tau.  Dispatch order: groups in
+  ascending resident id, tokens ascending inside a group.  Dropless (no
+  capacity factor).  Delta average order: (((d0 + d1) + d2) + ...) * fp32(1/S).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F64 = np.float64
+
+
+def _f64(a):
+    return np.asarray(a, dtype=F64)
+
+
+# --------------------------------------------------------------------------
+# Routing: logits, top-k selection, gate weights, residency mask
+# --------------------------------------------------------------------------
+
+def router_logits(x, w_router, inv_tau=1.0, bias=None):
+    """z_t = (x_t . W_r^T + b) * inv_tau over ALL E experts.
+
+    Skip-token keeps the router unpartitioned (Sec. 3.3 "Ghost Experts and
+    Skip-Token"), so every worker scores every expert; the router is the
+    gating projection of App. B.3.2.
+    """
+    z = _f64(x) @ _f64(w_router).T
+    if bias is not None:
+        z = z + _f64(bias)[None, :]
+    return z * F64(inv_tau)
+
+
+def topk_select(z, k):
+    """T(x): the k experts with the largest logits, ties to the lower id.
+
+    App. A (TopK of the router scores).  The score map (sigmoid or softmax) is
+    monotone, so selecting on logits selects the same set.
+    """
+    z = _f64(z)
+    Tn, E = z.shape
+    idx = np.empty((Tn, k), dtype=np.int64)
+    for t in range(Tn):
+        # stable sort of -z keeps equal logits in ascending expert id
+        order = np.argsort(-z[t], kind="stable")
+        idx[t] = order[:k]
+    return idx
+
+
+def gate_weights(z, idx, gate="softmax_topk"):
+    """s_i(x) for the selected experts (App. A; App. B.3.2 for sigmoid)."""
+    z = _f64(z)
+    Tn, k = idx.shape
+    w = np.empty((Tn, k), dtype=F64)
+    for t in range(Tn):
+        zs = z[t, idx[t]]
+        if gate == "sigmoid":
+            w[t] = 1.0 / (1.0 + np.exp(-zs))
+        elif gate == "softmax":
+            m = z[t].max()
+            e = np.exp(z[t] - m)
+            w[t] = e[idx[t]] / e.sum()
+        elif gate == "softmax_topk":
+            m = zs.max()
+            e = np.exp(zs - m)
+            w[t] = e / e.sum()
+        else:
+            raise ValueError(gate)
+    return w
+
+
+def resident_local_ids(resident):
+    """local id of every expert: its rank in the sorted resident set, -1 if ghost."""
+    resident = np.asarray(resident).astype(bool)
+    local = np.full(resident.shape[0], -1, dtype=np.int64)
+    r = 0
+    for e in range(resident.shape[0]):
+        if resident[e]:
+            local[e] = r
+            r += 1
+    return local
+
+
+def mask_routes(idx, resident):
+    """Ghost-expert mask (Sec. 3.3): local expert id per route, -1 for a ghost."""
+    lid = resident_local_ids(resident)
+    return lid[idx]
+
+
+def route(x, w_router, k, resident, inv_tau=1.0, gate="softmax_topk", bias=None):
+    z = router_logits(x, w_router, inv_tau, bias)
+    idx = topk_select(z, k)
+    w = gate_weights(z, idx, gate)
+    local = mask_routes(idx, resident)
+    return dict(logits=z, idx=idx, w=w, local=local)
+
+
+# --------------------------------------------------------------------------
+# Dispatch: stable grouping of the resident routes by local expert
+# --------------------------------------------------------------------------
+
+def dispatch_plan(local, E_r):
+    """counts, exclusive-scan offsets, perm (route id t*k+j per slot) and inv_perm.
+
+    Tokens go only to experts hosted on this worker (Sec. 3.3.2 "System
+    context and routing logic"); ghost routes get no slot (inv_perm = -1).
+    """
+    local = np.asarray(local)
+    Tn, k = local.shape
+    counts = np.zeros(E_r, dtype=np.int64)
+    for t in range(Tn):
+        for j in range(k):
+            if local[t, j] >= 0:
+                counts[local[t, j]] += 1
+    offsets = np.zeros(E_r + 1, dtype=np.int64)
+    for r in range(E_r):
+        offsets[r + 1] = offsets[r] + counts[r]
+    perm = []
+    inv_perm = np.full((Tn, k), -1, dtype=np.int64)
+    for r in range(E_r):
+        for t in range(Tn):
+            for j in range(k):
+                if local[t, j] == r:
+                    inv_perm[t, j] = len(perm)
+                    perm.append(t * k + j)
+    return dict(counts=counts, offsets=offsets, perm=np.array(perm, dtype=np.int64),
+                inv_perm=inv_perm)
+
+
+def gather_rows(x, perm, k):
+    """Xp[p] = x[perm[p] // k]."""
+    x = _f64(x)
+    return x[np.asarray(perm, dtype=np.int64) // k] if len(perm) else np.zeros((0, x.shape[1]))
+
+
+# --------------------------------------------------------------------------
+# Expert FFN (SwiGLU, no biases)
+# --------------------------------------------------------------------------
+
+def silu(a):
+    return a / (1.0 + np.exp(-a))
+
+
+def swiglu_fwd(X, w_gate_up, w_down):
+    """One expert: G = X Wg^T, U = X Wu^T, Hh = silu(G)*U, Y = Hh Wd^T.
+
+    w_gate_up [2H, d] holds the gate rows then the up rows; w_down [d, H].
+    """
+    X = _f64(X)
+    H = w_gate_up.shape[0] // 2
+    Wg = _f64(w_gate_up[:H])
+    Wu = _f64(w_gate_up[H:])
+    G = X @ Wg.T
+    U = X @ Wu.T
+    Hh = silu(G) * U
+    Y = Hh @ _f64(w_down).T
+    return dict(G=G, U=U, Hh=Hh, Y=Y)
+
+
+def swiglu_bwd(dY, X, G, U, Hh, w_gate_up, w_down):
+    """Chain rule of swiglu_fwd for one expert.
+
+    dHh = dY Wd; dWd = dY^T Hh; dG = dHh*U*silu'(G); dU = dHh*silu(G);
+    dX = dG Wg + dU Wu; dWg = dG^T X; dWu = dU^T X.
+    """
+    dY, X, G, U, Hh = map(_f64, (dY, X, G, U, Hh))
+    H = w_gate_up.shape[0] // 2
+    Wg = _f64(w_gate_up[:H])
+    Wu = _f64(w_gate_up[H:])
+    Wd = _f64(w_down)
+    dHh = dY @ Wd
+    dWd = dY.T @ Hh
+    sg = 1.0 / (1.0 + np.exp(-G))
+    dG = dHh * U * (sg * (1.0 + G * (1.0 - sg)))
+    dU = dHh * (G * sg)
+    dX = dG @ Wg + dU @ Wu
+    dWgu = np.concatenate([dG.T @ X, dU.T @ X], axis=0)
+    return dict(dHh=dHh, dG=dG, dU=dU, dX=dX, dW_gate_up=dWgu, dW_down=dWd)
+
+
+def grouped_ffn_fwd(Xp, offsets, w_gate_up, w_down):
+    """Per resident group r: rows [offsets[r], offsets[r+1]) of Xp through expert r."""
+    Xp = _f64(Xp)
+    n = int(offsets[-1])
+    H = w_gate_up.shape[1] // 2
+    d = w_down.shape[1]
+    G = np.zeros((n, H)); U = np.zeros((n, H)); Hh = np.zeros((n, H)); Y = np.zeros((n, d))
+    for r in range(len(offsets) - 1):
+        a, b = int(offsets[r]), int(offsets[r + 1])
+        if b > a:
+            o = swiglu_fwd(Xp[a:b], w_gate_up[r], w_down[r])
+            G[a:b], U[a:b], Hh[a:b], Y[a:b] = o["G"], o["U"], o["Hh"], o["Y"]
+    return dict(G=G, U=U, Hh=Hh, Y=Y)
+
+
+def grouped_ffn_bwd(dYp, Xp, G, U, Hh, offsets, w_gate_up, w_down):
+    n = int(offsets[-1])
+    Er = len(offsets) - 1
+    H = w_gate_up.shape[1] // 2
+    d = w_down.shape[1]
+    dXp = np.zeros((n, d)); dG = np.zeros((n, H)); dU = np.zeros((n, H))
+    dWgu = np.zeros((Er, 2 * H, d)); dWd = np.zeros((Er, d, H))
+    for r in range(Er):
+        a, b = int(offsets[r]), int(offsets[r + 1])
+        if b > a:
+            o = swiglu_bwd(dYp[a:b], Xp[a:b], G[a:b], U[a:b], Hh[a:b], w_gate_up[r], w_down[r])
+            dXp[a:b], dG[a:b], dU[a:b] = o["dX"], o["dG"], o["dU"]
+            dWgu[r], dWd[r] = o["dW_gate_up"], o["dW_down"]
+    return dict(dXp=dXp, dG=dG, dU=dU, dW_gate_up=dWgu, dW_down=dWd)
+
+
+# --------------------------------------------------------------------------
+# Combine (weighted sum over resident routes) and its backward
+# --------------------------------------------------------------------------
+
+def combine_fwd(Yp, w, inv_perm, y_add=None):
+    """y_t = sum_{j: route resident} w_tj * Yp[inv_perm[t,j]]  (+ y_add_t).
+
+    A route to a ghost expert contributes nothing (Sec. 3.3); a token whose
+    k routes are all ghosts gets exactly y_add_t (0 without shared experts).
+    """
+    Yp = _f64(Yp)
+    Tn, k = inv_perm.shape
+    d = Yp.shape[1] if Yp.ndim == 2 and Yp.shape[0] else (y_add.shape[1] if y_add is not None else 0)
+    y = np.zeros((Tn, d))
+    for t in range(Tn):
+        for j in range(k):
+            p = inv_perm[t, j]
+            if p >= 0:
+                y[t] += F64(w[t, j]) * Yp[p]
+    if y_add is not None:
+        y = y + _f64(y_add)
+    return y
+
+
+def combine_bwd(dy, Yp, w, inv_perm):
+    """dYp[p] = w_tj * dy_t ; dw_tj = <dy_t, Yp[p]>  (0 for a ghost route)."""
+    dy = _f64(dy); Yp = _f64(Yp)
+    Tn, k = inv_perm.shape
+    dYp = np.zeros_like(Yp)
+    dw = np.zeros((Tn, k))
+    for t in range(Tn):
+        for j in range(k):
+            p = inv_perm[t, j]
+            if p >= 0:
+                dYp[p] = F64(w[t, j]) * dy[t]
+                dw[t, j] = dy[t] @ Yp[p]
+    return dict(dYp=dYp, dw=dw)
+
+
+def dispatch_bwd(dXp, inv_perm, d, dx_add=None):
+    """dx_t = sum_{j: resident} dXp[inv_perm[t,j]]  (+ dx_add_t)."""
+    dXp = _f64(dXp)
+    Tn, k = inv_perm.shape
+    dx = np.zeros((Tn, d))
+    for t in range(Tn):
+        for j in range(k):
+            p = inv_perm[t, j]
+            if p >= 0:
+                dx[t] += dXp[p]
+    if dx_add is not None:
+        dx = dx + _f64(dx_add)
+    return dx
+
+
+# --------------------------------------------------------------------------
+# Router backward
+# --------------------------------------------------------------------------
+
+def gate_bwd(z, idx, w, dw, gate="softmax_topk"):
+    """dL/dz [T, E] from dL/dw [T, k], with the top-k set held fixed.
+
+    softmax_topk: w = softmax over the selected logits -> dz_Kj = w_j (dw_j - <w, dw>)
+    softmax:      w_j = p_Kj, p = softmax(z) over all E -> dz_e = p_e (g_e - <w, dw>),
+                  g_e = dw_j where e = K_j, else 0
+    sigmoid:      dz_Kj = dw_j w_j (1 - w_j)
+    """
+    z = _f64(z); w = _f64(w); dw = _f64(dw)
+    Tn, E = z.shape
+    k = idx.shape[1]
+    dz = np.zeros((Tn, E))
+    for t in range(Tn):
+        if gate == "softmax_topk":
+            s = float(w[t] @ dw[t])
+            for j in range(k):
+                dz[t, idx[t, j]] = w[t, j] * (dw[t, j] - s)
+        elif gate == "softmax":
+            p = np.exp(z[t] - z[t].max()); p /= p.sum()
+            g = np.zeros(E)
+            for j in range(k):
+                g[idx[t, j]] = dw[t, j]
+            dz[t] = p * (g - float(w[t] @ dw[t]))
+        elif gate == "sigmoid":
+            for j in range(k):
+                dz[t, idx[t, j]] = dw[t, j] * w[t, j] * (1.0 - w[t, j])
+        else:
+            raise ValueError(gate)
+    return dz
+
+
+def route_bwd(x, w_router, idx, w, logits, dw, inv_tau=1.0, gate="softmax_topk"):
+    """Backward of z = (x W_r^T + b) * inv_tau through the gate weights.
+
+    ds = dz * inv_tau;  dW_r = ds^T x;  db = sum_t ds_t;  dx_router = ds W_r.
+    """
+    dz = gate_bwd(logits, idx, w, dw, gate)
+    ds = dz * F64(inv_tau)
+    x = _f64(x)
+    return dict(dz=dz, dW_router=ds.T @ x, d_bias=ds.sum(axis=0), dx=ds @ _f64(w_router))
+
+
+# --------------------------------------------------------------------------
+# Whole layer (composition of the steps)
+# --------------------------------------------------------------------------
+
+def layer_fwd(inp, inv_tau=1.0, gate="softmax_topk", logits=None):
+    """Forward of the resident-expert layer.
+
+    ``logits`` (optional) replaces the router projection, so the selection can
+    be checked on exactly the logits another implementation produced.
+    """
+    cfg = inp["cfg"]
+    k, E_r = cfg["k"], cfg["E_r"]
+    x = _f64(inp["x"])
+    if logits is None:
+        z = router_logits(x, inp["w_router"], inv_tau, inp.get("router_bias"))
+    else:
+        z = _f64(logits)
+    idx = topk_select(z, k)
+    w = gate_weights(z, idx, gate)
+    local = mask_routes(idx, inp["resident"])
+    plan = dispatch_plan(local, E_r)
+    Xp = gather_rows(x, plan["perm"], k)
+    f = grouped_ffn_fwd(Xp, plan["offsets"], inp["w_gate_up"], inp["w_down"])
+    ys = None
+    shared = None
+    if inp.get("shared_gate_up") is not None:
+        shared = swiglu_fwd(x, inp["shared_gate_up"][0], inp["shared_down"][0])
+        ys = shared["Y"]
+    y = combine_fwd(f["Y"], w, plan["inv_perm"], ys)
+    return dict(logits=z, idx=idx, w=w, local=local, **plan, Xp=Xp, G=f["G"], U=f["U"],
+                Hh=f["Hh"], Yp=f["Y"], shared=shared, y=y)
+
+
+def layer_bwd(inp, fwd, dy, inv_tau=1.0, gate="softmax_topk"):
+    """Backward of the resident-expert layer for upstream gradient dy."""
+    cfg = inp["cfg"]
+    d = cfg["d"]
+    x = _f64(inp["x"])
+    cb = combine_bwd(dy, fwd["Yp"], fwd["w"], fwd["inv_perm"])
+    gb = grouped_ffn_bwd(cb["dYp"], fwd["Xp"], fwd["G"], fwd["U"], fwd["Hh"], fwd["offsets"],
+                         inp["w_gate_up"], inp["w_down"])
+    dx_shared = None
+    sb = None
+    if fwd["shared"] is not None:
+        s = fwd["shared"]
+        sb = swiglu_bwd(dy, x, s["G"], s["U"], s["Hh"], inp["shared_gate_up"][0], inp["shared_down"][0])
+        dx_shared = sb["dX"]
+    dx = dispatch_bwd(gb["dXp"], fwd["inv_perm"], d, dx_shared)
+    rb = route_bwd(x, inp["w_router"], fwd["idx"], fwd["w"], fwd["logits"], cb["dw"], inv_tau, gate)
+    dx = dx + rb["dx"]
+    return dict(dYp=cb["dYp"], dw=cb["dw"], dXp=gb["dXp"], dG=gb["dG"], dU=gb["dU"],
+                dW_gate_up=gb["dW_gate_up"], dW_down=gb["dW_down"], shared=sb,
+                dz=rb["dz"], dW_router=rb["dW_router"], d_bias=rb["d_bias"], dx=dx)
+
+
+# --------------------------------------------------------------------------
+# Round boundary: expert-wise pseudo-gradient delta
+# --------------------------------------------------------------------------
+
+def expert_delta(theta_start, theta_now, peers):
+    """Delta of this site and its average over the replica group, in fp32.
+
+    Alg. 2 (round end): sparse parameters are aggregated within each expert's
+    replica group.  Delta_local = theta_start - theta_now; the group average is
+    (((Delta_local + D_1) + D_2) + ...) * fp32(1 / (n_peers + 1)), evaluated
+    in exactly that order in fp32, so the result is reproducible bit for bit.
+    """
+    f32 = np.float32
+    a = np.asarray(theta_start, dtype=f32)
+    b = np.asarray(theta_now, dtype=f32)
+    dl = (a - b).astype(f32)
+    acc = dl.copy()
+    for p in peers:
+        acc = (acc + np.asarray(p, dtype=f32)).astype(f32)
+    scale = f32(1.0) / f32(len(peers) + 1)
+    return dl, (acc * scale).astype(f32)
