@@ -1,0 +1,241 @@
+"""Benchmark of one worker's local training step through the resident-expert
+MoE layer on one MI355X.
+
+A step is one forward + backward of the whole layer (router, ghost-expert
+mask, dispatch, grouped SwiGLU experts, shared experts, combine, and all of
+their backward), and - at the round cadence (every ``--round-every`` steps,
+32 = the smallest number of local steps between synchronisations in the
+paper's sweep grid, App. F) - the round-boundary expert delta averaged over
+the expert's replica group.  Inputs are seeded synthetic tensors already
+resident in HBM; the timed region holds exactly ``--steps`` steps bracketed by
+torch.cuda.synchronize().
+
+Prints ONE JSON line.  Besides the contract fields it carries:
+  roofline      the dominant kernel's achieved rate vs the MI355X peak, from
+                algorithmic flops (or bytes) per launch and its average launch
+                duration measured with HIP events in a second pass of the same
+                steps (the library's moe_timing facility);
+  kernels       the same for every kernel of the step;
+  cpu_baseline  the CPU oracle on a bounded token sample of the same workload.
+
+    python bench.py [--gpus 1] [--steps 64] [--warmup 10] [--workload 2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--round-every", type=int, default=32)
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    return ap.parse_args()
+
+
+def algorithmic_work(cfg, n, t_act, s):
+    """Per-step algorithmic flops / bytes of every kernel (summed over its launches).
+
+    n: executed (resident) routes; t_act: tokens with at least one resident
+    route; s: bytes per activation element.
+    """
+    T, d, E, k, H = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["H"]
+    Hs = cfg["n_shared"] * cfg["Hs"]
+    rows = [(n, H)] + ([(T, Hs)] if Hs else [])
+    w = {}
+    # grouped GEMMs: flops (MFMA-bound)
+    w["gemm_gu_fwd"] = ("flop", sum(2.0 * m * d * 2 * h for m, h in rows))
+    w["gemm_down_fwd"] = ("flop", sum(2.0 * m * h * d for m, h in rows))
+    w["gemm_dhh_bwd"] = ("flop", sum(2.0 * m * d * h for m, h in rows))
+    w["gemm_dx_bwd"] = ("flop", sum(2.0 * m * 2 * h * d for m, h in rows))
+    w["gemm_dwd"] = ("flop", sum(2.0 * m * d * h for m, h in rows))
+    w["gemm_dwgu"] = ("flop", sum(2.0 * m * 2 * h * d for m, h in rows))
+    # routing / data movement: bytes (HBM-bound)
+    w["route_fwd"] = ("byte", T * d * s + E * d * s + T * E * 4 + 3 * T * k * 4)
+    w["dispatch_count"] = ("byte", T * k * 4)
+    w["dispatch_scan"] = ("byte", 0)
+    w["dispatch_scatter"] = ("byte", T * k * 4 + n * 4 + T * k * 4)
+    w["dispatch_gather"] = ("byte", t_act * d * s + n * d * s + T * k * 4)
+    w["combine_fwd"] = ("byte", n * d * s + (T * d * s if Hs else 0) + T * d * s + T * k * 8)
+    w["combine_bwd"] = ("byte", t_act * d * s + 2 * n * d * s + T * k * 12)
+    w["unpermute"] = ("byte", n * d * s + (T * d * s if Hs else 0) + T * d * s + T * k * 4)
+    w["route_dz"] = ("byte", T * k * 12 + T * E * 4)
+    w["route_dw_partial"] = ("byte", T * E * 4 + T * d * s)
+    w["route_dw_reduce"] = ("byte", E * d * 4)
+    w["route_dx"] = ("byte", T * E * 4 + 2 * T * d * s + E * d * s)
+    return w
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2606_19025_amd import binding as B
+    from paper_2606_19025_amd import inputs as I
+    from paper_2606_19025_amd.layer import ResidentMoELayer, expert_delta
+
+    B.lib()
+    wl = args.workload
+    log(f"[bench] workload {wl}: generating inputs")
+    inp = I.make_layer_inputs(wl, seed=args.seed)
+    cfg = inp["cfg"]
+    T, d, E, k, H, Er = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["H"], cfg["E_r"]
+    Hs = cfg["n_shared"] * cfg["Hs"]
+    dt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    s_bytes = 2 if dt == torch.bfloat16 else 4
+    dev = lambda a, t=dt: None if a is None else torch.from_numpy(
+        np.ascontiguousarray(a, np.float32)).cuda().to(t)
+    x, dy, wr, wgu, wd = (dev(inp[n]) for n in ("x", "dy", "w_router", "w_gate_up", "w_down"))
+    bias = dev(inp.get("router_bias"), torch.float32)
+    sgu, sd = dev(inp.get("shared_gate_up")), dev(inp.get("shared_down"))
+    L = ResidentMoELayer(T, d, E, k, H, inp["resident"], dtype=dt, n_shared_hidden=Hs)
+    # round boundary: fp32 master copies of the resident experts
+    n_params = Er * (2 * H * d + d * H)
+    log(f"[bench] round-boundary state: {n_params / 1e6:.1f} M fp32 params x {2 + max(1, cfg['n_peers'])}")
+    dpar = I.make_delta_inputs(wl, n_params, seed=args.seed)
+    th0, th1 = dev(dpar["theta_start"], torch.float32), dev(dpar["theta_now"], torch.float32)
+    peers = [dev(p, torch.float32) for p in dpar["peers"]]
+    avg = torch.empty_like(th0)
+    del dpar
+
+    def step(i):
+        L.forward(x, wr, wgu, wd, bias, sgu, sd)
+        L.backward(dy, x, wr, wgu, wd, sgu, sd)
+        if (i + 1) % args.round_every == 0:
+            expert_delta(th0, th1, peers, delta_avg=avg)
+
+    log(f"[bench] warmup {args.warmup}")
+    for i in range(args.warmup):
+        step(i)
+    expert_delta(th0, th1, peers, delta_avg=avg)
+    torch.cuda.synchronize()
+
+    log(f"[bench] timing {args.steps} steps")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for i in range(args.steps):
+        step(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = ev0.elapsed_time(ev1)
+    ms_per_step = ms_total / args.steps
+    value = T / (ms_per_step / 1e3)
+    n = int(L.offsets[-1].item())
+    local = L.topk_local.cpu().numpy()
+    t_act = int((local >= 0).any(axis=1).sum())
+    log(f"[bench] {ms_per_step:.3f} ms/step ({wall:.2f} s wall), n={n}, tokens/s={value:.4g}")
+
+    kernels = {}
+    roofline = None
+    if not args.no_kernel_timing:
+        B.moe_timing_enable(64 * (args.steps + 2))
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        stats = B.moe_timing_collect()
+        B.moe_timing_enable(0)
+        work = algorithmic_work(cfg, n, t_act, s_bytes)
+        n_delta = args.steps // args.round_every
+        work["expert_delta"] = ("byte", 4.0 * n_params * (3 + len(peers)))
+        for name, (launches, tot, mn, mx) in stats.items():
+            kind, per_step = work.get(name, ("byte", 0.0))
+            steps_with = n_delta if name == "expert_delta" else args.steps
+            amount = per_step * steps_with
+            rate = amount / (tot / 1e3) if tot > 0 else 0.0
+            if kind == "flop":
+                ent = dict(unit="TFLOP/s", achieved=rate / 1e12,
+                           peak=PEAK_BF16_TFLOPS if s_bytes == 2 else PEAK_F32_TFLOPS)
+            else:
+                ent = dict(unit="GB/s", achieved=rate / 1e9, peak=PEAK_HBM_GBS)
+            ent["frac"] = ent["achieved"] / ent["peak"]
+            ent.update(launches=launches, avg_us=1e3 * tot / max(launches, 1),
+                       ms_per_step=tot / args.steps)
+            kernels[name] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in ent.items()}
+        dom = max((nm for nm in kernels if nm != "expert_delta"),
+                  key=lambda nm: kernels[nm]["ms_per_step"])
+        kd = kernels[dom]
+        kind, per_step = work[dom]
+        roofline = dict(kernel=dom, bound="mfma" if kind == "flop" else "hbm",
+                        achieved=kd["achieved"], peak=kd["peak"], unit=kd["unit"],
+                        frac=kd["frac"], avg_us=kd["avg_us"],
+                        per_launch=per_step / max(1, kd["launches"] // args.steps),
+                        traffic=None)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import moe_oracle as O
+        ts = args.cpu_sample_tokens or min(T, 4096)
+        sample = I.make_layer_inputs(wl, seed=args.seed, T=ts)
+        try:
+            from threadpoolctl import threadpool_info
+            blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        except Exception:  # pragma: no cover
+            blas_threads = None
+        cores = len(os.sched_getaffinity(0))
+        log(f"[bench] cpu oracle on {ts} tokens ({cores} cores)")
+        c0 = time.perf_counter()
+        f = O.layer_fwd(sample)
+        O.layer_bwd(sample, f, sample["dy"])
+        csec = time.perf_counter() - c0
+        cpu = dict(value=round(ts / csec, 3), unit="tokens/s", cores=blas_threads or cores,
+                   kind="oracle", seconds=round(csec, 2),
+                   sample=f"first {ts} of {T} tokens of the same workload, fp64 NumPy oracle "
+                          f"fwd+bwd of the layer (round-boundary delta not included); "
+                          f"{cores} cores in the affinity mask")
+
+    out = {
+        "metric": "MoE layer fwd+bwd tokens/s (1 GPU)",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if s_bytes == 2 else "f32",
+        "data": "synthetic (seeded, shapes of the workload)",
+        "config": {"workload": cfg["name"], "T": T, "d": d, "E": E, "E_resident": Er, "k": k,
+                   "H": H, "shared_hidden": Hs, "round_every": args.round_every,
+                   "executed_routes": n, "skip_fraction": round(1 - n / (T * k), 4)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,233 @@
+/*
+ * moe_resident.h - C ABI of the resident-expert MoE layer on MI355X (gfx950).
+ *
+ * One worker's local training step through a mixture-of-experts layer in which
+ * the worker holds only its resident subset S_m of the experts (arxiv
+ * 2606.19025, Sec. 3.3 "Experts partitioning" and "Ghost Experts and
+ * Skip-Token"; Alg. 2 "Simplified View").  The router is not partitioned: it
+ * scores all E experts, the top-k is taken over all of them, and routes whose
+ * expert is not resident ("ghost experts") are skipped - they contribute
+ * nothing to the output and receive no gradient through an expert path.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers are DEVICE pointers owned by the caller, unless stated
+ *    otherwise.  Tensors are dense, row-major and contiguous.
+ *  - dtype is MOE_F32 or MOE_BF16 and applies to activations, expert weights
+ *    and router weights.  Logits, gate weights, their gradients, dz and every
+ *    weight gradient are always fp32.  bf16 results are rounded to nearest
+ *    even; all accumulation is fp32.
+ *  - Arguments are validated on the host before anything is launched; a
+ *    failed check returns a negative status and launches nothing.  The
+ *    message for the last failure of the calling thread is moe_last_error().
+ *  - Calls are asynchronous on `stream`: they never allocate, never
+ *    synchronise the host, and never read device data back (data-dependent
+ *    sizes, such as the number of executed routes, stay on the device).
+ *  - The library keeps no state between calls and is reentrant.  Results are
+ *    deterministic: the same inputs give the same bits on every call.
+ *  - Non-finite inputs give unspecified (but in-bounds) results.
+ */
+#ifndef MOE_RESIDENT_H
+#define MOE_RESIDENT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element types */
+enum { MOE_F32 = 0, MOE_BF16 = 1 };
+
+/* gate functions s_i(x) applied to the selected logits z (App. A; App. B.3.2):
+ *  MOE_GATE_SOFTMAX_TOPK  softmax over all E experts renormalised over the
+ *                         global top-k, i.e. softmax of the k selected logits;
+ *                         the k weights of a token sum to 1 BEFORE masking and
+ *                         are never renormalised over the surviving resident
+ *                         routes (App. B.3.2: an unavailable expert must not
+ *                         skew the weights of the available ones).
+ *  MOE_GATE_SOFTMAX       raw softmax probability over all E experts.
+ *  MOE_GATE_SIGMOID       independent logistic gate (the sigma-MoE gate). */
+enum { MOE_GATE_SOFTMAX_TOPK = 0, MOE_GATE_SOFTMAX = 1, MOE_GATE_SIGMOID = 2 };
+
+/* status codes */
+enum { MOE_OK = 0, MOE_ERR_ARG = -1, MOE_ERR_UNSUPPORTED = -2, MOE_ERR_HIP = -3 };
+
+/* Message for the last non-OK return on the calling thread ("" if none). */
+const char* moe_last_error(void);
+
+/* ABI version of this header (incremented on incompatible change). */
+int moe_abi_version(void);
+
+/*
+ * Router scores, top-k selection, gate weights and ghost-expert mask
+ * (App. A: T(x) = TopK of the router scores; Sec. 3.3: ghost experts).
+ *
+ *   z[t,e]        = (x[t,:] . w_router[e,:] + router_bias[e]) * inv_tau, all E
+ *   topk_idx[t,j] = the k experts with the largest z[t,:], in descending z;
+ *                   equal logits go to the lower expert id
+ *   topk_w[t,j]   = gate weight of topk_idx[t,j] (see MOE_GATE_*)
+ *   topk_local[t,j] = rank of topk_idx[t,j] in the sorted resident set, or -1
+ *                   when that expert is not resident (a ghost route)
+ *
+ * x [T,d] dtype; w_router [E,d] dtype; router_bias [E] fp32 or NULL;
+ * resident [E] uint8 (nonzero = resident on this worker);
+ * logits [T,E] fp32 or NULL (not written when NULL);
+ * topk_idx, topk_local [T,k] int32; topk_w [T,k] fp32.
+ * Limits: 1 <= k <= E <= 256, T >= 0, d >= 1 (d % 8 == 0 for bf16).
+ */
+int moe_route_mask(const void* x, const void* w_router, const float* router_bias, int dtype,
+                   int T, int d, int E, int k, float inv_tau, int gate,
+                   const uint8_t* resident, float* logits, int32_t* topk_idx,
+                   float* topk_w, int32_t* topk_local, hipStream_t stream);
+
+/*
+ * Backward of moe_route_mask with the top-k set held fixed.
+ *
+ *   dz[t,e]         = dL/dz[t,e] (fp32 [T,E], written in full; zero off the
+ *                     top-k for the SOFTMAX_TOPK and SIGMOID gates)
+ *   dw_router[e,:]  = inv_tau * sum_t dz[t,e] x[t,:]      (fp32 [E,d])
+ *   d_bias[e]       = inv_tau * sum_t dz[t,e]             (fp32 [E] or NULL)
+ *   dx[t,:]        (+)= inv_tau * sum_e dz[t,e] w_router[e,:]   (dtype [T,d])
+ *
+ * d_topk_w [T,k] fp32 is dL/dtopk_w (0 for ghost routes, as moe_combine_bwd
+ * writes it).  logits is required for MOE_GATE_SOFTMAX and may be NULL
+ * otherwise.  accumulate_dx != 0 adds into dx, else overwrites it.
+ * ws: device workspace of at least moe_route_bwd_workspace_size(T, d, E) bytes.
+ */
+size_t moe_route_bwd_workspace_size(int T, int d, int E);
+int moe_route_bwd(const void* x, const void* w_router, int dtype, int T, int d, int E, int k,
+                  float inv_tau, int gate, const int32_t* topk_idx, const float* topk_w,
+                  const float* logits, const float* d_topk_w, float* dz, float* dw_router,
+                  float* d_bias, void* dx, int accumulate_dx, void* ws, size_t ws_bytes,
+                  hipStream_t stream);
+
+/*
+ * Dispatch: group the resident routes by local expert (tokens are processed
+ * only by experts hosted on this worker, Sec. 3.3.2) and gather their rows.
+ *
+ *   counts[r]  = number of routes with topk_local == r            [E_r]
+ *   offsets[r] = sum_{r' < r} counts[r'];  offsets[E_r] = n          [E_r+1]
+ *   slots [offsets[r], offsets[r+1]) hold the routes of local expert r in
+ *   ascending token order; perm[p] = t*k + j of the route in slot p
+ *   inv_perm[t,j] = its slot, or -1 for a ghost route               [T,k]
+ *   xp[p,:] = x[perm[p]/k, :]                                         [cap,d]
+ *
+ * cap = T * min(k, E_r) bounds n; perm and xp have cap rows, of which rows
+ * n..cap-1 are left untouched.  ws: at least moe_dispatch_workspace_size()
+ * bytes.  Limits: E_r <= 256.
+ */
+size_t moe_dispatch_workspace_size(int T, int k, int E_r);
+int moe_dispatch(const void* x, int dtype, int T, int d, int k, int E_r,
+                 const int32_t* topk_local, int32_t* counts, int32_t* offsets,
+                 int32_t* perm, int32_t* inv_perm, void* xp, void* ws, size_t ws_bytes,
+                 hipStream_t stream);
+
+/*
+ * Backward of the gather (un-permute):
+ *   dx[t,:] (+)= sum_{j: inv_perm[t,j] >= 0} dxp[inv_perm[t,j], :]
+ * A token whose routes are all ghosts gets exactly 0 (or keeps dx when
+ * accumulate != 0).  dxp [cap,d], dx [T,d], both dtype.  Slots outside
+ * [0, cap) are treated as ghost routes (cap = rows of dxp).
+ */
+int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
+                     const int32_t* inv_perm, void* dx, int accumulate, hipStream_t stream);
+
+/*
+ * Grouped SwiGLU expert FFN, forward.  Group g is rows [offsets[g],
+ * offsets[g+1]) of xp and uses expert g's weights:
+ *   G = X Wg^T, U = X Wu^T, Hh = silu(G) * U, Y = Hh Wd^T   (no biases)
+ * w_gate_up [n_groups, 2H, d]: rows 0..H-1 are Wg, rows H..2H-1 are Wu.
+ * w_down    [n_groups, d, H].
+ * Outputs (rows of each group only): gu [cap, 2H] = [G | U], h [cap, H] = Hh,
+ * yp [cap, d].  Shared (always-active) experts are run through the same call
+ * with n_groups = 1, offsets = {0, T}, xp = x; several shared experts on the
+ * same input are one expert with their hidden units concatenated.
+ * offsets is a device array of n_groups + 1 non-decreasing int32 values; each
+ * group is clamped to [0, cap].
+ * Limits (bf16): d % 64 == 0, H % 64 == 0.
+ */
+int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_down, int dtype,
+                        int cap, int d, int H, int n_groups, const int32_t* offsets,
+                        void* gu, void* h, void* yp, hipStream_t stream);
+
+/*
+ * Grouped SwiGLU expert FFN, backward (chain rule of the forward, per group):
+ *   dHh = dY Wd;  dG = dHh * U * silu'(G);  dU = dHh * silu(G)
+ *   dX  = dG Wg + dU Wu
+ *   dWd = dY^T Hh;  dWg = dG^T X;  dWu = dU^T X           (fp32, per expert)
+ * dyp [cap,d], xp [cap,d], gu [cap,2H], h [cap,H] as written by the forward.
+ * Outputs: dgu [cap,2H] = [dG | dU] (dtype), dxp [cap,d] (dtype),
+ * dw_gate_up [n_groups,2H,d] fp32, dw_down [n_groups,d,H] fp32 - written for
+ * every group (zero for an empty group), or added to when accumulate_dw != 0.
+ */
+int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
+                        const void* w_gate_up, const void* w_down, int dtype, int cap, int d,
+                        int H, int n_groups, const int32_t* offsets, void* dgu, void* dxp,
+                        float* dw_gate_up, float* dw_down, int accumulate_dw,
+                        hipStream_t stream);
+
+/*
+ * Weighted combine (App. A: y = sum_{i in T(x)} s_i(x) E_i(x)):
+ *   y[t,:] = sum_{j: inv_perm[t,j] >= 0} topk_w[t,j] * yp[inv_perm[t,j], :]
+ *            (+ y_add[t,:] when y_add != NULL, e.g. the shared experts' output)
+ * Ghost routes are skipped; a token whose routes are all ghosts gets exactly
+ * y_add[t,:] (exactly 0 when y_add == NULL).  yp [cap,d], y_add, y [T,d].
+ * Slots outside [0, cap) are treated as ghost routes (cap = rows of yp).
+ */
+int moe_combine_fwd(const void* yp, int dtype, int T, int d, int k, int cap, const float* topk_w,
+                    const int32_t* inv_perm, const void* y_add, void* y, hipStream_t stream);
+
+/*
+ * Backward of the combine:
+ *   dyp[p,:]      = topk_w[t,j] * dy[t,:]         for p = inv_perm[t,j] >= 0
+ *   d_topk_w[t,j] = <dy[t,:], yp[p,:]>  (fp32), 0 for a ghost route
+ * yp, dyp [cap,d]; slots outside [0, cap) are treated as ghost routes.
+ */
+int moe_combine_bwd(const void* dy, const void* yp, int dtype, int T, int d, int k, int cap,
+                    const float* topk_w, const int32_t* inv_perm, void* dyp, float* d_topk_w,
+                    hipStream_t stream);
+
+/*
+ * Round boundary: expert-wise pseudo-gradient of the resident experts and its
+ * average over the expert's replica group (Alg. 2, aggregation of the sparse
+ * parameters within expert replica groups; Sec. 3.4 "Round structure").
+ *   delta_local = theta_start - theta_now
+ *   delta_avg   = (((delta_local + peers[0]) + peers[1]) + ...) * (1/(n_peers+1))
+ * evaluated elementwise in fp32 in exactly that order (the reciprocal is the
+ * fp32-rounded 1/(n_peers+1)), so the result is reproducible bit for bit.
+ * peers is a HOST array of n_peers device pointers, each to n_params fp32
+ * values (the other replicas' deltas).  delta_local may be NULL.
+ * Limits: 0 <= n_peers <= 16.
+ */
+int moe_expert_delta(const float* theta_start, const float* theta_now,
+                     const float* const* peers, int n_peers, size_t n_params,
+                     float* delta_local, float* delta_avg, hipStream_t stream);
+
+/*
+ * Measurement support for benchmarks and profilers (not part of the layer).
+ * moe_timing_enable(capacity > 0) creates a pool of 2*capacity HIP events on
+ * the current device and from then on brackets every kernel this library
+ * launches with an event pair on the launch's stream (launches beyond the
+ * capacity are not recorded).  moe_timing_enable(0) stops recording and
+ * releases the pool.  moe_timing_collect() waits for the recorded events,
+ * sums the elapsed time per kernel name into out[0..*n_out) (at most max_out
+ * entries; names are static strings owned by the library) and clears the
+ * record.  Enabling is the one call that allocates (the event pool); it is
+ * process-wide and must not race with launches on other threads.
+ */
+typedef struct {
+  const char* name;
+  int launches;
+  float total_ms;
+  float min_ms;
+  float max_ms;
+} moe_kernel_time;
+int moe_timing_enable(int capacity);
+int moe_timing_collect(moe_kernel_time* out, int max_out, int* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_RESIDENT_H */

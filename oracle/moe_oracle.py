@@ -257,8 +257,7 @@ def combine_fwd(Yp, w, inv_perm, y_add=None):
     """
     Yp = _f64(Yp)
     Tn, k = inv_perm.shape
-    d = Yp.shape[1] if Yp.ndim == 2 and Yp.shape[0] else (y_add.shape[1] if y_add is not None else 0)
-    y = np.zeros((Tn, d))
+    y = np.zeros((Tn, Yp.shape[1]))
     for t in range(Tn):
         for j in range(k):
             p = inv_perm[t, j]

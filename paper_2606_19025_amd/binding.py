@@ -1,0 +1,209 @@
+"""ctypes binding of libmoe_resident.so (see include/moe_resident.h).
+
+Argument marshalling only: every function here has the name of the C entry
+point it calls, takes torch tensors (or None for NULL, or raw integer device
+addresses), passes their device pointers and sizes through unchanged and
+raises MoeError with the library's message when the status is not MOE_OK.
+No arithmetic of the layer happens in Python.  There is no fallback: if the
+native library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+from .build import LIB_PATH
+
+MOE_F32, MOE_BF16 = 0, 1
+MOE_GATE_SOFTMAX_TOPK, MOE_GATE_SOFTMAX, MOE_GATE_SIGMOID = 0, 1, 2
+GATES = {"softmax_topk": MOE_GATE_SOFTMAX_TOPK, "softmax": MOE_GATE_SOFTMAX,
+         "sigmoid": MOE_GATE_SIGMOID}
+
+EXPORTS = [
+    "moe_last_error", "moe_abi_version", "moe_route_mask", "moe_route_bwd_workspace_size",
+    "moe_route_bwd", "moe_dispatch_workspace_size", "moe_dispatch", "moe_dispatch_bwd",
+    "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_combine_fwd", "moe_combine_bwd",
+    "moe_expert_delta", "moe_timing_enable", "moe_timing_collect",
+]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} returned {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+_P = C.c_void_p
+_I = C.c_int
+_F = C.c_float
+_Z = C.c_size_t
+
+_SIGS = {
+    "moe_last_error": (C.c_char_p, []),
+    "moe_abi_version": (_I, []),
+    "moe_route_mask": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P, _P]),
+    "moe_route_bwd_workspace_size": (_Z, [_I, _I, _I]),
+    "moe_route_bwd": (_I, [_P, _P, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P, _P, _P, _P,
+                           _I, _P, _Z, _P]),
+    "moe_dispatch_workspace_size": (_Z, [_I, _I, _I]),
+    "moe_dispatch": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+    "moe_dispatch_bwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _I, _P]),
+    "moe_grouped_ffn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "moe_grouped_ffn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P,
+                                 _I, _P]),
+    "moe_combine_fwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "moe_combine_bwd": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "moe_expert_delta": (_I, [_P, _P, C.POINTER(C.c_void_p), _I, _Z, _P, _P, _P]),
+    "moe_timing_enable": (_I, [_I]),
+    "moe_timing_collect": (_I, [_P, _I, C.POINTER(C.c_int)]),
+}
+
+
+class moe_kernel_time(C.Structure):
+    _fields_ = [("name", C.c_char_p), ("launches", C.c_int), ("total_ms", C.c_float),
+                ("min_ms", C.c_float), ("max_ms", C.c_float)]
+
+
+def lib(path: str | None = None):
+    """Load the native library once (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        p = path or LIB_PATH
+        if not os.path.exists(p):
+            raise RuntimeError(f"{p} is missing: build it with __graft_entry__.build() "
+                               "or python -m paper_2606_19025_amd.build")
+        handle = C.CDLL(p)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise MoeError(fn, status, lib().moe_last_error().decode())
+    return status
+
+
+def dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype == torch.float32:
+        return MOE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def moe_last_error() -> str:
+    return lib().moe_last_error().decode()
+
+
+def moe_abi_version() -> int:
+    return lib().moe_abi_version()
+
+
+def moe_route_mask(x, w_router, router_bias, dtype, T, d, E, k, inv_tau, gate, resident, logits,
+                   topk_idx, topk_w, topk_local, stream=None):
+    return _check("moe_route_mask", lib().moe_route_mask(
+        _ptr(x), _ptr(w_router), _ptr(router_bias), dtype, T, d, E, k, inv_tau, gate,
+        _ptr(resident), _ptr(logits), _ptr(topk_idx), _ptr(topk_w), _ptr(topk_local),
+        _stream(stream)))
+
+
+def moe_route_bwd_workspace_size(T, d, E) -> int:
+    return lib().moe_route_bwd_workspace_size(T, d, E)
+
+
+def moe_route_bwd(x, w_router, dtype, T, d, E, k, inv_tau, gate, topk_idx, topk_w, logits,
+                  d_topk_w, dz, dw_router, d_bias, dx, accumulate_dx, ws, ws_bytes, stream=None):
+    return _check("moe_route_bwd", lib().moe_route_bwd(
+        _ptr(x), _ptr(w_router), dtype, T, d, E, k, inv_tau, gate, _ptr(topk_idx), _ptr(topk_w),
+        _ptr(logits), _ptr(d_topk_w), _ptr(dz), _ptr(dw_router), _ptr(d_bias), _ptr(dx),
+        accumulate_dx, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moe_dispatch_workspace_size(T, k, E_r) -> int:
+    return lib().moe_dispatch_workspace_size(T, k, E_r)
+
+
+def moe_dispatch(x, dtype, T, d, k, E_r, topk_local, counts, offsets, perm, inv_perm, xp, ws,
+                 ws_bytes, stream=None):
+    return _check("moe_dispatch", lib().moe_dispatch(
+        _ptr(x), dtype, T, d, k, E_r, _ptr(topk_local), _ptr(counts), _ptr(offsets), _ptr(perm),
+        _ptr(inv_perm), _ptr(xp), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moe_dispatch_bwd(dxp, dtype, T, d, k, cap, inv_perm, dx, accumulate, stream=None):
+    return _check("moe_dispatch_bwd", lib().moe_dispatch_bwd(
+        _ptr(dxp), dtype, T, d, k, cap, _ptr(inv_perm), _ptr(dx), accumulate, _stream(stream)))
+
+
+def moe_grouped_ffn_fwd(xp, w_gate_up, w_down, dtype, cap, d, H, n_groups, offsets, gu, h, yp,
+                        stream=None):
+    return _check("moe_grouped_ffn_fwd", lib().moe_grouped_ffn_fwd(
+        _ptr(xp), _ptr(w_gate_up), _ptr(w_down), dtype, cap, d, H, n_groups, _ptr(offsets),
+        _ptr(gu), _ptr(h), _ptr(yp), _stream(stream)))
+
+
+def moe_grouped_ffn_bwd(dyp, xp, gu, h, w_gate_up, w_down, dtype, cap, d, H, n_groups, offsets,
+                        dgu, dxp, dw_gate_up, dw_down, accumulate_dw, stream=None):
+    return _check("moe_grouped_ffn_bwd", lib().moe_grouped_ffn_bwd(
+        _ptr(dyp), _ptr(xp), _ptr(gu), _ptr(h), _ptr(w_gate_up), _ptr(w_down), dtype, cap, d, H,
+        n_groups, _ptr(offsets), _ptr(dgu), _ptr(dxp), _ptr(dw_gate_up), _ptr(dw_down),
+        accumulate_dw, _stream(stream)))
+
+
+def moe_combine_fwd(yp, dtype, T, d, k, cap, topk_w, inv_perm, y_add, y, stream=None):
+    return _check("moe_combine_fwd", lib().moe_combine_fwd(
+        _ptr(yp), dtype, T, d, k, cap, _ptr(topk_w), _ptr(inv_perm), _ptr(y_add), _ptr(y),
+        _stream(stream)))
+
+
+def moe_combine_bwd(dy, yp, dtype, T, d, k, cap, topk_w, inv_perm, dyp, d_topk_w, stream=None):
+    return _check("moe_combine_bwd", lib().moe_combine_bwd(
+        _ptr(dy), _ptr(yp), dtype, T, d, k, cap, _ptr(topk_w), _ptr(inv_perm), _ptr(dyp),
+        _ptr(d_topk_w), _stream(stream)))
+
+
+def moe_expert_delta(theta_start, theta_now, peers, n_peers, n_params, delta_local, delta_avg,
+                     stream=None):
+    arr = (C.c_void_p * max(1, n_peers))(*[_ptr(p) for p in (peers or [])][:n_peers]) \
+        if n_peers else None
+    return _check("moe_expert_delta", lib().moe_expert_delta(
+        _ptr(theta_start), _ptr(theta_now), arr, n_peers, n_params, _ptr(delta_local),
+        _ptr(delta_avg), _stream(stream)))
+
+
+def moe_timing_enable(capacity):
+    return _check("moe_timing_enable", lib().moe_timing_enable(capacity))
+
+
+def moe_timing_collect(max_out=64):
+    """{kernel name: (launches, total_ms, min_ms, max_ms)} of the recorded launches."""
+    arr = (moe_kernel_time * max_out)()
+    n = C.c_int(0)
+    _check("moe_timing_collect", lib().moe_timing_collect(C.cast(arr, C.c_void_p), max_out,
+                                                          C.byref(n)))
+    return {arr[i].name.decode(): (arr[i].launches, arr[i].total_ms, arr[i].min_ms, arr[i].max_ms)
+            for i in range(n.value)}

@@ -1,0 +1,350 @@
+// C ABI of the resident-expert MoE layer: argument validation on the host,
+// then the kernel launchers.  Declarations and contracts: moe_resident.h.
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "moe_resident.h"
+#include "timing.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return MOE_OK;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE(cond, ...) \
+  do {                     \
+    if (!(cond)) return fail(MOE_ERR_ARG, __VA_ARGS__); \
+  } while (0)
+#define SUPPORT(cond, ...) \
+  do {                     \
+    if (!(cond)) return fail(MOE_ERR_UNSUPPORTED, __VA_ARGS__); \
+  } while (0)
+
+int check_dtype(int dtype) {
+  SUPPORT(dtype == MOE_F32 || dtype == MOE_BF16, "unsupported dtype %d", dtype);
+  return MOE_OK;
+}
+
+// row vectors of 16 bytes: d % 8 == 0 and 16-byte aligned base pointers
+int check_rows16(int d, const char* name, const void* p) {
+  SUPPORT(d % 8 == 0, "d = %d must be a multiple of 8", d);
+  SUPPORT(p == nullptr || aligned16(p), "%s must be 16-byte aligned", name);
+  return MOE_OK;
+}
+
+// ---------------------------------------------------------------- timing pool
+std::mutex g_tmu;
+std::atomic<bool> g_ton{false};
+std::vector<hipEvent_t> g_pool;
+struct TimingRec {
+  const char* name;
+  int ev;
+};
+std::vector<TimingRec> g_recs;
+int g_next = 0;
+thread_local int t_open = -1;
+
+void release_pool() {
+  for (hipEvent_t e : g_pool) (void)hipEventDestroy(e);
+  g_pool.clear();
+  g_recs.clear();
+  g_next = 0;
+}
+
+}  // namespace
+
+namespace moe {
+bool timing_on() { return g_ton.load(std::memory_order_relaxed); }
+
+void timing_begin(const char* name, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_tmu);
+  t_open = -1;
+  if (g_next + 2 > (int)g_pool.size()) return;
+  const int ev = g_next;
+  g_next += 2;
+  if (hipEventRecord(g_pool[ev], s) != hipSuccess) return;
+  g_recs.push_back({name, ev});
+  t_open = ev;
+}
+
+void timing_end(hipStream_t s) {
+  if (t_open < 0) return;
+  std::lock_guard<std::mutex> lock(g_tmu);
+  (void)hipEventRecord(g_pool[t_open + 1], s);
+  t_open = -1;
+}
+}  // namespace moe
+
+extern "C" {
+
+int moe_timing_enable(int capacity) {
+  REQUIRE(capacity >= 0, "capacity = %d must be >= 0", capacity);
+  std::lock_guard<std::mutex> lock(g_tmu);
+  g_ton.store(false);
+  release_pool();
+  if (capacity == 0) return ok();
+  g_pool.resize(2 * (size_t)capacity);
+  for (auto& e : g_pool) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+      release_pool();
+      return fail(MOE_ERR_HIP, "hipEventCreate failed");
+    }
+  }
+  g_recs.reserve(capacity);
+  g_ton.store(true);
+  return ok();
+}
+
+int moe_timing_collect(moe_kernel_time* out, int max_out, int* n_out) {
+  REQUIRE(out && n_out && max_out >= 0, "out and n_out must not be NULL");
+  std::lock_guard<std::mutex> lock(g_tmu);
+  int n = 0;
+  for (const TimingRec& r : g_recs) {
+    hipError_t e = hipEventSynchronize(g_pool[r.ev + 1]);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, g_pool[r.ev], g_pool[r.ev + 1]);
+    if (e != hipSuccess) {
+      g_recs.clear();
+      g_next = 0;
+      return fail(MOE_ERR_HIP, "timing: %s", hipGetErrorString(e));
+    }
+    int i = 0;
+    while (i < n && std::strcmp(out[i].name, r.name) != 0) ++i;
+    if (i == n) {
+      if (n == max_out) continue;
+      out[n++] = moe_kernel_time{r.name, 0, 0.f, 1e30f, 0.f};
+    }
+    out[i].launches += 1;
+    out[i].total_ms += ms;
+    out[i].min_ms = std::min(out[i].min_ms, ms);
+    out[i].max_ms = std::max(out[i].max_ms, ms);
+  }
+  g_recs.clear();
+  g_next = 0;
+  *n_out = n;
+  return ok();
+}
+
+const char* moe_last_error(void) { return g_err.c_str(); }
+
+int moe_abi_version(void) { return 1; }
+
+int moe_route_mask(const void* x, const void* w_router, const float* router_bias, int dtype,
+                   int T, int d, int E, int k, float inv_tau, int gate,
+                   const uint8_t* resident, float* logits, int32_t* topk_idx, float* topk_w,
+                   int32_t* topk_local, hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0, "T = %d must be >= 0", T);
+  REQUIRE(d >= 1, "d = %d must be >= 1", d);
+  REQUIRE(E >= 1 && E <= 256, "E = %d must be in [1, 256]", E);
+  REQUIRE(k >= 1 && k <= E, "k = %d must be in [1, E = %d]", k, E);
+  REQUIRE(gate >= MOE_GATE_SOFTMAX_TOPK && gate <= MOE_GATE_SIGMOID, "unknown gate %d", gate);
+  REQUIRE(std::isfinite(inv_tau) && inv_tau > 0.f, "inv_tau must be finite and > 0");
+  REQUIRE(w_router && resident, "w_router and resident must not be NULL");
+  REQUIRE(T == 0 || (x && topk_idx && topk_w && topk_local), "x and the top-k outputs must not be NULL");
+  if (dtype == MOE_BF16) {
+    if ((r = check_rows16(d, "x", x)) != MOE_OK) return r;
+    if ((r = check_rows16(d, "w_router", w_router)) != MOE_OK) return r;
+  }
+  return hip_status(moe::launch_route_fwd(x, w_router, router_bias, dtype == MOE_BF16, T, d, E, k,
+                                          inv_tau, gate, resident, logits, topk_idx, topk_w,
+                                          topk_local, stream),
+                    "moe_route_mask");
+}
+
+size_t moe_route_bwd_workspace_size(int T, int d, int E) {
+  if (T < 0 || d < 1 || E < 1) return 0;
+  return moe::route_bwd_ws_bytes(T, d, E);
+}
+
+int moe_route_bwd(const void* x, const void* w_router, int dtype, int T, int d, int E, int k,
+                  float inv_tau, int gate, const int32_t* topk_idx, const float* topk_w,
+                  const float* logits, const float* d_topk_w, float* dz, float* dw_router,
+                  float* d_bias, void* dx, int accumulate_dx, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1, "bad sizes T = %d, d = %d", T, d);
+  REQUIRE(E >= 1 && E <= 256, "E = %d must be in [1, 256]", E);
+  REQUIRE(k >= 1 && k <= E, "k = %d must be in [1, E = %d]", k, E);
+  REQUIRE(gate >= MOE_GATE_SOFTMAX_TOPK && gate <= MOE_GATE_SIGMOID, "unknown gate %d", gate);
+  REQUIRE(std::isfinite(inv_tau) && inv_tau > 0.f, "inv_tau must be finite and > 0");
+  REQUIRE(w_router && dw_router, "w_router and dw_router must not be NULL");
+  REQUIRE(T == 0 || (x && topk_idx && topk_w && d_topk_w && dz && dx),
+          "x, topk_idx, topk_w, d_topk_w, dz and dx must not be NULL");
+  REQUIRE(gate != MOE_GATE_SOFTMAX || T == 0 || logits, "logits are required for MOE_GATE_SOFTMAX");
+  const size_t need = moe::route_bwd_ws_bytes(T, d, E);
+  REQUIRE(ws && ws_bytes >= need, "workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+  if ((r = check_rows16(d, "dx", dx)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "w_router", w_router)) != MOE_OK) return r;
+  return hip_status(moe::launch_route_bwd(x, w_router, dtype == MOE_BF16, T, d, E, k, inv_tau, gate,
+                                          topk_idx, topk_w, logits, d_topk_w, dz, dw_router,
+                                          d_bias, dx, accumulate_dx, ws, stream),
+                    "moe_route_bwd");
+}
+
+size_t moe_dispatch_workspace_size(int T, int k, int E_r) {
+  if (T < 0 || k < 1 || E_r < 0) return 0;
+  return moe::dispatch_ws_bytes(T, k, E_r);
+}
+
+int moe_dispatch(const void* x, int dtype, int T, int d, int k, int E_r,
+                 const int32_t* topk_local, int32_t* counts, int32_t* offsets, int32_t* perm,
+                 int32_t* inv_perm, void* xp, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1 && k >= 1, "bad sizes T = %d, d = %d, k = %d", T, d, k);
+  REQUIRE(E_r >= 0 && E_r <= 256, "E_r = %d must be in [0, 256]", E_r);
+  REQUIRE(offsets && (E_r == 0 || counts), "counts and offsets must not be NULL");
+  REQUIRE(T == 0 || (x && topk_local && inv_perm && (E_r == 0 || (perm && xp))),
+          "x, topk_local, perm, inv_perm and xp must not be NULL");
+  const size_t need = moe::dispatch_ws_bytes(T, k, E_r);
+  REQUIRE(ws && ws_bytes >= need, "workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+  if ((r = check_rows16(d, "x", x)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "xp", xp)) != MOE_OK) return r;
+  return hip_status(moe::launch_dispatch(x, dtype == MOE_BF16, T, d, k, E_r, topk_local, counts,
+                                         offsets, perm, inv_perm, xp, ws, stream),
+                    "moe_dispatch");
+}
+
+int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
+                     const int32_t* inv_perm, void* dx, int accumulate, hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1 && k >= 1 && cap >= 0, "bad sizes T = %d, d = %d, k = %d, cap = %d",
+          T, d, k, cap);
+  REQUIRE(T == 0 || (inv_perm && dx && dxp), "dxp, inv_perm and dx must not be NULL");
+  if ((r = check_rows16(d, "dxp", dxp)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "dx", dx)) != MOE_OK) return r;
+  return hip_status(moe::launch_dispatch_bwd(dxp, dtype == MOE_BF16, T, d, k, cap, inv_perm, dx,
+                                             accumulate, stream),
+                    "moe_dispatch_bwd");
+}
+
+static int check_ffn(int dtype, int cap, int d, int H, int n_groups, const int32_t* offsets) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(cap >= 0 && d >= 1 && H >= 1, "bad sizes cap = %d, d = %d, H = %d", cap, d, H);
+  REQUIRE(n_groups >= 0, "n_groups = %d must be >= 0", n_groups);
+  REQUIRE(offsets, "offsets must not be NULL");
+  SUPPORT(H % 64 == 0, "H = %d must be a multiple of 64", H);
+  if (dtype == MOE_BF16) SUPPORT(d % 64 == 0, "d = %d must be a multiple of 64 for bf16", d);
+  else SUPPORT(d % 8 == 0, "d = %d must be a multiple of 8", d);
+  return MOE_OK;
+}
+
+int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_down, int dtype,
+                        int cap, int d, int H, int n_groups, const int32_t* offsets, void* gu,
+                        void* h, void* yp, hipStream_t stream) {
+  int r;
+  if ((r = check_ffn(dtype, cap, d, H, n_groups, offsets)) != MOE_OK) return r;
+  REQUIRE(n_groups == 0 || (w_gate_up && w_down), "expert weights must not be NULL");
+  REQUIRE(cap == 0 || (xp && gu && h && yp), "xp, gu, h and yp must not be NULL");
+  for (const void* p : {xp, w_gate_up, w_down, (const void*)gu, (const void*)h, (const void*)yp})
+    SUPPORT(p == nullptr || aligned16(p), "operands must be 16-byte aligned");
+  return hip_status(moe::launch_ffn_fwd(xp, w_gate_up, w_down, dtype == MOE_BF16, cap, d, H,
+                                        n_groups, offsets, gu, h, yp, stream),
+                    "moe_grouped_ffn_fwd");
+}
+
+int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
+                        const void* w_gate_up, const void* w_down, int dtype, int cap, int d,
+                        int H, int n_groups, const int32_t* offsets, void* dgu, void* dxp,
+                        float* dw_gate_up, float* dw_down, int accumulate_dw,
+                        hipStream_t stream) {
+  int r;
+  if ((r = check_ffn(dtype, cap, d, H, n_groups, offsets)) != MOE_OK) return r;
+  REQUIRE(n_groups == 0 || (w_gate_up && w_down && dw_gate_up && dw_down),
+          "expert weights and their gradients must not be NULL");
+  REQUIRE(cap == 0 || (dyp && xp && gu && h && dgu && dxp),
+          "dyp, xp, gu, h, dgu and dxp must not be NULL");
+  for (const void* p : {dyp, xp, gu, h, w_gate_up, w_down, (const void*)dgu, (const void*)dxp})
+    SUPPORT(p == nullptr || aligned16(p), "operands must be 16-byte aligned");
+  return hip_status(moe::launch_ffn_bwd(dyp, xp, gu, h, w_gate_up, w_down, dtype == MOE_BF16, cap,
+                                        d, H, n_groups, offsets, dgu, dxp, dw_gate_up, dw_down,
+                                        accumulate_dw, stream),
+                    "moe_grouped_ffn_bwd");
+}
+
+int moe_combine_fwd(const void* yp, int dtype, int T, int d, int k, int cap, const float* topk_w,
+                    const int32_t* inv_perm, const void* y_add, void* y, hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1 && k >= 1 && cap >= 0, "bad sizes T = %d, d = %d, k = %d, cap = %d",
+          T, d, k, cap);
+  REQUIRE(T == 0 || (topk_w && inv_perm && y), "topk_w, inv_perm and y must not be NULL");
+  if ((r = check_rows16(d, "yp", yp)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "y_add", y_add)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "y", y)) != MOE_OK) return r;
+  return hip_status(moe::launch_combine_fwd(yp, dtype == MOE_BF16, T, d, k, cap, topk_w, inv_perm,
+                                            y_add, y, stream),
+                    "moe_combine_fwd");
+}
+
+int moe_combine_bwd(const void* dy, const void* yp, int dtype, int T, int d, int k, int cap,
+                    const float* topk_w, const int32_t* inv_perm, void* dyp, float* d_topk_w,
+                    hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1 && k >= 1 && cap >= 0, "bad sizes T = %d, d = %d, k = %d, cap = %d",
+          T, d, k, cap);
+  REQUIRE(T == 0 || (dy && topk_w && inv_perm && d_topk_w), "dy, topk_w, inv_perm and d_topk_w must not be NULL");
+  if ((r = check_rows16(d, "dy", dy)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "yp", yp)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "dyp", dyp)) != MOE_OK) return r;
+  return hip_status(moe::launch_combine_bwd(dy, yp, dtype == MOE_BF16, T, d, k, cap, topk_w,
+                                            inv_perm, dyp, d_topk_w, stream),
+                    "moe_combine_bwd");
+}
+
+int moe_expert_delta(const float* theta_start, const float* theta_now,
+                     const float* const* peers, int n_peers, size_t n_params, float* delta_local,
+                     float* delta_avg, hipStream_t stream) {
+  REQUIRE(n_peers >= 0 && n_peers <= moe::kMaxPeers, "n_peers = %d must be in [0, %d]", n_peers,
+          moe::kMaxPeers);
+  REQUIRE(n_params == 0 || (theta_start && theta_now && delta_avg),
+          "theta_start, theta_now and delta_avg must not be NULL");
+  REQUIRE(n_peers == 0 || peers, "peers must not be NULL when n_peers > 0");
+  for (int p = 0; p < n_peers; ++p) {
+    REQUIRE(n_params == 0 || peers[p], "peers[%d] must not be NULL", p);
+    SUPPORT(peers[p] == nullptr || aligned16(peers[p]), "peers[%d] must be 16-byte aligned", p);
+  }
+  for (const void* p : {(const void*)theta_start, (const void*)theta_now, (const void*)delta_local,
+                        (const void*)delta_avg})
+    SUPPORT(p == nullptr || aligned16(p), "arrays must be 16-byte aligned");
+  return hip_status(moe::launch_expert_delta(theta_start, theta_now, peers, n_peers, n_params,
+                                             delta_local, delta_avg, stream),
+                    "moe_expert_delta");
+}
+
+}  // extern "C"

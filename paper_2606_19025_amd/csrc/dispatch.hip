@@ -1,0 +1,376 @@
+// Dispatch of the resident routes, its backward, the weighted combine and its
+// backward.
+//
+// Routing is strictly local (Sec. 3.3.2 "System context and routing logic"):
+// a route is either executed by one of the worker's resident experts or, for a
+// ghost expert, skipped (Sec. 3.3 "Ghost Experts and Skip-Token").  The
+// dispatch is a stable counting sort of the routes by local expert id:
+//   1. per 256-token block, an LDS histogram of local ids;
+//   2. one block scans the histograms (expert-major, then block) into the
+//      global offsets and per-block bases;
+//   3. per block, an LDS bitmap [expert][token] gives every route its rank
+//      among earlier tokens of the same expert (popcount), hence its slot;
+//   4. the rows are gathered token-major: each wave reads a token row once and
+//      writes it to every slot of that token (16-byte vector accesses).
+// Combine, combine backward and un-permute are token-major too: one wave per
+// token, 16-byte loads of the routed rows, fp32 accumulation.
+#include "common.h"
+#include "kernels.h"
+#include "timing.h"
+
+namespace moe {
+namespace {
+
+constexpr int DB = 256;  // tokens per block of the counting sort
+
+__global__ __launch_bounds__(DB) void dispatch_count_kernel(const int32_t* local, int T, int k,
+                                                            int E_r, int32_t* blk_counts) {
+  __shared__ int hist[256];
+  for (int r = threadIdx.x; r < E_r; r += DB) hist[r] = 0;
+  __syncthreads();
+  const int t = blockIdx.x * DB + threadIdx.x;
+  if (t < T) {
+    for (int j = 0; j < k; ++j) {
+      const int r = local[(size_t)t * k + j];
+      if (r >= 0 && r < E_r) atomicAdd(&hist[r], 1);
+    }
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < E_r; r += DB) blk_counts[(size_t)blockIdx.x * E_r + r] = hist[r];
+}
+
+// One block: counts, offsets and blk_base[b][r] = offsets[r] + sum_{b'<b} cnt[b'][r].
+__global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* blk_counts, int nblk,
+                                                           int E_r, int32_t* blk_base,
+                                                           int32_t* counts, int32_t* offsets) {
+  __shared__ int tot[257];
+  const int r = threadIdx.x;
+  int run = 0;
+  if (r < E_r) {
+    for (int b = 0; b < nblk; ++b) {
+      blk_base[(size_t)b * E_r + r] = run;
+      run += blk_counts[(size_t)b * E_r + r];
+    }
+    counts[r] = run;
+  }
+  tot[r] = (r < E_r) ? run : 0;
+  __syncthreads();
+  if (r == 0) {  // exclusive scan over at most 256 experts, in order
+    int s = 0;
+    for (int i = 0; i < E_r; ++i) { const int c = tot[i]; tot[i] = s; s += c; }
+    tot[256] = s;
+  }
+  __syncthreads();
+  if (r < E_r) {
+    const int base = tot[r];
+    offsets[r] = base;
+    for (int b = 0; b < nblk; ++b) blk_base[(size_t)b * E_r + r] += base;
+  }
+  if (r == 0) offsets[E_r] = tot[256];
+}
+
+__global__ __launch_bounds__(DB) void dispatch_scatter_kernel(const int32_t* local, int T, int k,
+                                                              int E_r, int cap,
+                                                              const int32_t* blk_base,
+                                                              int32_t* perm, int32_t* inv_perm) {
+  __shared__ uint32_t bits[256][DB / 32];
+  for (int i = threadIdx.x; i < E_r * (DB / 32); i += DB) bits[i / (DB / 32)][i % (DB / 32)] = 0;
+  __syncthreads();
+  const int t = blockIdx.x * DB + threadIdx.x;
+  const int word = threadIdx.x >> 5, bit = threadIdx.x & 31;
+  if (t < T) {
+    for (int j = 0; j < k; ++j) {
+      const int r = local[(size_t)t * k + j];
+      if (r >= 0 && r < E_r) atomicOr(&bits[r][word], 1u << bit);
+    }
+  }
+  __syncthreads();
+  if (t < T) {
+    for (int j = 0; j < k; ++j) {
+      const int r = local[(size_t)t * k + j];
+      const size_t o = (size_t)t * k + j;
+      if (r >= 0 && r < E_r) {
+        int rank = __popc(bits[r][word] & ((1u << bit) - 1u));
+        for (int w = 0; w < word; ++w) rank += __popc(bits[r][w]);
+        const int p = blk_base[(size_t)blockIdx.x * E_r + r] + rank;
+        // p < cap whenever a token's routes name distinct experts; anything
+        // else is malformed input and its extra routes are dropped
+        if (p < cap) perm[p] = (int32_t)o;
+        inv_perm[o] = p < cap ? p : -1;
+      } else {
+        inv_perm[o] = -1;
+      }
+    }
+  }
+}
+
+// Slot of route (t, j) (o = t*k): lanes j < k read inv_perm and broadcast;
+// slots outside [0, cap) count as ghost routes.
+DEVI int slot_of(const int32_t* inv_perm, size_t o, int j, int k, int cap) {
+  const int lane = threadIdx.x & 63;
+  int p;
+  if (k <= 64) {
+    const int mine = (lane < k) ? inv_perm[o + lane] : -1;
+    p = __shfl(mine, j & 63, 64);
+  } else {
+    p = inv_perm[o + j];
+  }
+  return (p >= 0 && p < cap) ? p : -1;
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void gather_rows_kernel(const T* x, int T_, int d, int k, int cap,
+                                                          const int32_t* inv_perm, T* xp) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  int slots[8];
+  int ns = 0;
+  for (int j = 0; j < k; ++j) {
+    const int p = slot_of(inv_perm, o, j, k, cap);
+    if (p >= 0) {
+      if (ns < 8) slots[ns++] = p;
+      else {  // more than 8 resident routes: copy this one directly
+        for (int c = lane * V; c < d; c += 64 * V)
+          *reinterpret_cast<u32x4_t*>(xp + (size_t)p * d + c) =
+              *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
+      }
+    }
+  }
+  if (ns == 0) return;
+  for (int c = lane * V; c < d; c += 64 * V) {
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
+    for (int s = 0; s < ns; ++s) *reinterpret_cast<u32x4_t*>(xp + (size_t)slots[s] * d + c) = v;
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void unpermute_kernel(const T* dxp, int T_, int d, int k, int cap,
+                                                        const int32_t* inv_perm, T* dx,
+                                                        int accumulate) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  // the column loop runs the same number of times in every lane, so the slot
+  // broadcasts (cross-lane) always read active lanes
+  for (int c0 = 0; c0 < d; c0 += 64 * V) {
+    const int c = c0 + lane * V;
+    const bool act = c < d;
+    float acc[V];
+#pragma unroll
+    for (int u = 0; u < V; ++u) acc[u] = 0.f;
+    if (accumulate && act) load16_f32(dx + (size_t)t * d + c, acc);
+    for (int j = 0; j < k; ++j) {
+      const int p = slot_of(inv_perm, o, j, k, cap);
+      if (p < 0 || !act) continue;
+      float v[V];
+      load16_f32(dxp + (size_t)p * d + c, v);
+#pragma unroll
+      for (int u = 0; u < V; ++u) acc[u] += v[u];
+    }
+    if (act) store16_f32(dx + (size_t)t * d + c, acc);
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void combine_fwd_kernel(const T* yp, int T_, int d, int k, int cap,
+                                                          const float* tw,
+                                                          const int32_t* inv_perm,
+                                                          const T* y_add, T* y) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  for (int c0 = 0; c0 < d; c0 += 64 * V) {  // same trip count in every lane
+    const int c = c0 + lane * V;
+    const bool act = c < d;
+    float acc[V];
+#pragma unroll
+    for (int u = 0; u < V; ++u) acc[u] = 0.f;
+    for (int j = 0; j < k; ++j) {
+      const int p = slot_of(inv_perm, o, j, k, cap);
+      if (p < 0 || !act) continue;  // ghost route: skipped
+      const float wj = tw[o + j];
+      float v[V];
+      load16_f32(yp + (size_t)p * d + c, v);
+#pragma unroll
+      for (int u = 0; u < V; ++u) acc[u] = fmaf(wj, v[u], acc[u]);
+    }
+    if (!act) continue;
+    if (y_add) {
+      float v[V];
+      load16_f32(y_add + (size_t)t * d + c, v);
+#pragma unroll
+      for (int u = 0; u < V; ++u) acc[u] += v[u];
+    }
+    store16_f32(y + (size_t)t * d + c, acc);
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void combine_bwd_kernel(const T* dy, const T* yp, int T_, int d,
+                                                          int k, int cap, const float* tw,
+                                                          const int32_t* inv_perm, T* dyp,
+                                                          float* dtw) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  for (int j = 0; j < k; ++j) {
+    const int p = slot_of(inv_perm, o, j, k, cap);
+    if (p < 0) {  // ghost route: no gradient
+      if (lane == 0) dtw[o + j] = 0.f;
+      continue;
+    }
+    const float wj = tw[o + j];
+    float dot = 0.f;
+    for (int c = lane * V; c < d; c += 64 * V) {
+      float g[V], v[V], out[V];
+      load16_f32(dy + (size_t)t * d + c, g);
+      load16_f32(yp + (size_t)p * d + c, v);
+#pragma unroll
+      for (int u = 0; u < V; ++u) {
+        dot = fmaf(g[u], v[u], dot);
+        out[u] = wj * g[u];
+      }
+      store16_f32(dyp + (size_t)p * d + c, out);
+    }
+    dot = wave_sum(dot);
+    if (lane == 0) dtw[o + j] = dot;
+  }
+}
+
+struct DeltaArgs {
+  const float* start;
+  const float* now;
+  const float* peers[kMaxPeers];
+  float* dl;
+  float* avg;
+  size_t n;
+  int n_peers;
+  float scale;
+};
+
+__global__ __launch_bounds__(256) void expert_delta_kernel(DeltaArgs a) {
+  const size_t n4 = a.n / 4;
+  const size_t stride = (size_t)gridDim.x * 256;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
+    const f32x4_t s = reinterpret_cast<const f32x4_t*>(a.start)[i];
+    const f32x4_t w = reinterpret_cast<const f32x4_t*>(a.now)[i];
+    const f32x4_t dl = s - w;
+    f32x4_t acc = dl;
+    for (int p = 0; p < a.n_peers; ++p) acc = acc + reinterpret_cast<const f32x4_t*>(a.peers[p])[i];
+    if (a.dl) reinterpret_cast<f32x4_t*>(a.dl)[i] = dl;
+    reinterpret_cast<f32x4_t*>(a.avg)[i] = acc * a.scale;
+  }
+  // scalar tail
+  for (size_t i = n4 * 4 + (size_t)blockIdx.x * 256 + threadIdx.x; i < a.n; i += stride) {
+    const float dl = a.start[i] - a.now[i];
+    float acc = dl;
+    for (int p = 0; p < a.n_peers; ++p) acc = acc + a.peers[p][i];
+    if (a.dl) a.dl[i] = dl;
+    a.avg[i] = acc * a.scale;
+  }
+}
+
+}  // namespace
+
+size_t dispatch_ws_bytes(int T, int k, int E_r) {
+  (void)k;
+  const size_t nblk = (size_t)(T + DB - 1) / DB;
+  return 2 * nblk * (size_t)std::max(E_r, 1) * sizeof(int32_t) + 256;
+}
+
+hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r,
+                           const int32_t* local, int32_t* counts, int32_t* offsets,
+                           int32_t* perm, int32_t* inv_perm, void* xp, void* ws, hipStream_t s) {
+  const int nblk = ceil_div(T, DB);
+  const int cap = T * std::min(k, E_r);
+  int32_t* blk_counts = static_cast<int32_t*>(ws);
+  int32_t* blk_base = blk_counts + (size_t)nblk * std::max(E_r, 1);
+  if (nblk > 0 && E_r > 0)
+    MOE_TIMED("dispatch_count", s, dispatch_count_kernel<<<nblk, DB, 0, s>>>(local, T, k, E_r, blk_counts));
+  MOE_TIMED("dispatch_scan", s,
+            dispatch_scan_kernel<<<1, 256, 0, s>>>(blk_counts, E_r > 0 ? nblk : 0, E_r, blk_base,
+                                                   counts, offsets));
+  if (nblk > 0) {
+    MOE_TIMED("dispatch_scatter", s,
+              dispatch_scatter_kernel<<<nblk, DB, 0, s>>>(local, T, k, E_r, cap, blk_base, perm,
+                                                          inv_perm));
+    if (bf16)
+      MOE_TIMED("dispatch_gather", s, gather_rows_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
+          static_cast<const bf16_t*>(x), T, d, k, cap, inv_perm, static_cast<bf16_t*>(xp)));
+    else
+      MOE_TIMED("dispatch_gather", s, gather_rows_kernel<float><<<ceil_div(T, 4), 256, 0, s>>>(
+          static_cast<const float*>(x), T, d, k, cap, inv_perm, static_cast<float*>(xp)));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dispatch_bwd(const void* dxp, int bf16, int T, int d, int k, int cap,
+                               const int32_t* inv_perm, void* dx, int accumulate, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (bf16)
+    MOE_TIMED("unpermute", s, unpermute_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const bf16_t*>(dxp), T, d, k, cap, inv_perm, static_cast<bf16_t*>(dx), accumulate));
+  else
+    MOE_TIMED("unpermute", s, unpermute_kernel<float><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const float*>(dxp), T, d, k, cap, inv_perm, static_cast<float*>(dx), accumulate));
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_fwd(const void* yp, int bf16, int T, int d, int k, int cap,
+                              const float* tw, const int32_t* inv_perm, const void* y_add, void* y,
+                              hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (bf16)
+    MOE_TIMED("combine_fwd", s, combine_fwd_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const bf16_t*>(yp), T, d, k, cap, tw, inv_perm, static_cast<const bf16_t*>(y_add),
+        static_cast<bf16_t*>(y)));
+  else
+    MOE_TIMED("combine_fwd", s, combine_fwd_kernel<float><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const float*>(yp), T, d, k, cap, tw, inv_perm, static_cast<const float*>(y_add),
+        static_cast<float*>(y)));
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, int d, int k,
+                              int cap, const float* tw, const int32_t* inv_perm, void* dyp,
+                              float* dtw, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (bf16)
+    MOE_TIMED("combine_bwd", s, combine_bwd_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const bf16_t*>(dy), static_cast<const bf16_t*>(yp), T, d, k, cap, tw, inv_perm,
+        static_cast<bf16_t*>(dyp), dtw));
+  else
+    MOE_TIMED("combine_bwd", s, combine_bwd_kernel<float><<<ceil_div(T, 4), 256, 0, s>>>(
+        static_cast<const float*>(dy), static_cast<const float*>(yp), T, d, k, cap, tw, inv_perm,
+        static_cast<float*>(dyp), dtw));
+  return hipGetLastError();
+}
+
+hipError_t launch_expert_delta(const float* start, const float* now, const float* const* peers,
+                               int n_peers, size_t n, float* dl, float* avg, hipStream_t s) {
+  DeltaArgs a{};
+  a.start = start;
+  a.now = now;
+  for (int p = 0; p < n_peers; ++p) a.peers[p] = peers[p];
+  a.dl = dl;
+  a.avg = avg;
+  a.n = n;
+  a.n_peers = n_peers;
+  a.scale = 1.0f / (float)(n_peers + 1);
+  if (n == 0) return hipSuccess;
+  const size_t want = (n / 4 + 255) / 256;
+  const int blocks = (int)std::max<size_t>(1, std::min<size_t>(want, 8192));
+  MOE_TIMED("expert_delta", s, expert_delta_kernel<<<blocks, 256, 0, s>>>(a));
+  return hipGetLastError();
+}
+
+}  // namespace moe

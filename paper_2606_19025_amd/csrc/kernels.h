@@ -1,0 +1,49 @@
+// Host-side launchers of the gfx950 kernels (internal; the public ABI is in
+// include/moe_resident.h).  Each launcher assumes validated arguments and
+// only enqueues work on `stream`; it returns hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int bf16, int T,
+                            int d, int E, int k, float inv_tau, int gate, const uint8_t* resident,
+                            float* logits, int32_t* idx, float* tw, int32_t* local,
+                            hipStream_t s);
+
+size_t route_bwd_ws_bytes(int T, int d, int E);
+hipError_t launch_route_bwd(const void* x, const void* w, int bf16, int T, int d, int E, int k,
+                            float inv_tau, int gate, const int32_t* idx, const float* tw,
+                            const float* logits, const float* dtw, float* dz, float* dw_router,
+                            float* d_bias, void* dx, int accumulate_dx, void* ws,
+                            hipStream_t s);
+
+size_t dispatch_ws_bytes(int T, int k, int E_r);
+hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r,
+                           const int32_t* local, int32_t* counts, int32_t* offsets,
+                           int32_t* perm, int32_t* inv_perm, void* xp, void* ws, hipStream_t s);
+hipError_t launch_dispatch_bwd(const void* dxp, int bf16, int T, int d, int k, int cap,
+                               const int32_t* inv_perm, void* dx, int accumulate, hipStream_t s);
+
+hipError_t launch_combine_fwd(const void* yp, int bf16, int T, int d, int k, int cap,
+                              const float* tw, const int32_t* inv_perm, const void* y_add, void* y,
+                              hipStream_t s);
+hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, int d, int k,
+                              int cap, const float* tw, const int32_t* inv_perm, void* dyp,
+                              float* dtw, hipStream_t s);
+
+hipError_t launch_ffn_fwd(const void* xp, const void* wgu, const void* wd, int bf16, int cap,
+                          int d, int H, int n_groups, const int32_t* offsets, void* gu, void* h,
+                          void* yp, hipStream_t s);
+hipError_t launch_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
+                          const void* wgu, const void* wd, int bf16, int cap, int d, int H,
+                          int n_groups, const int32_t* offsets, void* dgu, void* dxp,
+                          float* dwgu, float* dwd, int accumulate_dw, hipStream_t s);
+
+constexpr int kMaxPeers = 16;
+hipError_t launch_expert_delta(const float* start, const float* now, const float* const* peers,
+                               int n_peers, size_t n, float* dl, float* avg, hipStream_t s);
+
+}  // namespace moe

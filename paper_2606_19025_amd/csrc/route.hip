@@ -1,0 +1,445 @@
+// Router: logits over all E experts, top-k, gate weights, ghost-expert mask,
+// and the router backward.
+//
+// Forward (App. A: TopK of the router scores; Sec. 3.3: the router stays
+// unpartitioned under skip-token, routes to non-resident experts are masked):
+//   one block = 32 tokens, 4 waves.  bf16 logits use v_mfma_f32_32x32x16_bf16
+//   (tokens x experts tiles, the d reduction split over the 4 waves and summed
+//   in a fixed order through LDS); fp32 logits use plain FMA loops.  Each wave
+//   then takes tokens one at a time, lane = expert, and finds the top-k by k
+//   wave-wide (max logit, min id) reductions.
+#include "common.h"
+#include "kernels.h"
+#include "timing.h"
+
+namespace moe {
+namespace {
+
+constexpr int RT_TOK = 32;   // tokens per block
+constexpr int RT_THREADS = 256;
+
+struct RouteFwdArgs {
+  const void* x;
+  const void* w;
+  const float* bias;
+  const uint8_t* resident;
+  float* logits;
+  int32_t* idx;
+  float* tw;
+  int32_t* local;
+  int T, d, E, k, gate;
+  float inv_tau;
+};
+
+// Wave-wide (value desc, id asc) argmax.
+DEVI void wave_argmax(float& v, int& e) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov = __shfl_xor(v, o, 64);
+    int oe = __shfl_xor(e, o, 64);
+    if (ov > v || (ov == v && oe < e)) { v = ov; e = oe; }
+  }
+}
+
+// Local id (rank among resident experts, -1 for ghosts) of every expert, via
+// ballots over chunks of 64 experts.  Executed by wave 0.
+DEVI void build_local_map(const uint8_t* resident, int E, int* lmap) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    const bool r = (e < E) && resident[e] != 0;
+    const uint64_t m = __ballot(r);
+    const int below = __popcll(m & ((1ull << lane) - 1ull));
+    if (e < E) lmap[e] = r ? base + below : -1;
+    base += __popcll(m);
+  }
+}
+
+// bf16 logits of RT_TOK tokens into zl[RT_TOK][ldz] (raw dot products).
+template <int NEB>
+DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
+  const bf16_t* x = static_cast<const bf16_t*>(a.x);
+  const bf16_t* w = static_cast<const bf16_t*>(a.w);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int row = lane & 31;
+  const int half = lane >> 5;
+  const int t = t0 + row;
+  f32x16_t acc[NEB];
+#pragma unroll
+  for (int eb = 0; eb < NEB; ++eb) acc[eb] = f32x16_t{};
+  const bf16x8_t zero8 = {};
+  // wave w handles 64-wide slices w, w+4, w+8, ... of the d reduction; the
+  // lane's 32 consecutive elements of a slice feed the 4 k16 MFMA steps in
+  // the same order for the token and the expert operand
+  for (int kb = wave; kb * 64 < a.d; kb += 4) {
+    const int c0 = kb * 64 + half * 32;
+    bf16x8_t av[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = c0 + q * 8;
+      av[q] = (t < a.T && c + 8 <= a.d)
+                  ? *reinterpret_cast<const bf16x8_t*>(x + (size_t)t * a.d + c) : zero8;
+    }
+#pragma unroll
+    for (int eb = 0; eb < NEB; ++eb) {
+      const int e = eb * 32 + row;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = c0 + q * 8;
+        bf16x8_t bv = (e < a.E && c + 8 <= a.d)
+                          ? *reinterpret_cast<const bf16x8_t*>(w + (size_t)e * a.d + c) : zero8;
+        acc[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[q], bv, acc[eb], 0, 0, 0);
+      }
+    }
+  }
+  // deterministic cross-wave sum: wave 0 stores, waves 1..3 add in order
+  for (int wv = 0; wv < 4; ++wv) {
+    if (wave == wv) {
+#pragma unroll
+      for (int eb = 0; eb < NEB; ++eb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int i = (r >> 2) * 8 + half * 4 + (r & 3);
+          const int e = eb * 32 + row;
+          if (e < a.E) {
+            float* p = zl + i * ldz + e;
+            *p = (wv == 0) ? acc[eb][r] : *p + acc[eb][r];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+DEVI void logits_f32(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
+  const float* x = static_cast<const float*>(a.x);
+  const float* w = static_cast<const float*>(a.w);
+  for (int p = threadIdx.x; p < RT_TOK * a.E; p += RT_THREADS) {
+    const int i = p / a.E, e = p % a.E;
+    const int t = t0 + i;
+    float s = 0.f;
+    if (t < a.T) {
+      const float* xr = x + (size_t)t * a.d;
+      const float* wr = w + (size_t)e * a.d;
+      for (int c = 0; c < a.d; ++c) s = fmaf(xr[c], wr[c], s);
+    }
+    zl[i * ldz + e] = s;
+  }
+  __syncthreads();
+}
+
+template <int NEB, bool BF16>
+__global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
+  constexpr int LDZ = NEB * 32 + 1;
+  constexpr int NQ = (NEB * 32 + 63) / 64;  // logits (and selections) per lane
+  __shared__ float zl[RT_TOK * LDZ];
+  __shared__ int lmap[256];
+  const int t0 = blockIdx.x * RT_TOK;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  if (wave == 0) build_local_map(a.resident, a.E, lmap);
+  if constexpr (BF16) logits_mfma<NEB>(a, t0, zl, LDZ);
+  else logits_f32(a, t0, zl, LDZ);
+  // z = (dot + bias) * inv_tau
+  for (int p = threadIdx.x; p < RT_TOK * a.E; p += RT_THREADS) {
+    const int i = p / a.E, e = p % a.E;
+    float v = zl[i * LDZ + e];
+    if (a.bias) v += a.bias[e];
+    v *= a.inv_tau;
+    zl[i * LDZ + e] = v;
+    const int t = t0 + i;
+    if (a.logits && t < a.T) a.logits[(size_t)t * a.E + e] = v;
+  }
+  __syncthreads();
+
+  for (int i = wave; i < RT_TOK; i += 4) {
+    const int t = t0 + i;
+    if (t >= a.T) break;
+    float v[NQ];
+    bool taken[NQ];
+    int my_e[NQ];
+    float my_z[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int e = q * 64 + lane;
+      taken[q] = !(e < a.E);
+      v[q] = (e < a.E) ? zl[i * LDZ + e] : 0.f;
+      if (v[q] != v[q]) v[q] = -INFINITY;  // NaN ranks last; some expert is always picked
+      my_e[q] = 0;
+      my_z[q] = 0.f;
+    }
+    float zmax = 0.f;
+    for (int j = 0; j < a.k; ++j) {
+      float bv = -INFINITY;
+      int be = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int e = q * 64 + lane;
+        if (!taken[q] && (v[q] > bv || (v[q] == bv && e < be))) { bv = v[q]; be = e; }
+      }
+      wave_argmax(bv, be);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        if (q * 64 + lane == be) taken[q] = true;
+        if (q * 64 + lane == j) { my_e[q] = be; my_z[q] = bv; }
+      }
+      if (j == 0) zmax = bv;
+    }
+    // gate weights of the selected experts (selection j lives in lane j % 64)
+    float denom = 1.f;
+    if (a.gate == 0) {  // softmax over the k selected logits
+      float s = 0.f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        if (q * 64 + lane < a.k) s += expf(my_z[q] - zmax);
+      denom = wave_sum(s);
+    } else if (a.gate == 1) {  // softmax over all E logits
+      float s = 0.f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        if (q * 64 + lane < a.E) s += expf(v[q] - zmax);
+      denom = wave_sum(s);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int j = q * 64 + lane;
+      if (j < a.k) {
+        float wj;
+        if (a.gate == 2) wj = sigmoid_f(my_z[q]);
+        else wj = expf(my_z[q] - zmax) / denom;
+        const size_t o = (size_t)t * a.k + j;
+        a.idx[o] = my_e[q];
+        a.tw[o] = wj;
+        a.local[o] = lmap[my_e[q]];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward.  dz per token (wave per token, lane per expert), then
+// dW_r = inv_tau * dz^T x as per-chunk partial sums reduced in a fixed order,
+// and dx (+)= inv_tau * dz W_r.
+
+struct RouteBwdArgs {
+  const void* x;
+  const void* w;
+  const int32_t* idx;
+  const float* tw;
+  const float* logits;
+  const float* dtw;
+  float* dz;
+  float* dw;
+  float* db;
+  void* dx;
+  float* part_w;  // [n_chunks][E][d]
+  float* part_b;  // [n_chunks][E]
+  int T, d, E, k, gate, accumulate_dx, n_chunks;
+  float inv_tau;
+};
+
+constexpr int RB_CHUNK = 512;  // tokens per partial sum of dW_r
+
+__global__ __launch_bounds__(256) void route_dz_kernel(RouteBwdArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= a.T) return;
+  const size_t o = (size_t)t * a.k;
+  // s = <w, dw> over the k routes (lane-parallel, fixed tree order)
+  float s = 0.f;
+  for (int j = lane; j < a.k; j += 64) s += a.tw[o + j] * a.dtw[o + j];
+  s = wave_sum(s);
+  float zmax = 0.f, denom = 1.f;
+  if (a.gate == 1) {
+    float m = -INFINITY;
+    for (int e = lane; e < a.E; e += 64) m = fmaxf(m, a.logits[(size_t)t * a.E + e]);
+    zmax = wave_max(m);
+    float acc = 0.f;
+    for (int e = lane; e < a.E; e += 64) acc += expf(a.logits[(size_t)t * a.E + e] - zmax);
+    denom = wave_sum(acc);
+  }
+  for (int e = lane; e < a.E; e += 64) {
+    int jj = -1;
+    for (int j = 0; j < a.k; ++j)
+      if (a.idx[o + j] == e) { jj = j; break; }
+    float g = 0.f;
+    if (a.gate == 0) {
+      if (jj >= 0) g = a.tw[o + jj] * (a.dtw[o + jj] - s);
+    } else if (a.gate == 2) {
+      if (jj >= 0) { const float wv = a.tw[o + jj]; g = a.dtw[o + jj] * wv * (1.f - wv); }
+    } else {
+      const float p = expf(a.logits[(size_t)t * a.E + e] - zmax) / denom;
+      g = p * ((jj >= 0 ? a.dtw[o + jj] : 0.f) - s);
+    }
+    a.dz[(size_t)t * a.E + e] = g;
+  }
+}
+
+// partial[c][e][col] = sum_{t in chunk c} dz[t,e] x[t,col]; block = 64 cols x
+// 64 experts of one chunk, thread = 4 experts x 4 cols.
+template <class T>
+__global__ __launch_bounds__(256) void route_dw_partial_kernel(RouteBwdArgs a) {
+  __shared__ float sdz[32][65];
+  __shared__ float sx[32][65];
+  const T* x = static_cast<const T*>(a.x);
+  const int c0 = blockIdx.x * 64;
+  const int e0 = blockIdx.y * 64;
+  const int chunk = blockIdx.z;
+  const int tb = chunk * RB_CHUNK;
+  const int te = min(a.T, tb + RB_CHUNK);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4] = {};
+  float bacc = 0.f;
+  for (int t1 = tb; t1 < te; t1 += 32) {
+    for (int p = threadIdx.x; p < 32 * 64; p += 256) {
+      const int i = p >> 6, c = p & 63;
+      const int t = t1 + i;
+      sdz[i][c] = (t < te && e0 + c < a.E) ? a.dz[(size_t)t * a.E + e0 + c] : 0.f;
+      sx[i][c] = (t < te && c0 + c < a.d) ? to_f32(x[(size_t)t * a.d + c0 + c]) : 0.f;
+    }
+    __syncthreads();
+    for (int i = 0; i < 32; ++i) {
+      float zv[4], xv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) { zv[u] = sdz[i][ty * 4 + u]; xv[u] = sx[i][tx * 4 + u]; }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(zv[u], xv[v], acc[u][v]);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64)
+      for (int i = 0; i < 32; ++i) bacc += sdz[i][threadIdx.x];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int e = e0 + ty * 4 + u;
+    if (e >= a.E) continue;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int c = c0 + tx * 4 + v;
+      if (c < a.d) a.part_w[((size_t)chunk * a.E + e) * a.d + c] = acc[u][v];
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 64 && e0 + threadIdx.x < a.E)
+    a.part_b[(size_t)chunk * a.E + e0 + threadIdx.x] = bacc;
+}
+
+__global__ __launch_bounds__(256) void route_dw_reduce_kernel(RouteBwdArgs a) {
+  const size_t n = (size_t)a.E * a.d;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    float s = 0.f;
+    for (int c = 0; c < a.n_chunks; ++c) s += a.part_w[(size_t)c * n + i];
+    a.dw[i] = s * a.inv_tau;
+  }
+  if (a.db && blockIdx.x == 0) {
+    for (int e = threadIdx.x; e < a.E; e += 256) {
+      float s = 0.f;
+      for (int c = 0; c < a.n_chunks; ++c) s += a.part_b[(size_t)c * a.E + e];
+      a.db[e] = s * a.inv_tau;
+    }
+  }
+}
+
+// dx[t, c..c+V) (+)= inv_tau * sum_e dz[t,e] W_r[e, c..c+V); block = 8 tokens,
+// thread = 8 tokens x one 16-byte column vector.
+template <class T>
+__global__ __launch_bounds__(256) void route_dx_kernel(RouteBwdArgs a) {
+  constexpr int V = Vec16<T>::N;
+  constexpr int TT = 8;
+  __shared__ float sdz[TT][257];
+  const T* w = static_cast<const T*>(a.w);
+  T* dx = static_cast<T*>(a.dx);
+  const int t0 = blockIdx.x * TT;
+  for (int p = threadIdx.x; p < TT * a.E; p += 256) {
+    const int i = p / a.E, e = p % a.E;
+    sdz[i][e] = (t0 + i < a.T) ? a.dz[(size_t)(t0 + i) * a.E + e] : 0.f;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x * V; c < a.d; c += 256 * V) {
+    float acc[TT][V];
+#pragma unroll
+    for (int i = 0; i < TT; ++i)
+#pragma unroll
+      for (int u = 0; u < V; ++u) acc[i][u] = 0.f;
+    for (int e = 0; e < a.E; ++e) {
+      float wv[V];
+      load16_f32(w + (size_t)e * a.d + c, wv);
+#pragma unroll
+      for (int i = 0; i < TT; ++i) {
+        const float z = sdz[i][e];
+#pragma unroll
+        for (int u = 0; u < V; ++u) acc[i][u] = fmaf(z, wv[u], acc[i][u]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < TT; ++i) {
+      const int t = t0 + i;
+      if (t >= a.T) break;
+      T* p = dx + (size_t)t * a.d + c;
+      float o[V];
+      if (a.accumulate_dx) load16_f32(p, o);
+#pragma unroll
+      for (int u = 0; u < V; ++u) o[u] = (a.accumulate_dx ? o[u] : 0.f) + a.inv_tau * acc[i][u];
+      store16_f32(p, o);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int bf16, int T,
+                            int d, int E, int k, float inv_tau, int gate, const uint8_t* resident,
+                            float* logits, int32_t* idx, float* tw, int32_t* local,
+                            hipStream_t s) {
+  RouteFwdArgs a{x, w, bias, resident, logits, idx, tw, local, T, d, E, k, gate, inv_tau};
+  if (T == 0) return hipSuccess;
+  const dim3 grid(ceil_div(T, RT_TOK));
+  const int neb = E <= 32 ? 1 : E <= 64 ? 2 : E <= 128 ? 4 : 8;
+#define ROUTE_CASE(N)                                                                 \
+  case N:                                                                             \
+    if (bf16) MOE_TIMED("route_fwd", s, route_fwd_kernel<N, true><<<grid, RT_THREADS, 0, s>>>(a)); \
+    else MOE_TIMED("route_fwd", s, route_fwd_kernel<N, false><<<grid, RT_THREADS, 0, s>>>(a));     \
+    break;
+  switch (neb) { ROUTE_CASE(1) ROUTE_CASE(2) ROUTE_CASE(4) ROUTE_CASE(8) }
+#undef ROUTE_CASE
+  return hipGetLastError();
+}
+
+size_t route_bwd_ws_bytes(int T, int d, int E) {
+  const size_t chunks = (size_t)(T + RB_CHUNK - 1) / RB_CHUNK;
+  return chunks * (size_t)E * ((size_t)d + 1) * sizeof(float) + 256;
+}
+
+hipError_t launch_route_bwd(const void* x, const void* w, int bf16, int T, int d, int E, int k,
+                            float inv_tau, int gate, const int32_t* idx, const float* tw,
+                            const float* logits, const float* dtw, float* dz, float* dw_router,
+                            float* d_bias, void* dx, int accumulate_dx, void* ws,
+                            hipStream_t s) {
+  const int n_chunks = (T + RB_CHUNK - 1) / RB_CHUNK;
+  float* part_w = static_cast<float*>(ws);
+  float* part_b = part_w + (size_t)n_chunks * E * d;
+  RouteBwdArgs a{x, w, idx, tw, logits, dtw, dz, dw_router, d_bias, dx, part_w, part_b,
+                 T, d, E, k, gate, accumulate_dx, n_chunks, inv_tau};
+  if (T > 0) MOE_TIMED("route_dz", s, route_dz_kernel<<<ceil_div(T, 4), 256, 0, s>>>(a));
+  if (n_chunks > 0) {
+    const dim3 g(ceil_div(d, 64), ceil_div(E, 64), n_chunks);
+    if (bf16) MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<bf16_t><<<g, 256, 0, s>>>(a));
+    else MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<float><<<g, 256, 0, s>>>(a));
+  }
+  {
+    // n_chunks == 0 (T == 0) sums nothing and writes zeros
+    const int blocks = (int)std::min<size_t>(2048, ((size_t)E * d + 255) / 256);
+    MOE_TIMED("route_dw_reduce", s, route_dw_reduce_kernel<<<blocks, 256, 0, s>>>(a));
+  }
+  if (T > 0) {
+    if (bf16) MOE_TIMED("route_dx", s, route_dx_kernel<bf16_t><<<ceil_div(T, 8), 256, 0, s>>>(a));
+    else MOE_TIMED("route_dx", s, route_dx_kernel<float><<<ceil_div(T, 8), 256, 0, s>>>(a));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,132 @@
+"""One worker's local step through the resident-expert MoE layer.
+
+``ResidentMoELayer`` owns the device buffers of one layer shape and issues the
+C entry points in order; it computes nothing itself.
+
+Forward:  moe_route_mask -> moe_dispatch -> moe_grouped_ffn_fwd (resident
+          experts) [-> moe_grouped_ffn_fwd (shared experts, identity dispatch)]
+          -> moe_combine_fwd
+Backward: moe_combine_bwd -> moe_grouped_ffn_bwd (resident)
+          [-> moe_grouped_ffn_bwd (shared), writing dx] -> moe_dispatch_bwd
+          -> moe_route_bwd (adds the router's dx)
+Round boundary: moe_expert_delta over the fp32 master copies.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import binding as B
+
+
+class ResidentMoELayer:
+    def __init__(self, T, d, E, k, H, resident, dtype=torch.bfloat16, n_shared_hidden=0,
+                 gate="softmax_topk", inv_tau=1.0, device="cuda"):
+        self.T, self.d, self.E, self.k, self.H = int(T), int(d), int(E), int(k), int(H)
+        res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
+        assert res.numel() == self.E
+        self.E_r = int(res.sum().item())
+        self.cap = self.T * min(self.k, self.E_r)
+        self.dtype = dtype
+        self.dt = B.MOE_BF16 if dtype == torch.bfloat16 else B.MOE_F32
+        self.gate = B.GATES[gate] if isinstance(gate, str) else int(gate)
+        self.inv_tau = float(inv_tau)
+        self.Hs = int(n_shared_hidden)
+        self.device = device
+        dev = torch.device(device)
+        T, d, E, k, H, cap = self.T, self.d, self.E, self.k, self.H, self.cap
+        f32, i32, act = torch.float32, torch.int32, dtype
+        e = lambda *s, dt=act: torch.empty(*s, dtype=dt, device=dev)
+        self.resident = res.to(dev)
+        # routing
+        self.logits = e(T, E, dt=f32)
+        self.topk_idx = e(T, k, dt=i32)
+        self.topk_w = e(T, k, dt=f32)
+        self.topk_local = e(T, k, dt=i32)
+        # dispatch
+        self.counts = e(max(self.E_r, 1), dt=i32)
+        self.offsets = e(self.E_r + 1, dt=i32)
+        self.perm = e(max(cap, 1), dt=i32)
+        self.inv_perm = e(T, k, dt=i32)
+        self.ws_dispatch_bytes = B.moe_dispatch_workspace_size(T, k, self.E_r)
+        self.ws_dispatch = e(self.ws_dispatch_bytes, dt=torch.uint8)
+        # experts
+        rows = max(cap, 1)
+        self.xp = e(rows, d)
+        self.gu = e(rows, 2 * H)
+        self.h = e(rows, H)
+        self.yp = e(rows, d)
+        self.y = e(T, d)
+        # backward
+        self.dyp = e(rows, d)
+        self.dtopk_w = e(T, k, dt=f32)
+        self.dgu = e(rows, 2 * H)
+        self.dxp = e(rows, d)
+        self.dw_gate_up = e(max(self.E_r, 1), 2 * H, d, dt=f32)
+        self.dw_down = e(max(self.E_r, 1), d, H, dt=f32)
+        self.dx = e(T, d)
+        self.dz = e(T, E, dt=f32)
+        self.dw_router = e(E, d, dt=f32)
+        self.d_bias = e(E, dt=f32)
+        self.ws_route_bytes = B.moe_route_bwd_workspace_size(T, d, E)
+        self.ws_route = e(self.ws_route_bytes, dt=torch.uint8)
+        if self.Hs:
+            Hs = self.Hs
+            self.s_offsets = torch.tensor([0, T], dtype=i32, device=dev)
+            self.s_gu = e(T, 2 * Hs)
+            self.s_h = e(T, Hs)
+            self.s_y = e(T, d)
+            self.s_dgu = e(T, 2 * Hs)
+            self.s_dw_gate_up = e(1, 2 * Hs, d, dt=f32)
+            self.s_dw_down = e(1, d, Hs, dt=f32)
+
+    # ------------------------------------------------------------------ forward
+    def forward(self, x, w_router, w_gate_up, w_down, router_bias=None, shared_gate_up=None,
+                shared_down=None, stream=None):
+        T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        B.moe_route_mask(x, w_router, router_bias, dt, T, d, E, k, self.inv_tau, self.gate,
+                         self.resident, self.logits, self.topk_idx, self.topk_w, self.topk_local,
+                         stream)
+        B.moe_dispatch(x, dt, T, d, k, self.E_r, self.topk_local, self.counts, self.offsets,
+                       self.perm, self.inv_perm, self.xp, self.ws_dispatch, self.ws_dispatch_bytes,
+                       stream)
+        B.moe_grouped_ffn_fwd(self.xp, w_gate_up, w_down, dt, cap, d, H, self.E_r, self.offsets,
+                              self.gu, self.h, self.yp, stream)
+        y_add = None
+        if self.Hs:
+            B.moe_grouped_ffn_fwd(x, shared_gate_up, shared_down, dt, T, d, self.Hs, 1,
+                                  self.s_offsets, self.s_gu, self.s_h, self.s_y, stream)
+            y_add = self.s_y
+        B.moe_combine_fwd(self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, y_add, self.y,
+                          stream)
+        return self.y
+
+    # ----------------------------------------------------------------- backward
+    def backward(self, dy, x, w_router, w_gate_up, w_down, shared_gate_up=None, shared_down=None,
+                 accumulate_dw=0, stream=None):
+        T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        B.moe_combine_bwd(dy, self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, self.dyp,
+                          self.dtopk_w, stream)
+        B.moe_grouped_ffn_bwd(self.dyp, self.xp, self.gu, self.h, w_gate_up, w_down, dt, cap, d, H,
+                              self.E_r, self.offsets, self.dgu, self.dxp, self.dw_gate_up,
+                              self.dw_down, accumulate_dw, stream)
+        if self.Hs:
+            # the shared experts see every token with weight 1: their dxp is dx
+            B.moe_grouped_ffn_bwd(dy, x, self.s_gu, self.s_h, shared_gate_up, shared_down, dt, T,
+                                  d, self.Hs, 1, self.s_offsets, self.s_dgu, self.dx,
+                                  self.s_dw_gate_up, self.s_dw_down, accumulate_dw, stream)
+        B.moe_dispatch_bwd(self.dxp, dt, T, d, k, cap, self.inv_perm, self.dx, 1 if self.Hs else 0,
+                           stream)
+        B.moe_route_bwd(x, w_router, dt, T, d, E, k, self.inv_tau, self.gate, self.topk_idx,
+                        self.topk_w, self.logits, self.dtopk_w, self.dz, self.dw_router,
+                        self.d_bias, self.dx, 1, self.ws_route, self.ws_route_bytes, stream)
+        return self.dx
+
+
+def expert_delta(theta_start, theta_now, peers, delta_local=None, delta_avg=None, stream=None):
+    """Round-boundary pseudo-gradient of the resident experts and its replica-group average."""
+    n = theta_start.numel()
+    if delta_avg is None:
+        delta_avg = torch.empty_like(theta_start)
+    B.moe_expert_delta(theta_start, theta_now, list(peers), len(peers), n, delta_local, delta_avg,
+                       stream)
+    return delta_avg

@@ -1,0 +1,136 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Full-layer parity on the small and mid workloads, edge cases (ragged sizes,
+empty and full resident sets, k = 1, ties, all gate functions, temperature,
+router bias, accumulation), determinism, and the round-boundary delta.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe_oracle as O
+from paper_2606_19025_amd import binding as B
+from paper_2606_19025_amd import inputs as I
+from paper_2606_19025_amd.layer import expert_delta
+
+from .parity_helpers import (TOL, assert_close, check_layer_against_oracle, dev, gpu_outputs,
+                             host, run_gpu_layer, say)
+
+pytestmark = pytest.mark.gpu
+
+
+def synth_inputs(T, d, E, k, H, resident, dtype="bf16", seed=0, shared_hidden=0, bias=False,
+                 wscale=0.02):
+    g = np.random.default_rng(seed)
+    rnd = I.bf16_round if dtype == "bf16" else (lambda a: np.asarray(a, np.float32))
+    resident = sorted(resident)
+    Er = len(resident)
+    res = np.zeros(E, np.uint8)
+    res[resident] = 1
+    nrm = lambda *s: g.standard_normal(s, dtype=np.float32)
+    inp = dict(cfg=dict(T=T, d=d, E=E, k=k, H=H, E_r=Er, resident=resident, dtype=dtype,
+                        n_shared=1 if shared_hidden else 0, Hs=shared_hidden),
+               x=rnd(nrm(T, d)), dy=rnd(nrm(T, d)), w_router=rnd(nrm(E, d) * wscale * 4),
+               w_gate_up=rnd(nrm(Er, 2 * H, d) * wscale), w_down=rnd(nrm(Er, d, H) * wscale),
+               resident=res, router_bias=(nrm(E) * 0.1) if bias else None)
+    if shared_hidden:
+        inp["shared_gate_up"] = rnd(nrm(1, 2 * shared_hidden, d) * wscale)
+        inp["shared_down"] = rnd(nrm(1, d, shared_hidden) * wscale)
+    return inp
+
+
+@pytest.mark.parametrize("wl", [0, 1, 3])
+def test_layer_parity_workload(gpu_lib, wl):
+    say(f"[parity] workload {wl}")
+    inp = I.make_layer_inputs(wl)
+    L, _ = run_gpu_layer(inp)
+    g = gpu_outputs(L)
+    errs = check_layer_against_oracle(inp, g)
+    say(f"[parity] workload {wl} n={g['n']} errs={ {k: (round(v, 8) if isinstance(v, float) else v) for k, v in errs.items()} }")
+
+
+CASES = {
+    # name: (T, d, E, k, H, resident, dtype, shared_hidden, bias, gate, inv_tau)
+    "ragged-bf16": (777, 128, 12, 3, 192, [0, 2, 3, 7, 11], "bf16", 0, False, "softmax_topk", 1.0),
+    "ragged-f32": (333, 72, 10, 2, 64, [1, 4, 5], "f32", 0, False, "softmax_topk", 1.0),
+    "shared-bias-tau": (300, 128, 16, 4, 128, list(range(4, 12)), "bf16", 128, True, "softmax_topk", 0.8),
+    "softmax-raw": (256, 64, 8, 2, 64, [0, 1, 6], "bf16", 0, False, "softmax", 1.0),
+    "sigmoid": (256, 64, 8, 2, 64, [0, 1, 6], "f32", 0, False, "sigmoid", 1.3),
+    "k1-single-resident": (200, 64, 4, 1, 64, [2], "bf16", 0, False, "softmax_topk", 1.0),
+    "all-resident": (256, 128, 8, 2, 128, list(range(8)), "bf16", 0, False, "softmax_topk", 1.0),
+    "no-resident": (128, 64, 8, 2, 64, [], "bf16", 64, False, "softmax_topk", 1.0),
+    "many-experts": (300, 64, 256, 8, 64, list(range(0, 256, 5)), "bf16", 0, False, "softmax_topk", 1.0),
+    "multi-tile-groups": (1500, 256, 4, 2, 256, [0, 1, 3], "bf16", 0, False, "softmax_topk", 1.0),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_layer_parity_edge_cases(gpu_lib, name):
+    T, d, E, k, H, res, dt, hs, bias, gate, tau = CASES[name]
+    say(f"[edge] {name}")
+    inp = synth_inputs(T, d, E, k, H, res, dt, seed=len(name), shared_hidden=hs, bias=bias)
+    if not res:  # no resident expert: weights of zero experts
+        inp["w_gate_up"] = np.zeros((0, 2 * H, d), np.float32)
+        inp["w_down"] = np.zeros((0, d, H), np.float32)
+    L, _ = run_gpu_layer(inp, gate=gate, inv_tau=tau)
+    g = gpu_outputs(L)
+    check_layer_against_oracle(inp, g, gate=gate, inv_tau=tau)
+    if not res:
+        assert g["n"] == 0
+        assert np.all(g["dz"] == 0) and np.all(g["dw"] == 0)
+
+
+def test_topk_ties_go_to_lower_expert_id(gpu_lib):
+    # one-hot tokens and repeated router columns give exactly equal logits
+    T, d, E, k = 64, 64, 8, 3
+    x = np.zeros((T, d), np.float32)
+    x[np.arange(T), np.arange(T) % d] = 1.0
+    w = np.zeros((E, d), np.float32)
+    w[[1, 3, 6], :] = 0.5   # three-way tie at the top
+    w[[2, 7], :] = 0.25     # two-way tie below
+    res = np.zeros(E, np.uint8); res[[3, 7]] = 1
+    idx = torch.empty(T, k, dtype=torch.int32, device="cuda")
+    loc = torch.empty_like(idx)
+    tw = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    B.moe_route_mask(dev(x, torch.bfloat16), dev(w, torch.bfloat16), None, B.MOE_BF16, T, d, E, k,
+                     1.0, 0, torch.from_numpy(res).cuda(), None, idx, tw, loc)
+    torch.cuda.synchronize()
+    assert np.all(host(idx) == np.array([1, 3, 6]))
+    assert np.all(host(loc) == np.array([-1, 0, -1]))
+    np.testing.assert_allclose(host(tw), 1.0 / 3.0, rtol=1e-6)
+
+
+def test_layer_is_deterministic(gpu_lib):
+    inp = synth_inputs(600, 128, 12, 3, 128, [0, 3, 5, 8], "bf16", seed=5, shared_hidden=64)
+    L1, _ = run_gpu_layer(inp)
+    a = gpu_outputs(L1)
+    L2, _ = run_gpu_layer(inp, layer=L1)
+    b = gpu_outputs(L2)
+    for key in ("logits", "w", "idx", "perm", "y", "dx", "dz", "dW_router", "dW_gate_up",
+                "dW_down", "s_dW_gate_up"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_accumulate_dw_adds(gpu_lib):
+    inp = synth_inputs(300, 128, 8, 2, 128, [1, 2, 5], "f32", seed=9)
+    L, d_in = run_gpu_layer(inp)
+    first = host(L.dw_gate_up).copy(), host(L.dw_down).copy()
+    L.backward(d_in["dy"], d_in["x"], d_in["w_router"], d_in["w_gate_up"], d_in["w_down"],
+               accumulate_dw=1)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(host(L.dw_gate_up), 2 * first[0], rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(host(L.dw_down), 2 * first[1], rtol=1e-6, atol=1e-7)
+
+
+@pytest.mark.parametrize("n,n_peers", [(1, 0), (1000, 1), (4099, 3), (65536 * 4 + 3, 3), (777, 5)])
+def test_expert_delta_bit_exact(gpu_lib, n, n_peers):
+    d = I.make_delta_inputs(4, n)
+    peers = [d["peers"][i % len(d["peers"])] * (1 + i) for i in range(n_peers)]
+    dl_ref, avg_ref = O.expert_delta(d["theta_start"], d["theta_now"], peers)
+    ts, tn = dev(d["theta_start"], torch.float32), dev(d["theta_now"], torch.float32)
+    pd = [dev(p, torch.float32) for p in peers]
+    dl = torch.empty_like(ts)
+    avg = expert_delta(ts, tn, pd, delta_local=dl)
+    torch.cuda.synchronize()
+    assert np.array_equal(dl.cpu().numpy(), dl_ref)
+    assert np.array_equal(avg.cpu().numpy(), avg_ref)

@@ -233,7 +233,7 @@ def test_empty_resident_set_gives_zero_routed_output():
     inp = tiny_inputs(T=20, E=4, k=2, resident=(), shared=0)
     inp["w_gate_up"] = np.zeros((0, 16, 16)); inp["w_down"] = np.zeros((0, 16, 8))
     fwd = O.layer_fwd(inp)
-    assert fwd["offsets"][-1] == 0 and np.all(fwd["y"] == 0.0)
+    assert fwd["offsets"][-1] == 0 and fwd["y"].shape == (20, 16) and np.all(fwd["y"] == 0.0)
 
 
 def test_skip_fraction_matches_sigma_st():
