@@ -232,168 +232,204 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
+//
+// Block tile 256 x 256, k-step 64, 256 threads = 4 waves in a 2 x 2 grid;
+// each wave owns a 128 x 128 sub-tile = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles
+// (256 fp32 accumulators per lane), which keeps the LDS read traffic at
+// 8 KB per 16 MFMAs.  Operand tiles go global -> LDS with 16-byte
+// global_load_lds (no VGPR staging), two stages double-buffered (128 KB).
+//
+// LDS layouts (per operand and stage, 32 KB):
+//  k-contiguous operand (rows = M or N index): row r holds 64 k = 128 B; its
+//    16-byte chunk kc sits at chunk position kc ^ (r & 7).  A fragment row
+//    is one ds_read_b128.
+//  m/n-contiguous operand (rows = k): row k holds 256 m = 512 B; its 32-byte
+//    chunk c sits at position c ^ (2 * (k & 3)).  A fragment is two
+//    ds_read_b64_tr_b16: in each 16-lane group, lane j points at (k0 + j/4,
+//    m0 + 4*(j%4)) and lane i receives m0 + i for k0..k0+3.
+// Rows outside the valid range are clamped to a valid row (finite data) and
+// the corresponding outputs are not stored; in the ragged-K tail the B
+// fragment elements past the group's last row are zeroed in registers.
 
-constexpr int MB = 128, NB = 128, KB = 64;  // block tile
-constexpr int TILE_ELEMS = 128 * KB;        // one operand stage in LDS (bf16)
+constexpr int GT = 256;                     // block tile (M and N)
+constexpr int GK = 64;                      // k-step
+constexpr int OP_BYTES = GT * GK * 2;       // one operand stage: 32 KB
+constexpr int LDS_BYTES = 4 * OP_BYTES;     // 2 stages x (A, B)
 
-// LDS element offset of the 16-byte chunk kc (0..7) of row r.
-DEVI int lds_off(int r, int kc) { return r * KB + ((kc ^ (r & 7)) << 3); }
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8_t;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// Registers staged between the global load and the LDS store of one operand.
-struct Stage {
-  u32x4_t v[4];
-};
+DEVI void load_to_lds(const bf16_t* g, char* lds_base) {
+  __builtin_amdgcn_global_load_lds((glb_void_t*)g, (lds_void_t*)lds_base, 16, 0, 0);
+}
 
-// k-contiguous operand: 128 rows x 8 chunks; thread loads chunks tid + 256*i.
-// row_ptr(r) returns the element pointer of row r at k = 0, or nullptr.
+// k-contiguous fill: wave w issues loads i = 0..7, load q = 4i + w covers rows
+// 8q .. 8q+7; lane l writes chunk position l%8 of row 8q + l/8.
 template <class RowPtr>
-DEVI void load_kc(Stage& st, RowPtr row_ptr, int k0) {
+DEVI void fill_kc(char* lds_op, const RowPtr& row_ptr, int k0) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int kc = (lane & 7) ^ ((lane >> 3) & 7);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = threadIdx.x + 256 * i;
-    const int r = q >> 3, kc = q & 7;
-    const bf16_t* p = row_ptr(r);
-    st.v[i] = p ? *reinterpret_cast<const u32x4_t*>(p + k0 + kc * 8) : u32x4_t{0, 0, 0, 0};
+  for (int i = 0; i < 8; ++i) {
+    const int q = i * 4 + w;
+    const int row = q * 8 + (lane >> 3);
+    load_to_lds(row_ptr(row) + k0 + kc * 8, lds_op + q * 1024);
   }
 }
 
-DEVI void store_kc(const Stage& st, bf16_t* lds) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = threadIdx.x + 256 * i;
-    const int r = q >> 3, kc = q & 7;
-    *reinterpret_cast<u32x4_t*>(lds + lds_off(r, kc)) = st.v[i];
-  }
-}
-
-// mn-contiguous operand: thread loads k-rows kb*4+u (u<4) x elements mb*8..+8
-// with mb = tid & 15, kb = tid >> 4.  elem_ptr(k, c) returns the pointer of
-// (k, c..c+8) or nullptr when out of range.
+// m/n-contiguous fill: load q covers k-rows 2q, 2q+1 (512 B each); lane l
+// writes the 16-byte slot l%32 of row 2q + l/32.
 template <class ElemPtr>
-DEVI void load_mn(Stage& st, ElemPtr elem_ptr, int k0) {
-  const int mb = threadIdx.x & 15, kb = threadIdx.x >> 4;
+DEVI void fill_mn(char* lds_op, const ElemPtr& elem_ptr, int k0) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ps = lane & 31;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const bf16_t* p = elem_ptr(k0 + kb * 4 + u, mb * 8);
-    st.v[u] = p ? *reinterpret_cast<const u32x4_t*>(p) : u32x4_t{0, 0, 0, 0};
+  for (int i = 0; i < 8; ++i) {
+    const int q = i * 4 + w;
+    const int row = q * 2 + (lane >> 5);
+    const int c = (ps >> 1) ^ (2 * (row & 3));
+    load_to_lds(elem_ptr(k0 + row, c * 16 + (ps & 1) * 8), lds_op + q * 1024);
   }
 }
 
-DEVI void store_mn(const Stage& st, bf16_t* lds) {
-  const int mb = threadIdx.x & 15, kb = threadIdx.x >> 4;
-  const int kc = kb >> 1, sub = (kb & 1) * 4;
+// fragment of rows/cols [mb, mb+32) at k16-step s, k-contiguous layout
+DEVI bf16x8_t frag_kc(const char* lds_op, int mb, int s) {
+  const int lane = threadIdx.x & 63;
+  const int row = mb + (lane & 31);
+  const int kc = s * 2 + (lane >> 5);
+  return *reinterpret_cast<const bf16x8_t*>(lds_op + row * 128 + ((kc ^ (row & 7)) << 4));
+}
+
+// same fragment from the m/n-contiguous layout with two transposing reads
+DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, i = lane & 15;
+  const int mn = mb + 16 * (g & 1) + 4 * (i & 3);
+  s16x4_t v[2];
 #pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const int dw = m >> 1;
-    const uint32_t sel = (m & 1) ? 0x07060302u : 0x05040100u;
-    u32x2_t o;
-    o[0] = __builtin_amdgcn_perm(st.v[1][dw], st.v[0][dw], sel);
-    o[1] = __builtin_amdgcn_perm(st.v[3][dw], st.v[2][dw], sel);
-    const int r = mb * 8 + m;
-    *reinterpret_cast<u32x2_t*>(lds + lds_off(r, kc) + sub) = o;
+  for (int h = 0; h < 2; ++h) {
+    const int k = s * 16 + 8 * (g >> 1) + 4 * h + (i >> 2);
+    const int pc = (mn >> 4) ^ (2 * (k & 3));
+    const char* p = lds_op + k * 512 + pc * 32 + (mn & 15) * 2;
+    v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
   }
+  // whole-vector concatenation (element-wise inserts of bit-cast lanes were
+  // mis-generated into a splat of element 0)
+  const s16x8_t both = __builtin_shufflevector(v[0], v[1], 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8_t, both);
 }
 
 template <int KIND>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   using K_ = Kind<KIND>;
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2 * 2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
   Tile tl;
-  if (!decode_tile<MB, NB, KIND>(a, tl)) return;
+  if (!decode_tile<GT, GT, KIND>(a, tl)) return;
   const bf16_t* A = static_cast<const bf16_t*>(a.A);
   const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
   const int Kd = K_::MRAG ? a.K : tl.rows;
-  const int nk = (Kd + KB - 1) / KB;
+  const int nk = (Kd + GK - 1) / GK;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int tile_n = blockIdx.x;
+  const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
 
-  auto a_row = [&](int r) -> const bf16_t* {
-    return r < tl.rows ? A + (size_t)(tl.row0 + r) * a.lda : nullptr;
+  // operand pointers; out-of-range indices are clamped to valid memory
+  auto a_row = [&](int r) -> const bf16_t* {  // M-ragged A, k-contiguous
+    return A + (size_t)min(tl.row0 + r, last_row) * a.lda;
   };
-  auto a_elem = [&](int k, int c) -> const bf16_t* {  // TN: A(i=c, k)
-    return (k < Kd && tl.m0 + c + 8 <= a.M) ? A + (size_t)(tl.row0 + k) * a.lda + tl.m0 + c : nullptr;
+  auto a_elem = [&](int k, int c) -> const bf16_t* {  // TN A(i = m0 + c, k)
+    const int m = (tl.m0 + c + 8 <= a.M) ? tl.m0 + c : 0;
+    return A + (size_t)min(tl.row0 + k, last_row) * a.lda + m;
   };
-  auto b_row = [&](int r) -> const bf16_t* {  // NT
+  auto b_row = [&](int r) -> const bf16_t* {  // NT B rows
     if constexpr (KIND == GU_FWD) {
       bool ok;
-      const int br = gu_brow<NB>(tile_n, r, a.H, ok);
-      return ok ? B + (size_t)br * a.ldb : nullptr;
+      int br = gu_brow<GT>(tile_n, r, a.H, ok);
+      if (!ok) br = 0;
+      return B + (size_t)br * a.ldb;
     } else {
-      return tl.n0 + r < a.N ? B + (size_t)(tl.n0 + r) * a.ldb : nullptr;
+      return B + (size_t)min(tl.n0 + r, a.N - 1) * a.ldb;
     }
   };
-  auto b_elem = [&](int k, int c) -> const bf16_t* {  // NN / TN: B(k, n = c)
-    if (k >= Kd || tl.n0 + c + 8 > a.N) return nullptr;
-    if constexpr (K_::MRAG) return B + (size_t)k * a.ldb + tl.n0 + c;
-    else return B + (size_t)(tl.row0 + k) * a.ldb + tl.n0 + c;
+  auto b_elem = [&](int k, int c) -> const bf16_t* {  // NN / TN B(k, n = n0 + c)
+    const int n = (tl.n0 + c + 8 <= a.N) ? tl.n0 + c : 0;
+    if constexpr (K_::MRAG) return B + (size_t)k * a.ldb + n;
+    else return B + (size_t)min(tl.row0 + k, last_row) * a.ldb + n;
   };
 
-  Stage sa, sb;
-  auto load_stage = [&](int kt) {
-    const int k0 = kt * KB;
-    if constexpr (K_::A_KC) load_kc(sa, a_row, k0); else load_mn(sa, a_elem, k0);
-    if constexpr (K_::B_KC) load_kc(sb, b_row, k0); else load_mn(sb, b_elem, k0);
-  };
-  auto store_stage = [&](int buf) {
-    bf16_t* la = lds + buf * 2 * TILE_ELEMS;
-    bf16_t* lb = la + TILE_ELEMS;
-    if constexpr (K_::A_KC) store_kc(sa, la); else store_mn(sa, la);
-    if constexpr (K_::B_KC) store_kc(sb, lb); else store_mn(sb, lb);
+  auto fill = [&](int kt, int buf) {
+    char* la = lds + buf * 2 * OP_BYTES;
+    char* lb = la + OP_BYTES;
+    const int k0 = kt * GK;
+    if constexpr (K_::A_KC) fill_kc(la, a_row, k0); else fill_mn(la, a_elem, k0);
+    if constexpr (K_::B_KC) fill_kc(lb, b_row, k0); else fill_mn(lb, b_elem, k0);
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
 
   if (nk > 0) {
-    load_stage(0);
-    store_stage(0);
+    fill(0, 0);
+    __builtin_amdgcn_s_waitcnt(0x0);  // vmcnt(0) expcnt(0) lgkmcnt(0)
     __syncthreads();
   }
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) load_stage(kt + 1);
-    const bf16_t* la = lds + cur * 2 * TILE_ELEMS;
-    const bf16_t* lb = la + TILE_ELEMS;
+    if (kt + 1 < nk) fill(kt + 1, cur ^ 1);
+    const char* la = lds + cur * 2 * OP_BYTES;
+    const char* lb = la + OP_BYTES;
+    const bool tail = !K_::MRAG && (kt + 1) * GK > Kd;
 #pragma unroll
-    for (int s = 0; s < KB / 16; ++s) {
-      const int kc = s * 2 + (lane >> 5);
-      bf16x8_t af[2], bfr[2];
+    for (int s = 0; s < GK / 16; ++s) {
+      bf16x8_t af[4], bfr[4];
 #pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        const int ra = wm * 64 + f * 32 + (lane & 31);
-        const int rb = wn * 64 + f * 32 + (lane & 31);
-        af[f] = *reinterpret_cast<const bf16x8_t*>(la + lds_off(ra, kc));
-        bfr[f] = *reinterpret_cast<const bf16x8_t*>(lb + lds_off(rb, kc));
+      for (int f = 0; f < 4; ++f) {
+        af[f] = K_::A_KC ? frag_kc(la, wm * 128 + f * 32, s) : frag_mn(la, wm * 128 + f * 32, s);
+        bfr[f] = K_::B_KC ? frag_kc(lb, wn * 128 + f * 32, s) : frag_mn(lb, wn * 128 + f * 32, s);
+      }
+      if (tail) {  // zero B past the group's last row (A there is finite)
+        const int kbase = kt * GK + s * 16 + 8 * (lane >> 5);
+#pragma unroll
+        for (int f = 0; f < 4; ++f)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (kbase + e >= Kd) bfr[f][e] = (bf16_t)0.0f;
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_stage(cur ^ 1);
+    __builtin_amdgcn_s_waitcnt(0x0);
     __syncthreads();
   }
 
   // accumulator (i, j) register r holds C[row, col] with
-  //   row = (r/4)*8 + (lane/32)*4 + r%4,  col = lane%32  inside the 32x32 tile
+  //   row = (r/4)*8 + (lane/32)*4 + r%4,  col = lane%32  inside its 32x32 tile
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      const int row = wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
       if constexpr (KIND == GU_FWD) {
-        // acc[i][0] = gate, acc[i][1] = up of hidden unit h
-        const int h = tile_n * (NB / 2) + wn * 32 + (lane & 31);
-        epi_swiglu<bf16_t>(a, tl, row, h, acc[i][0][r], acc[i][1][r]);
+        // tiles (i, 2p) = gate and (i, 2p+1) = up of hidden units h
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int h = tile_n * (GT / 2) + (2 * wn + p) * 32 + (lane & 31);
+          epi_swiglu<bf16_t>(a, tl, row, h, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+        }
       } else {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = wn * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < 4; ++j) {
+          const int col = wn * 128 + j * 32 + (lane & 31);
           epi_store<KIND, bf16_t>(a, tl, row, col, acc[i][j][r]);
         }
       }
@@ -403,7 +439,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 
 template <int KIND>
 hipError_t run_gemm(const GemmArgs& a, int bf16, hipStream_t s) {
-  const int BMt = bf16 ? MB : 64, BNt = bf16 ? NB : 64;
+  const int BMt = bf16 ? GT : 64, BNt = bf16 ? GT : 64;
   dim3 grid;
   const int ncols = (KIND == GU_FWD) ? 2 * a.H : a.N;
   grid.x = ceil_div(ncols, BNt);
