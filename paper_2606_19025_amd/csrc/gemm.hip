@@ -233,65 +233,115 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 //
-// Block tile 256 x 256, k-step 64, 256 threads = 4 waves in a 2 x 2 grid;
-// each wave owns a 128 x 128 sub-tile = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles
-// (256 fp32 accumulators per lane), which keeps the LDS read traffic at
-// 8 KB per 16 MFMAs.  Operand tiles go global -> LDS with 16-byte
-// global_load_lds (no VGPR staging), two stages double-buffered (128 KB).
+// Persistent: one 256-thread block per CU loops over output tiles.  Block tile
+// 256 x 256; the 4 waves form a 2 x 2 grid and each owns a 128 x 128 sub-tile
+// = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane), so
+// LDS read traffic stays at 8 KB per 16 MFMAs.
 //
-// LDS layouts (per operand and stage, 32 KB):
-//  k-contiguous operand (rows = M or N index): row r holds 64 k = 128 B; its
-//    16-byte chunk kc sits at chunk position kc ^ (r & 7).  A fragment row
-//    is one ds_read_b128.
+// Operands stream through a ring of NS = 4 LDS stages of one k-step (32) each
+// (32 KB per stage, 128 KB in all), filled with 16-byte global -> LDS DMA.
+// The DMA for k-step kt+4 is issued while k-step kt runs, so every load has
+// three k-steps (~100 MFMAs per wave) to land.  Per k-step and wave:
+//   k16-step 0: 16 MFMAs, interleaved with the LDS reads of k16-step 1
+//   wait for own DMA of k-step kt+1 (vmcnt(16) leaves kt+2, kt+3 in flight)
+//   and for the LDS reads, barrier (stage kt+1 complete, stage kt free)
+//   k16-step 1: 16 MFMAs, interleaved with the LDS reads of k-step kt+1's
+//   k16-step 0 and the DMA of k-step kt+4 into stage kt
+// Every k-step issues the same number of DMA loads (past the last k-step the
+// last one is loaded again into an unused stage) so vmcnt counting is uniform;
+// the ring is drained (vmcnt(0)) before a block moves to its next tile.
+//
+// Tile order: tiles are numbered with the n-tile fastest (M-ragged kinds:
+// m-tiles enumerated group by group; K-ragged kinds: group, m-tile, n-tile).
+// Workgroups are dealt to the 8 XCDs round-robin by id, so block b works on
+// tiles of the contiguous range assigned to XCD b % 8: the ~32 tiles an XCD
+// runs at a time share their operand panels in that XCD's L2.
+//
+// LDS layouts (per operand and stage, 16 KB):
+//  k-contiguous operand (rows = M or N index): row r holds 32 k = 64 B; its
+//    16-byte chunk kc sits at chunk position kc ^ ((r >> 2) & 3), so the 16
+//    lanes of one ds_read_b128 pass (16 consecutive rows, same kc) hit 16
+//    distinct 16-byte bank groups of the 64-bank LDS.
 //  m/n-contiguous operand (rows = k): row k holds 256 m = 512 B; its 32-byte
 //    chunk c sits at position c ^ (2 * (k & 3)).  A fragment is two
 //    ds_read_b64_tr_b16: in each 16-lane group, lane j points at (k0 + j/4,
 //    m0 + 4*(j%4)) and lane i receives m0 + i for k0..k0+3.
-// Rows outside the valid range are clamped to a valid row (finite data) and
-// the corresponding outputs are not stored; in the ragged-K tail the B
-// fragment elements past the group's last row are zeroed in registers.
+// The MFMA is issued with the B fragment as its first operand, so lane l
+// accumulates C[m0 + l%32][n0 + 8q + 4(l/32) + t] in register 4q + t: four
+// consecutive output columns per lane, stored with 8- or 16-byte vectors.
+// Out-of-range M/N rows are clamped to valid memory (their outputs are not
+// stored); k-rows past a group's last row (ragged K) are loaded from a
+// 16-byte zero block, so they contribute exactly 0.
 
 constexpr int GT = 256;                     // block tile (M and N)
-constexpr int GK = 64;                      // k-step
-constexpr int OP_BYTES = GT * GK * 2;       // one operand stage: 32 KB
-constexpr int LDS_BYTES = 4 * OP_BYTES;     // 2 stages x (A, B)
+constexpr int GK = 32;                      // k-step
+constexpr int NS = 4;                       // LDS ring stages
+constexpr int OP_BYTES = GT * GK * 2;       // one operand of one stage: 16 KB
+constexpr int STAGE_BYTES = 2 * OP_BYTES;   // A then B
+constexpr int LDS_BYTES = NS * STAGE_BYTES;
+constexpr int DMA_PER_OP = OP_BYTES / 1024 / 4;  // 16-byte DMA loads per wave per operand
+constexpr int N_XCD = 8;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8_t;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
 
+__device__ const u32x4_t kZero16 = {0u, 0u, 0u, 0u};
+
+// s_waitcnt immediate (gfx9 family): vmcnt in bits [3:0] and [15:14],
+// expcnt in [6:4], lgkmcnt in [11:8]; a field at its maximum does not wait.
+constexpr int waitcnt_imm(int vm, int lgkm) {
+  return (vm & 15) | (((vm >> 4) & 3) << 14) | (7 << 4) | ((lgkm & 15) << 8);
+}
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(waitcnt_imm((n), 15))
+#define WAIT_LGKMCNT(n) __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, (n)))
+
+// 16-byte global -> LDS DMA: lane l writes lds_base + 16 l (lds_base must be
+// wave-uniform).  Issued as inline asm so the compiler does not treat every
+// later LDS read as possibly aliasing the pending DMA (it would wait for all
+// outstanding global loads before each transposing read); the kernel waits for
+// the DMA explicitly (vmcnt) before the barrier that publishes a stage.
 DEVI void load_to_lds(const bf16_t* g, char* lds_base) {
-  __builtin_amdgcn_global_load_lds((glb_void_t*)g, (lds_void_t*)lds_base, 16, 0, 0);
+  const unsigned m0 = (unsigned)(uintptr_t)(lds_void_t*)lds_base;
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0)
+               : "m0", "memory");
 }
 
-// k-contiguous fill: wave w issues loads i = 0..7, load q = 4i + w covers rows
-// 8q .. 8q+7; lane l writes chunk position l%8 of row 8q + l/8.
+// Per-lane global addresses of the DMA loads a wave issues per operand and
+// k-step.  k-contiguous operand: load q = 4i + w covers rows 16q .. 16q+15,
+// lane l writes chunk position l%4 of row 16q + l/4.  m/n-contiguous operand:
+// load q covers k-rows 2q, 2q+1 (512 B each), lane l writes 16-byte slot l%32
+// of row 2q + l/32.
+struct DmaPtrs {
+  const bf16_t* p[DMA_PER_OP];
+};
+
+DEVI int kc_swz(int r) { return (r >> 2) & 3; }
+
 template <class RowPtr>
-DEVI void fill_kc(char* lds_op, const RowPtr& row_ptr, int k0) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int kc = (lane & 7) ^ ((lane >> 3) & 7);
+DEVI void dma_kc_init(DmaPtrs& d, const RowPtr& row_ptr, int w) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = i * 4 + w;
-    const int row = q * 8 + (lane >> 3);
-    load_to_lds(row_ptr(row) + k0 + kc * 8, lds_op + q * 1024);
+  for (int i = 0; i < DMA_PER_OP; ++i) {
+    const int row = (i * 4 + w) * 16 + (lane >> 2);
+    d.p[i] = row_ptr(row) + ((lane & 3) ^ kc_swz(row)) * 8;
   }
 }
 
-// m/n-contiguous fill: load q covers k-rows 2q, 2q+1 (512 B each); lane l
-// writes the 16-byte slot l%32 of row 2q + l/32.
+DEVI int mn_row(int i, int w) { return (i * 4 + w) * 2 + ((threadIdx.x & 63) >> 5); }
+DEVI int mn_col(int row) {
+  const int ps = threadIdx.x & 31;
+  return (((ps >> 1) ^ (2 * (row & 3))) * 16) + (ps & 1) * 8;
+}
+
 template <class ElemPtr>
-DEVI void fill_mn(char* lds_op, const ElemPtr& elem_ptr, int k0) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int ps = lane & 31;
+DEVI void dma_mn_init(DmaPtrs& d, const ElemPtr& elem_ptr, int w, int k0) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = i * 4 + w;
-    const int row = q * 2 + (lane >> 5);
-    const int c = (ps >> 1) ^ (2 * (row & 3));
-    load_to_lds(elem_ptr(k0 + row, c * 16 + (ps & 1) * 8), lds_op + q * 1024);
+  for (int i = 0; i < DMA_PER_OP; ++i) {
+    const int row = mn_row(i, w);
+    d.p[i] = elem_ptr(k0 + row, mn_col(row));
   }
 }
 
@@ -300,7 +350,7 @@ DEVI bf16x8_t frag_kc(const char* lds_op, int mb, int s) {
   const int lane = threadIdx.x & 63;
   const int row = mb + (lane & 31);
   const int kc = s * 2 + (lane >> 5);
-  return *reinterpret_cast<const bf16x8_t*>(lds_op + row * 128 + ((kc ^ (row & 7)) << 4));
+  return *reinterpret_cast<const bf16x8_t*>(lds_op + row * 64 + ((kc ^ kc_swz(row)) << 4));
 }
 
 // same fragment from the m/n-contiguous layout with two transposing reads
@@ -322,139 +372,322 @@ DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
   return __builtin_bit_cast(bf16x8_t, both);
 }
 
+DEVI void store4(bf16_t* p, const float* v) {
+  bf16x4_t o = {(bf16_t)v[0], (bf16_t)v[1], (bf16_t)v[2], (bf16_t)v[3]};
+  *reinterpret_cast<bf16x4_t*>(p) = o;
+}
+DEVI void load4(const bf16_t* p, float* v) {
+  const bf16x4_t x = *reinterpret_cast<const bf16x4_t*>(p);
+  v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
+}
+
+// Number of tiles of the launch and the tile with linear index t.
 template <int KIND>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
-  using K_ = Kind<KIND>;
-  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
-  Tile tl;
-  if (!decode_tile<GT, GT, KIND>(a, tl)) return;
-  const bf16_t* A = static_cast<const bf16_t*>(a.A);
-  const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
-  const int Kd = K_::MRAG ? a.K : tl.rows;
-  const int nk = (Kd + GK - 1) / GK;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int tile_n = blockIdx.x;
-  const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
-
-  // operand pointers; out-of-range indices are clamped to valid memory
-  auto a_row = [&](int r) -> const bf16_t* {  // M-ragged A, k-contiguous
-    return A + (size_t)min(tl.row0 + r, last_row) * a.lda;
-  };
-  auto a_elem = [&](int k, int c) -> const bf16_t* {  // TN A(i = m0 + c, k)
-    const int m = (tl.m0 + c + 8 <= a.M) ? tl.m0 + c : 0;
-    return A + (size_t)min(tl.row0 + k, last_row) * a.lda + m;
-  };
-  auto b_row = [&](int r) -> const bf16_t* {  // NT B rows
-    if constexpr (KIND == GU_FWD) {
-      bool ok;
-      int br = gu_brow<GT>(tile_n, r, a.H, ok);
-      if (!ok) br = 0;
-      return B + (size_t)br * a.ldb;
-    } else {
-      return B + (size_t)min(tl.n0 + r, a.N - 1) * a.ldb;
+DEVI int tile_count(const GemmArgs& a, int n_tiles) {
+  if constexpr (Kind<KIND>::MRAG) {
+    int tiles = 0;
+    int b = clamp_row(a.offsets[0], a.cap);
+    for (int g = 0; g < a.n_groups; ++g) {
+      int e = clamp_row(a.offsets[g + 1], a.cap);
+      if (e < b) e = b;
+      tiles += (e - b + GT - 1) / GT;
+      b = e;
     }
-  };
-  auto b_elem = [&](int k, int c) -> const bf16_t* {  // NN / TN B(k, n = n0 + c)
-    const int n = (tl.n0 + c + 8 <= a.N) ? tl.n0 + c : 0;
-    if constexpr (K_::MRAG) return B + (size_t)k * a.ldb + n;
-    else return B + (size_t)min(tl.row0 + k, last_row) * a.ldb + n;
-  };
-
-  auto fill = [&](int kt, int buf) {
-    char* la = lds + buf * 2 * OP_BYTES;
-    char* lb = la + OP_BYTES;
-    const int k0 = kt * GK;
-    if constexpr (K_::A_KC) fill_kc(la, a_row, k0); else fill_mn(la, a_elem, k0);
-    if constexpr (K_::B_KC) fill_kc(lb, b_row, k0); else fill_mn(lb, b_elem, k0);
-  };
-
-  f32x16_t acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-
-  if (nk > 0) {
-    fill(0, 0);
-    __builtin_amdgcn_s_waitcnt(0x0);  // vmcnt(0) expcnt(0) lgkmcnt(0)
-    __syncthreads();
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) fill(kt + 1, cur ^ 1);
-    const char* la = lds + cur * 2 * OP_BYTES;
-    const char* lb = la + OP_BYTES;
-    const bool tail = !K_::MRAG && (kt + 1) * GK > Kd;
-#pragma unroll
-    for (int s = 0; s < GK / 16; ++s) {
-      bf16x8_t af[4], bfr[4];
-#pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        af[f] = K_::A_KC ? frag_kc(la, wm * 128 + f * 32, s) : frag_mn(la, wm * 128 + f * 32, s);
-        bfr[f] = K_::B_KC ? frag_kc(lb, wn * 128 + f * 32, s) : frag_mn(lb, wn * 128 + f * 32, s);
-      }
-      if (tail) {  // zero B past the group's last row (A there is finite)
-        const int kbase = kt * GK + s * 16 + 8 * (lane >> 5);
-#pragma unroll
-        for (int f = 0; f < 4; ++f)
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (kbase + e >= Kd) bfr[f][e] = (bf16_t)0.0f;
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    __builtin_amdgcn_s_waitcnt(0x0);
-    __syncthreads();
-  }
-
-  // accumulator (i, j) register r holds C[row, col] with
-  //   row = (r/4)*8 + (lane/32)*4 + r%4,  col = lane%32  inside its 32x32 tile
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-      if constexpr (KIND == GU_FWD) {
-        // tiles (i, 2p) = gate and (i, 2p+1) = up of hidden units h
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const int h = tile_n * (GT / 2) + (2 * wn + p) * 32 + (lane & 31);
-          epi_swiglu<bf16_t>(a, tl, row, h, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = wn * 128 + j * 32 + (lane & 31);
-          epi_store<KIND, bf16_t>(a, tl, row, col, acc[i][j][r]);
-        }
-      }
-    }
+    return tiles * n_tiles;
+  } else {
+    return a.n_groups * ((a.M + GT - 1) / GT) * n_tiles;
   }
 }
 
 template <int KIND>
+DEVI void tile_decode(const GemmArgs& a, int t, int n_tiles, Tile& tl, int& tile_n) {
+  tile_n = t % n_tiles;
+  tl.n0 = tile_n * GT;
+  const int q = t / n_tiles;
+  if constexpr (Kind<KIND>::MRAG) {
+    int mt = q;
+    int b = clamp_row(a.offsets[0], a.cap);
+    for (int g = 0; g < a.n_groups; ++g) {
+      int e = clamp_row(a.offsets[g + 1], a.cap);
+      if (e < b) e = b;
+      const int tiles = (e - b + GT - 1) / GT;
+      if (mt < tiles) {
+        tl.g = g;
+        tl.row0 = b + mt * GT;
+        tl.rows = min(GT, e - tl.row0);
+        tl.m0 = 0;
+        return;
+      }
+      mt -= tiles;
+      b = e;
+    }
+    tl.g = 0; tl.row0 = 0; tl.rows = 0; tl.m0 = 0;  // not reached for t < count
+  } else {
+    const int m_tiles = (a.M + GT - 1) / GT;
+    tl.g = q / m_tiles;
+    tl.m0 = (q % m_tiles) * GT;
+    const int b = clamp_row(a.offsets[tl.g], a.cap);
+    const int e = clamp_row(a.offsets[tl.g + 1], a.cap);
+    tl.row0 = b;
+    tl.rows = e > b ? e - b : 0;
+  }
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
+  using K_ = Kind<KIND>;
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const bf16_t* zero16 = reinterpret_cast<const bf16_t*>(&kZero16);
+  const int n_tiles = ((KIND == GU_FWD ? 2 * a.H : a.N) + GT - 1) / GT;
+  const int total = tile_count<KIND>(a, n_tiles);
+  // XCD-aware assignment (the grid is a multiple of N_XCD blocks)
+  const int per_xcd = gridDim.x / N_XCD;
+  const int xcd = blockIdx.x % N_XCD;
+  const int t_lo = (int)((long)total * xcd / N_XCD);
+  const int t_hi = (int)((long)total * (xcd + 1) / N_XCD);
+
+  for (int t = t_lo + (int)(blockIdx.x / N_XCD); t < t_hi; t += per_xcd) {
+    Tile tl;
+    int tile_n;
+    tile_decode<KIND>(a, t, n_tiles, tl, tile_n);
+    const bf16_t* A = static_cast<const bf16_t*>(a.A);
+    const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
+    const int Kd = K_::MRAG ? a.K : tl.rows;
+    const int nk = (Kd + GK - 1) / GK;
+    const int n_full = Kd / GK;  // k-steps without a ragged tail
+    const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
+
+    // operand pointers; out-of-range M/N indices are clamped to valid memory
+    // (outputs not stored), out-of-range k-rows read zeros
+    auto a_row = [&](int r) -> const bf16_t* {  // M-ragged A, k-contiguous
+      return A + (size_t)min(tl.row0 + r, last_row) * a.lda;
+    };
+    auto a_elem = [&](int k, int c) -> const bf16_t* {  // TN A(i = m0 + c, k)
+      if (k >= Kd) return zero16;
+      const int m = (tl.m0 + c + 8 <= a.M) ? tl.m0 + c : 0;
+      return A + (size_t)(tl.row0 + k) * a.lda + m;
+    };
+    auto b_row = [&](int r) -> const bf16_t* {  // NT B rows
+      if constexpr (KIND == GU_FWD) {
+        bool ok;
+        int br = gu_brow<GT>(tile_n, r, a.H, ok);
+        if (!ok) br = 0;
+        return B + (size_t)br * a.ldb;
+      } else {
+        return B + (size_t)min(tl.n0 + r, a.N - 1) * a.ldb;
+      }
+    };
+    auto b_elem = [&](int k, int c) -> const bf16_t* {  // NN / TN B(k, n = n0 + c)
+      const int n = (tl.n0 + c + 8 <= a.N) ? tl.n0 + c : 0;
+      if constexpr (K_::MRAG) {
+        return B + (size_t)k * a.ldb + n;
+      } else {
+        if (k >= Kd) return zero16;
+        return B + (size_t)(tl.row0 + k) * a.ldb + n;
+      }
+    };
+
+    // DMA addresses at k-step 0 (k-contiguous operands advance by GK
+    // elements, m/n-contiguous ones by GK rows per k-step) and of the ragged
+    // tail k-step
+    DmaPtrs da, db, ta, tb;
+    if constexpr (K_::A_KC) dma_kc_init(da, a_row, wave); else dma_mn_init(da, a_elem, wave, 0);
+    if constexpr (K_::B_KC) dma_kc_init(db, b_row, wave); else dma_mn_init(db, b_elem, wave, 0);
+    if constexpr (!K_::MRAG) {
+      dma_mn_init(ta, a_elem, wave, n_full * GK);
+      dma_mn_init(tb, b_elem, wave, n_full * GK);
+    }
+    const long a_step = K_::A_KC ? GK : (long)GK * a.lda;
+    const long b_step = K_::B_KC ? GK : (long)GK * a.ldb;
+
+    // DMA load i (of DMA_PER_OP) of both operands for k-step ks into stage st
+    auto dma = [&](int ks, int st, int i) {
+      char* la = lds + st * STAGE_BYTES;
+      const bool tail = !K_::MRAG && ks >= n_full;
+      const bf16_t* pa = da.p[i] + ks * a_step;
+      const bf16_t* pb = db.p[i] + ks * b_step;
+      if constexpr (!K_::MRAG) {
+        pa = tail ? ta.p[i] : pa;
+        pb = tail ? tb.p[i] : pb;
+      }
+      load_to_lds(pa, la + (i * 4 + wave) * 1024);
+      load_to_lds(pb, la + OP_BYTES + (i * 4 + wave) * 1024);
+    };
+
+    auto read_frag = [&](const char* stage, int s, int idx, bf16x8_t* af, bf16x8_t* bfr) {
+      // idx 0..3: A fragment idx; 4..7: B fragment idx-4
+      if (idx < 4) {
+        af[idx] = K_::A_KC ? frag_kc(stage, wm * 128 + idx * 32, s)
+                           : frag_mn(stage, wm * 128 + idx * 32, s);
+      } else {
+        const int f = idx - 4;
+        const char* lb = stage + OP_BYTES;
+        bfr[f] = K_::B_KC ? frag_kc(lb, wn * 128 + f * 32, s) : frag_mn(lb, wn * 128 + f * 32, s);
+      }
+    };
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+
+    // One k16-step: 16 MFMAs on (A_c, B_c) in 8 chunks of two; chunk q also
+    // reads fragment q of the next k16-step (from stage_n) into (A_n, B_n)
+    // and, for q < DMA_PER_OP when dma_ks >= 0, issues DMA load q of k-step
+    // dma_ks into stage dma_st.  sched_barrier(0) fences keep this order, so
+    // each fragment read has a whole k16-step to land and the compiler's waits
+    // fall at the first use in the next k16-step.
+    auto kstep = [&](const bf16x8_t* A_c, const bf16x8_t* B_c, const char* stage_n, int s_n,
+                     bf16x8_t* A_n, bf16x8_t* B_n, int dma_ks, int dma_st) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (dma_ks >= 0 && q < DMA_PER_OP) dma(dma_ks, dma_st, q);
+        read_frag(stage_n, s_n, q, A_n, B_n);
+        const int i = q >> 1, j0 = 2 * (q & 1);
+        acc[i][j0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_c[j0], A_c[i], acc[i][j0], 0, 0, 0);
+        acc[i][j0 + 1] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_c[j0 + 1], A_c[i], acc[i][j0 + 1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+
+    bf16x8_t af0[4], bf0[4], af1[4], bf1[4];
+    if (nk > 0) {
+#pragma unroll
+      for (int p = 0; p < NS; ++p)
+#pragma unroll
+        for (int i = 0; i < DMA_PER_OP; ++i) dma(min(p, nk - 1), p, i);
+      // own DMA of k-step 0 done (3 k-steps' loads may stay in flight)
+      WAIT_VMCNT(2 * DMA_PER_OP * (NS - 1));
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 8; ++q) read_frag(lds, 0, q, af0, bf0);
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+      const int st = kt % NS;
+      const char* stage = lds + st * STAGE_BYTES;
+      const char* stage_next = lds + ((kt + 1) % NS) * STAGE_BYTES;
+      kstep(af0, bf0, stage, 1, af1, bf1, -1, 0);
+      WAIT_LGKMCNT(0);
+      WAIT_VMCNT(2 * DMA_PER_OP * (NS - 2));
+      __syncthreads();
+      kstep(af1, bf1, stage_next, 0, af0, bf0, min(kt + NS, nk - 1), st);
+    }
+    WAIT_VMCNT(0);  // drain the ring before the next tile
+
+    // epilogue: accumulator (i, j) register 4q + t holds
+    //   C[wm*128 + 32i + lane%32][wn*128 + 32j + 8q + 4(lane/32) + t]
+    const int r_in = lane & 31;
+    const int c_in = 4 * (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = wm * 128 + i * 32 + r_in;  // tile row
+      const bool row_ok = K_::MRAG ? row < tl.rows : tl.m0 + row < a.M;
+      if (!row_ok) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (KIND == GU_FWD) {
+          // fragments (i, 2p) = gate, (i, 2p+1) = up of hidden units h..h+3
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {
+            const int h = tile_n * (GT / 2) + (2 * wn + p) * 32 + 8 * q + c_in;
+            if (h >= a.H) continue;
+            const size_t m = (size_t)(tl.row0 + row);
+            float G[4], U[4], Hh[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              G[e] = acc[i][2 * p][4 * q + e];
+              U[e] = acc[i][2 * p + 1][4 * q + e];
+              Hh[e] = silu_f(G[e]) * U[e];
+            }
+            bf16_t* gu = static_cast<bf16_t*>(a.C);
+            store4(gu + m * 2 * a.H + h, G);
+            store4(gu + m * 2 * a.H + a.H + h, U);
+            store4(static_cast<bf16_t*>(a.out2) + m * a.H + h, Hh);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int col = tl.n0 + wn * 128 + j * 32 + 8 * q + c_in;
+            if (col >= a.N) continue;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+            if constexpr (KIND == DOWN_FWD || KIND == DX_BWD) {
+              store4(static_cast<bf16_t*>(a.C) + (size_t)(tl.row0 + row) * a.ldc + col, v);
+            } else if constexpr (KIND == DHH_BWD) {
+              const size_t m = (size_t)(tl.row0 + row);
+              const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
+              float G[4], U[4], dG[4], dU[4];
+              load4(gu + m * 2 * a.H + col, G);
+              load4(gu + m * 2 * a.H + a.H + col, U);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                dG[e] = v[e] * U[e] * dsilu_f(G[e]);
+                dU[e] = v[e] * silu_f(G[e]);
+              }
+              bf16_t* dgu = static_cast<bf16_t*>(a.C);
+              store4(dgu + m * 2 * a.H + col, dG);
+              store4(dgu + m * 2 * a.H + a.H + col, dU);
+            } else {  // DWD / DWGU: fp32 weight gradient of group g
+              float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
+                         (size_t)(tl.m0 + row) * a.ldc + col;
+              f32x4_t o = {v[0], v[1], v[2], v[3]};
+              if (a.accumulate) o += *reinterpret_cast<const f32x4_t*>(c);
+              *reinterpret_cast<f32x4_t*>(c) = o;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();  // LDS is reused by the next tile
+  }
+}
+
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+template <int KIND>
 hipError_t run_gemm(const GemmArgs& a, int bf16, hipStream_t s) {
-  const int BMt = bf16 ? GT : 64, BNt = bf16 ? GT : 64;
-  dim3 grid;
+  static constexpr const char* names[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
+                                          "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
   const int ncols = (KIND == GU_FWD) ? 2 * a.H : a.N;
-  grid.x = ceil_div(ncols, BNt);
+  if (bf16) {
+    // persistent: at most one block per CU, a multiple of N_XCD blocks
+    const long n_tiles = ceil_div(ncols, GT);
+    const long max_tiles = Kind<KIND>::MRAG ? (ceil_div(a.cap, GT) + (long)a.n_groups) * n_tiles
+                                            : (long)a.n_groups * ceil_div(a.M, GT) * n_tiles;
+    if (max_tiles == 0) return hipSuccess;
+    long blocks = std::min<long>(num_cus(), max_tiles);
+    blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
+    MOE_TIMED(names[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(a));
+    return hipGetLastError();
+  }
+  dim3 grid;
+  grid.x = ceil_div(ncols, 64);
   if (Kind<KIND>::MRAG) {
-    grid.y = ceil_div(a.cap, BMt) + a.n_groups;
+    grid.y = ceil_div(a.cap, 64) + a.n_groups;
     grid.z = 1;
   } else {
-    grid.y = ceil_div(a.M, BMt);
+    grid.y = ceil_div(a.M, 64);
     grid.z = a.n_groups;
   }
   if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
-  static constexpr const char* names[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
-                                          "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
-  if (bf16) MOE_TIMED(names[KIND], s, gemm_bf16_kernel<KIND><<<grid, 256, 0, s>>>(a));
-  else MOE_TIMED(names[KIND], s, gemm_f32_kernel<KIND><<<grid, 256, 0, s>>>(a));
+  MOE_TIMED(names[KIND], s, gemm_f32_kernel<KIND><<<grid, 256, 0, s>>>(a));
   return hipGetLastError();
 }
 
