@@ -74,6 +74,9 @@ def lib(path: str | None = None):
         if not os.path.exists(p):
             raise RuntimeError(f"{p} is missing: build it with __graft_entry__.build() "
                                "or python -m paper_2606_19025_amd.build")
+        # torch first: the library must bind to the HIP runtime torch already
+        # initialised (one runtime per process)
+        import torch  # noqa: F401
         handle = C.CDLL(p)
         for name, (res, args) in _SIGS.items():
             f = getattr(handle, name)

@@ -251,11 +251,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // last one is loaded again into an unused stage) so vmcnt counting is uniform;
 // the ring is drained (vmcnt(0)) before a block moves to its next tile.
 //
-// Tile order: tiles are numbered with the n-tile fastest (M-ragged kinds:
-// m-tiles enumerated group by group; K-ragged kinds: group, m-tile, n-tile).
-// Workgroups are dealt to the 8 XCDs round-robin by id, so block b works on
-// tiles of the contiguous range assigned to XCD b % 8: the ~32 tiles an XCD
-// runs at a time share their operand panels in that XCD's L2.
+// Tile order (see tile_decode): bands of GROUP_M m-tiles.  Workgroups are
+// dealt to the 8 XCDs round-robin by id, so block b works on tiles of the
+// contiguous range assigned to XCD b % 8: the 32 tiles an XCD runs at a time
+// form a GROUP_M x 8 rectangle whose operand panels its L2 serves.
 //
 // LDS layouts (per operand and stage, 16 KB):
 //  k-contiguous operand (rows = M or N index): row r holds 32 k = 64 B; its
@@ -381,9 +380,16 @@ DEVI void load4(const bf16_t* p, float* v) {
   v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
 }
 
-// Number of tiles of the launch and the tile with linear index t.
+// Tile enumeration.  Output tiles form an m_tiles x n_tiles grid (M-ragged
+// kinds: m-tiles of all groups in group order; K-ragged kinds: (group,
+// m-tile) pairs).  Linear tile t walks bands of GROUP_M m-tiles: inside a band
+// m varies fastest, then n, so any 32 consecutive tiles cover a GROUP_M x
+// (32 / GROUP_M) rectangle and share GROUP_M A panels and 32 / GROUP_M B
+// panels in L2.
+constexpr int GROUP_M = 4;
+
 template <int KIND>
-DEVI int tile_count(const GemmArgs& a, int n_tiles) {
+DEVI int m_tile_count(const GemmArgs& a) {
   if constexpr (Kind<KIND>::MRAG) {
     int tiles = 0;
     int b = clamp_row(a.offsets[0], a.cap);
@@ -393,17 +399,22 @@ DEVI int tile_count(const GemmArgs& a, int n_tiles) {
       tiles += (e - b + GT - 1) / GT;
       b = e;
     }
-    return tiles * n_tiles;
+    return tiles;
   } else {
-    return a.n_groups * ((a.M + GT - 1) / GT) * n_tiles;
+    return a.n_groups * ((a.M + GT - 1) / GT);
   }
 }
 
 template <int KIND>
-DEVI void tile_decode(const GemmArgs& a, int t, int n_tiles, Tile& tl, int& tile_n) {
-  tile_n = t % n_tiles;
+DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& tl,
+                      int& tile_n) {
+  const int band = t / (GROUP_M * n_tiles);
+  const int first_m = band * GROUP_M;
+  const int band_m = min(GROUP_M, m_tiles - first_m);
+  const int r = t - band * GROUP_M * n_tiles;
+  const int q = first_m + r % band_m;  // m-tile
+  tile_n = r / band_m;
   tl.n0 = tile_n * GT;
-  const int q = t / n_tiles;
   if constexpr (Kind<KIND>::MRAG) {
     int mt = q;
     int b = clamp_row(a.offsets[0], a.cap);
@@ -423,9 +434,9 @@ DEVI void tile_decode(const GemmArgs& a, int t, int n_tiles, Tile& tl, int& tile
     }
     tl.g = 0; tl.row0 = 0; tl.rows = 0; tl.m0 = 0;  // not reached for t < count
   } else {
-    const int m_tiles = (a.M + GT - 1) / GT;
-    tl.g = q / m_tiles;
-    tl.m0 = (q % m_tiles) * GT;
+    const int mt_per_g = (a.M + GT - 1) / GT;
+    tl.g = q / mt_per_g;
+    tl.m0 = (q % mt_per_g) * GT;
     const int b = clamp_row(a.offsets[tl.g], a.cap);
     const int e = clamp_row(a.offsets[tl.g + 1], a.cap);
     tl.row0 = b;
@@ -442,7 +453,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   const int wm = wave >> 1, wn = wave & 1;
   const bf16_t* zero16 = reinterpret_cast<const bf16_t*>(&kZero16);
   const int n_tiles = ((KIND == GU_FWD ? 2 * a.H : a.N) + GT - 1) / GT;
-  const int total = tile_count<KIND>(a, n_tiles);
+  const int m_tiles = m_tile_count<KIND>(a);
+  const int total = m_tiles * n_tiles;
   // XCD-aware assignment (the grid is a multiple of N_XCD blocks)
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
@@ -452,7 +464,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   for (int t = t_lo + (int)(blockIdx.x / N_XCD); t < t_hi; t += per_xcd) {
     Tile tl;
     int tile_n;
-    tile_decode<KIND>(a, t, n_tiles, tl, tile_n);
+    tile_decode<KIND>(a, t, m_tiles, n_tiles, tl, tile_n);
     const bf16_t* A = static_cast<const bf16_t*>(a.A);
     const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
     const int Kd = K_::MRAG ? a.K : tl.rows;
