@@ -380,6 +380,37 @@ DEVI void load4(const bf16_t* p, float* v) {
   v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
 }
 
+// Epilogue staging.  A wave's 128x128 bf16 sub-tile occupies 128 rows of
+// 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
+// the key is a bijection on r mod 32, so the accumulator writes (32 rows at
+// one unit per half-wave) hit 32 distinct bank pairs, and rows 2m, 2m+1
+// differ in key bit 3, so the SwiGLU reads (8 chunks of two rows per 16
+// lanes) fall on disjoint chunks.  A 16-byte chunk c is read back from chunk
+// c ^ (key >> 1), halves swapped when the key is odd.
+constexpr int EPI_WAVE_BYTES = 128 * 256;
+static_assert(4 * EPI_WAVE_BYTES <= LDS_BYTES, "epilogue staging exceeds the ring");
+
+DEVI int epi_key(int r) { return ((r & 1) << 3) | ((r >> 1) & 7) | (r & 16); }
+
+DEVI void epi_put(char* reg, int row, int u, float v0, float v1, float v2, float v3) {
+  bf16x4_t o = {(bf16_t)v0, (bf16_t)v1, (bf16_t)v2, (bf16_t)v3};
+  *reinterpret_cast<bf16x4_t*>(reg + row * 256 + ((u ^ epi_key(row)) << 3)) = o;
+}
+
+DEVI bf16x8_t epi_get(const char* reg, int row, int c) {
+  const int key = epi_key(row);
+  u32x4_t v = *reinterpret_cast<const u32x4_t*>(reg + row * 256 + ((c ^ (key >> 1)) << 4));
+  if (key & 1) v = __builtin_shufflevector(v, v, 2, 3, 0, 1);
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Hardware exp2 / reciprocal (about 1 ulp of fp32); their results are rounded
+// to bf16.
+DEVI float sigmoid_fast(float g) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.44269504088896341f * g));
+}
+DEVI float silu_fast(float g) { return g * sigmoid_fast(g); }
+
 // Tile enumeration.  Output tiles form an m_tiles x n_tiles grid (M-ragged
 // kinds: m-tiles of all groups in group order; K-ragged kinds: (group,
 // m-tile) pairs).  Linear tile t walks bands of GROUP_M m-tiles: inside a band
@@ -593,64 +624,118 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 
     // epilogue: accumulator (i, j) register 4q + t holds
     //   C[wm*128 + 32i + lane%32][wn*128 + 32j + 8q + 4(lane/32) + t]
-    const int r_in = lane & 31;
-    const int c_in = 4 * (lane >> 5);
+    if constexpr (KIND == DWD || KIND == DWGU) {
+      // fp32 weight gradient of group g, 16 bytes per lane straight from the
+      // accumulators
+      const int r_in = lane & 31;
+      const int c_in = 4 * (lane >> 5);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = wm * 128 + i * 32 + r_in;  // tile row
-      const bool row_ok = K_::MRAG ? row < tl.rows : tl.m0 + row < a.M;
-      if (!row_ok) continue;
+      for (int i = 0; i < 4; ++i) {
+        const int row = wm * 128 + i * 32 + r_in;
+        if (tl.m0 + row >= a.M) continue;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if constexpr (KIND == GU_FWD) {
-          // fragments (i, 2p) = gate, (i, 2p+1) = up of hidden units h..h+3
-#pragma unroll
-          for (int p = 0; p < 2; ++p) {
-            const int h = tile_n * (GT / 2) + (2 * wn + p) * 32 + 8 * q + c_in;
-            if (h >= a.H) continue;
-            const size_t m = (size_t)(tl.row0 + row);
-            float G[4], U[4], Hh[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              G[e] = acc[i][2 * p][4 * q + e];
-              U[e] = acc[i][2 * p + 1][4 * q + e];
-              Hh[e] = silu_f(G[e]) * U[e];
-            }
-            bf16_t* gu = static_cast<bf16_t*>(a.C);
-            store4(gu + m * 2 * a.H + h, G);
-            store4(gu + m * 2 * a.H + a.H + h, U);
-            store4(static_cast<bf16_t*>(a.out2) + m * a.H + h, Hh);
-          }
-        } else {
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int col = tl.n0 + wn * 128 + j * 32 + 8 * q + c_in;
             if (col >= a.N) continue;
-            float v[4];
+            float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
+                       (size_t)(tl.m0 + row) * a.ldc + col;
+            f32x4_t o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                         acc[i][j][4 * q + 3]};
+            if (a.accumulate) o += *reinterpret_cast<const f32x4_t*>(c);
+            *reinterpret_cast<f32x4_t*>(c) = o;
+          }
+      }
+    } else {
+      // bf16 outputs go through LDS so that every global access is a whole
+      // 16-byte chunk and a wave instruction covers 256 contiguous bytes of a
+      // row (4 rows) instead of 16 bytes of 32 rows.  Each wave transposes its
+      // 128x128 sub-tile in a private 32 KB region (the drained ring).
+      __syncthreads();  // every wave is done with the ring
+      char* reg = lds + wave * EPI_WAVE_BYTES;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-            if constexpr (KIND == DOWN_FWD || KIND == DX_BWD) {
-              store4(static_cast<bf16_t*>(a.C) + (size_t)(tl.row0 + row) * a.ldc + col, v);
-            } else if constexpr (KIND == DHH_BWD) {
-              const size_t m = (size_t)(tl.row0 + row);
-              const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
-              float G[4], U[4], dG[4], dU[4];
-              load4(gu + m * 2 * a.H + col, G);
-              load4(gu + m * 2 * a.H + a.H + col, U);
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                dG[e] = v[e] * U[e] * dsilu_f(G[e]);
-                dU[e] = v[e] * silu_f(G[e]);
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = i * 32 + (lane & 31);
+            const int u = 8 * j + 2 * q + (lane >> 5);
+            epi_put(reg, row, u, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                    acc[i][j][4 * q + 3]);
+          }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region is wave-private
+      const int row_lim = tl.rows - wm * 128;  // rows of this wave's sub-tile to store
+      if constexpr (KIND == GU_FWD) {
+        // region row: [G h0..31 | U h0..31 | G h32..63 | U h32..63] of the
+        // wave's 64 hidden units; lane -> (row, 8 hidden units)
+        const int h = tile_n * (GT / 2) + wn * 64 + 32 * ((lane & 7) >> 2) + 8 * (lane & 3);
+        const int cg = 8 * ((lane & 7) >> 2) + (lane & 3);
+        bf16_t* gu = static_cast<bf16_t*>(a.C);
+        bf16_t* hh = static_cast<bf16_t*>(a.out2);
+        if (h < a.H) {
+#pragma unroll 4
+          for (int it = 0; it < 16; ++it) {
+            const int row = it * 8 + (lane >> 3);
+            if (row >= row_lim) break;
+            const bf16x8_t G = epi_get(reg, row, cg);
+            const bf16x8_t U = epi_get(reg, row, cg + 4);
+            bf16x8_t Hv;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)(silu_fast((float)G[e]) * (float)U[e]);
+            const size_t m = (size_t)(tl.row0 + wm * 128 + row);
+            *reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + h) = G;
+            *reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + a.H + h) = U;
+            *reinterpret_cast<bf16x8_t*>(hh + m * a.H + h) = Hv;
+          }
+        }
+      } else {
+        const int c = lane & 15;
+        const int col = tl.n0 + wn * 128 + 8 * c;
+        if (col < a.N) {
+          if constexpr (KIND == DHH_BWD) {
+            // dG = dHh * U * silu'(G), dU = dHh * silu(G); G and U of a batch of
+            // rows are loaded before any store of it
+            const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
+            bf16_t* dgu = static_cast<bf16_t*>(a.C);
+            for (int it0 = 0; it0 < 32; it0 += 8) {
+              if (it0 * 4 >= row_lim) break;
+              bf16x8_t G[8], U[8];
+#pragma unroll
+              for (int b = 0; b < 8; ++b) {
+                const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
+                const size_t m = (size_t)(tl.row0 + wm * 128 + row);
+                G[b] = *reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col);
+                U[b] = *reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col);
               }
-              bf16_t* dgu = static_cast<bf16_t*>(a.C);
-              store4(dgu + m * 2 * a.H + col, dG);
-              store4(dgu + m * 2 * a.H + a.H + col, dU);
-            } else {  // DWD / DWGU: fp32 weight gradient of group g
-              float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
-                         (size_t)(tl.m0 + row) * a.ldc + col;
-              f32x4_t o = {v[0], v[1], v[2], v[3]};
-              if (a.accumulate) o += *reinterpret_cast<const f32x4_t*>(c);
-              *reinterpret_cast<f32x4_t*>(c) = o;
+#pragma unroll
+              for (int b = 0; b < 8; ++b) {
+                const int row = (it0 + b) * 4 + (lane >> 4);
+                const bf16x8_t v = epi_get(reg, row, c);
+                bf16x8_t dG, dU;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const float g = (float)G[b][e], dh = (float)v[e];
+                  const float s = sigmoid_fast(g);
+                  dG[e] = (bf16_t)(dh * (float)U[b][e] * (s * (1.0f + g * (1.0f - s))));
+                  dU[e] = (bf16_t)(dh * g * s);
+                }
+                if (row < row_lim) {
+                  const size_t m = (size_t)(tl.row0 + wm * 128 + row);
+                  *reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + col) = dG;
+                  *reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + a.H + col) = dU;
+                }
+              }
+            }
+          } else {  // DOWN_FWD / DX_BWD
+            bf16_t* C = static_cast<bf16_t*>(a.C);
+#pragma unroll 8
+            for (int it = 0; it < 32; ++it) {
+              const int row = it * 4 + (lane >> 4);
+              if (row >= row_lim) break;
+              *reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * 128 + row) * a.ldc + col) =
+                  epi_get(reg, row, c);
             }
           }
         }
