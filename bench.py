@@ -83,8 +83,12 @@ def algorithmic_work(cfg, n, t_act, s):
     w["unpermute"] = ("byte", n * d * s + (T * d * s if Hs else 0) + T * d * s + T * k * 4)
     w["route_dz"] = ("byte", T * k * 12 + T * E * 4)
     w["route_dw_partial"] = ("byte", T * E * 4 + T * d * s)
-    w["route_dw_reduce"] = ("byte", E * d * 4)
+    w["route_dw_reduce"] = ("byte", (-(-T // 256) + 1) * E * d * 4)
     w["route_dx"] = ("byte", T * E * 4 + 2 * T * d * s + E * d * s)
+    # fused bf16 router backward: x, dz and W_r in, dx read-modify-write,
+    # one fp32 dW_r partial per 256-token chunk out
+    w["route_bwd_mfma"] = ("byte", T * E * 4 + 3 * T * d * s + E * d * s
+                           + -(-T // 256) * E * d * 4)
     return w
 
 

@@ -94,7 +94,11 @@ int moe_route_mask(const void* x, const void* w_router, const float* router_bias
  * d_topk_w [T,k] fp32 is dL/dtopk_w (0 for ghost routes, as moe_combine_bwd
  * writes it).  logits is required for MOE_GATE_SOFTMAX and may be NULL
  * otherwise.  accumulate_dx != 0 adds into dx, else overwrites it.
- * ws: device workspace of at least moe_route_bwd_workspace_size(T, d, E) bytes.
+ * ws: device workspace (16-byte aligned) of at least
+ * moe_route_bwd_workspace_size(T, d, E) bytes.  In bf16 with E <= 64 and
+ * d % 128 == 0 the fp32 dz enters the MFMA products as a bf16 pair hi + lo
+ * (relative error <= 2^-17 per element); otherwise the sums run in fp32 FMA.
+ * Every sum is taken in a fixed order, so results are run-to-run identical.
  */
 size_t moe_route_bwd_workspace_size(int T, int d, int E);
 int moe_route_bwd(const void* x, const void* w_router, int dtype, int T, int d, int E, int k,

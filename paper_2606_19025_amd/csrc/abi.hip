@@ -205,8 +205,10 @@ int moe_route_bwd(const void* x, const void* w_router, int dtype, int T, int d, 
   REQUIRE(gate != MOE_GATE_SOFTMAX || T == 0 || logits, "logits are required for MOE_GATE_SOFTMAX");
   const size_t need = moe::route_bwd_ws_bytes(T, d, E);
   REQUIRE(ws && ws_bytes >= need, "workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+  if ((r = check_rows16(d, "x", x)) != MOE_OK) return r;
   if ((r = check_rows16(d, "dx", dx)) != MOE_OK) return r;
   if ((r = check_rows16(d, "w_router", w_router)) != MOE_OK) return r;
+  SUPPORT(aligned16(ws), "the workspace must be 16-byte aligned");
   return hip_status(moe::launch_route_bwd(x, w_router, dtype == MOE_BF16, T, d, E, k, inv_tau, gate,
                                           topk_idx, topk_w, logits, d_topk_w, dz, dw_router,
                                           d_bias, dx, accumulate_dx, ws, stream),

@@ -281,11 +281,6 @@ constexpr int LDS_BYTES = NS * STAGE_BYTES;
 constexpr int DMA_PER_OP = OP_BYTES / 1024 / 4;  // 16-byte DMA loads per wave per operand
 constexpr int N_XCD = 8;
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
-typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8_t;
-typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
-typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
 
 __device__ const u32x4_t kZero16 = {0u, 0u, 0u, 0u};
 

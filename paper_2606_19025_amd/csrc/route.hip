@@ -241,7 +241,7 @@ struct RouteBwdArgs {
   float inv_tau;
 };
 
-constexpr int RB_CHUNK = 512;  // tokens per partial sum of dW_r
+constexpr int RB_CHUNK = 256;  // tokens per partial sum of dW_r
 
 __global__ __launch_bounds__(256) void route_dz_kernel(RouteBwdArgs a) {
   const int lane = threadIdx.x & 63;
@@ -329,10 +329,20 @@ __global__ __launch_bounds__(256) void route_dw_partial_kernel(RouteBwdArgs a) {
 }
 
 __global__ __launch_bounds__(256) void route_dw_reduce_kernel(RouteBwdArgs a) {
+  // dW_r[i] = inv_tau * (((p_0[i] + p_1[i]) + p_2[i]) + ...); the chunk
+  // loads of a thread are issued 8 at a time
   const size_t n = (size_t)a.E * a.d;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
     float s = 0.f;
-    for (int c = 0; c < a.n_chunks; ++c) s += a.part_w[(size_t)c * n + i];
+    int c = 0;
+    for (; c + 8 <= a.n_chunks; c += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = a.part_w[(size_t)(c + u) * n + i];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; c < a.n_chunks; ++c) s += a.part_w[(size_t)c * n + i];
     a.dw[i] = s * a.inv_tau;
   }
   if (a.db && blockIdx.x == 0) {
@@ -389,6 +399,204 @@ __global__ __launch_bounds__(256) void route_dx_kernel(RouteBwdArgs a) {
   }
 }
 
+// bf16 router backward on MFMA (E <= 64, d % 128 == 0): one block = 128
+// columns x RB_CHUNK tokens, in sub-chunks of 64 tokens.  Per sub-chunk the
+// block stages x[tokens, cols] and dz[tokens, 0..63] in LDS, the fp32 dz split
+// into a bf16 pair hi + lo (|dz - hi - lo| <= 2^-17 |dz|), and computes
+//   dW partial[e, c] += sum_t (hi + lo)[t, e] x[t, c]            (k = tokens)
+//   dx[t, c] (+)= inv_tau * sum_e (hi + lo)[t, e] W_r[e, c]       (k = experts)
+// with v_mfma_f32_32x32x16_bf16; wave w owns columns 32w..32w+31 of both.
+// The next sub-chunk's x and dz are loaded into registers while the current
+// one is computed.  The per-chunk dW partials (and the d_bias partials of
+// blockIdx.x == 0) are summed in a fixed order by route_dw_reduce_kernel.
+constexpr int RBM_COLS = 128;
+constexpr int RBM_SUB = 64;                   // tokens per sub-chunk
+constexpr int RBM_XS = RBM_COLS * 2 + 64;     // x row stride (bytes): the 4 rows of
+                                              // a transposed read on distinct banks
+constexpr int RBM_ZS = 64 * 2 + 16;           // dz row stride: 16 rows of a 16-byte
+                                              // read on distinct banks
+constexpr int RBM_WS = RBM_COLS * 2 + 64;     // W_r row stride
+constexpr int RBM_LDS = RBM_SUB * RBM_XS + 2 * RBM_SUB * RBM_ZS + 64 * RBM_WS;
+constexpr int RBM_XV = RBM_SUB * RBM_COLS / 8 / 256;  // 16-byte x vectors per thread
+constexpr int RBM_ZV = RBM_SUB * 64 / 8 / 256;        // 8-expert dz groups per thread
+static_assert(RBM_XV * 256 * 8 == RBM_SUB * RBM_COLS && RBM_ZV * 256 * 8 == RBM_SUB * 64,
+              "staging split");
+
+__global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[RBM_LDS];
+  char* xs = lds;
+  char* zh = xs + RBM_SUB * RBM_XS;
+  char* zl = zh + RBM_SUB * RBM_ZS;
+  char* wl = zl + RBM_SUB * RBM_ZS;
+  __shared__ float bpart[4][64];
+  const bf16_t* x = static_cast<const bf16_t*>(a.x);
+  const bf16_t* w = static_cast<const bf16_t*>(a.w);
+  bf16_t* dx = static_cast<bf16_t*>(a.dx);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int c0 = blockIdx.x * RBM_COLS;
+  const int chunk = blockIdx.y;
+  const int n_sub = min(RB_CHUNK, a.T - chunk * RB_CHUNK + RBM_SUB - 1) / RBM_SUB;
+  const bool vec_dz = (a.E & 3) == 0 && ((uintptr_t)a.dz & 15) == 0;
+  const u32x4_t zero4 = {0u, 0u, 0u, 0u};
+
+  // W_r[0..63, c0..c0+127] (rows >= E are zero)
+  for (int p = tid; p < 64 * (RBM_COLS / 8); p += 256) {
+    const int e = p / (RBM_COLS / 8), c = (p % (RBM_COLS / 8)) * 8;
+    *reinterpret_cast<u32x4_t*>(wl + e * RBM_WS + c * 2) =
+        e < a.E ? *reinterpret_cast<const u32x4_t*>(w + (size_t)e * a.d + c0 + c) : zero4;
+  }
+
+  // register staging of one sub-chunk: thread owns x vectors p = tid + 256 v
+  // (row p / 16, columns 8 (p % 16)..) and dz groups p = tid + 256 v (row p / 8,
+  // experts 8 (p % 8)..)
+  u32x4_t xr[RBM_XV];
+  float zr[RBM_ZV][8];
+  auto load_sub = [&](int t0) {
+#pragma unroll
+    for (int v = 0; v < RBM_XV; ++v) {
+      const int p = tid + 256 * v;
+      const int t = t0 + (p >> 4);
+      xr[v] = t < a.T ? *reinterpret_cast<const u32x4_t*>(x + (size_t)t * a.d + c0 + (p & 15) * 8)
+                      : zero4;
+    }
+#pragma unroll
+    for (int v = 0; v < RBM_ZV; ++v) {
+      const int p = tid + 256 * v;
+      const int t = t0 + (p >> 3), e0 = (p & 7) * 8;
+      const float* src = a.dz + (size_t)t * a.E + e0;
+      if (t < a.T && vec_dz && e0 + 8 <= a.E) {
+        const f32x4_t u0 = *reinterpret_cast<const f32x4_t*>(src);
+        const f32x4_t u1 = *reinterpret_cast<const f32x4_t*>(src + 4);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) { zr[v][u] = u0[u]; zr[v][4 + u] = u1[u]; }
+      } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) zr[v][u] = (t < a.T && e0 + u < a.E) ? src[u] : 0.f;
+      }
+    }
+  };
+  auto store_sub = [&]() {
+#pragma unroll
+    for (int v = 0; v < RBM_XV; ++v) {
+      const int p = tid + 256 * v;
+      *reinterpret_cast<u32x4_t*>(xs + (p >> 4) * RBM_XS + (p & 15) * 16) = xr[v];
+    }
+#pragma unroll
+    for (int v = 0; v < RBM_ZV; ++v) {
+      const int p = tid + 256 * v;
+      bf16x8_t hi, lo;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bf16_t h = (bf16_t)zr[v][u];
+        hi[u] = h;
+        lo[u] = (bf16_t)(zr[v][u] - (float)h);
+      }
+      *reinterpret_cast<bf16x8_t*>(zh + (p >> 3) * RBM_ZS + (p & 7) * 16) = hi;
+      *reinterpret_cast<bf16x8_t*>(zl + (p >> 3) * RBM_ZS + (p & 7) * 16) = lo;
+    }
+  };
+
+  f32x16_t accw[2] = {f32x16_t{}, f32x16_t{}};
+  float bsum = 0.f;
+  if (n_sub > 0) load_sub(chunk * RB_CHUNK);
+  for (int sc = 0; sc < n_sub; ++sc) {
+    const int t0 = chunk * RB_CHUNK + sc * RBM_SUB;
+    __syncthreads();  // previous sub-chunk's LDS reads are done
+    store_sub();
+    __syncthreads();
+    if (sc + 1 < n_sub) load_sub(t0 + RBM_SUB);
+    if (blockIdx.x == 0 && lane < a.E) {
+      // d_bias: 16 tokens per wave, fixed order, exact fp32 dz
+      for (int i = 0; i < RBM_SUB / 4; ++i) {
+        const int t = t0 + wave * (RBM_SUB / 4) + i;
+        if (t < a.T) bsum += a.dz[(size_t)t * a.E + lane];
+      }
+    }
+    // old dx of this wave's outputs (read before the MFMAs)
+    bf16x4_t old[2][4];
+    if (a.accumulate_dx) {
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        const int t = min(t0 + tb * 32 + (lane & 31), a.T - 1);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          old[tb][q] = *reinterpret_cast<const bf16x4_t*>(
+              dx + (size_t)t * a.d + c0 + wave * 32 + 8 * q + 4 * (lane >> 5));
+      }
+    }
+
+    // dW partial: k = tokens, m = experts (2 blocks), n = columns
+#pragma unroll
+    for (int ks = 0; ks < RBM_SUB / 16; ++ks) {
+      const bf16x8_t bx = frag_tr(xs, RBM_XS, ks * 16, wave * 32);
+#pragma unroll
+      for (int eb = 0; eb < 2; ++eb) {
+        const bf16x8_t ah = frag_tr(zh, RBM_ZS, ks * 16, eb * 32);
+        const bf16x8_t al = frag_tr(zl, RBM_ZS, ks * 16, eb * 32);
+        accw[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ah, accw[eb], 0, 0, 0);
+        accw[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, al, accw[eb], 0, 0, 0);
+      }
+    }
+
+    // dx: k = experts (4 k16-steps), m = tokens (2 blocks), n = columns
+    f32x16_t accx[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const bf16x8_t bw = frag_tr(wl, RBM_WS, ks * 16, wave * 32);
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        const int r = tb * 32 + (lane & 31);
+        const int e = ks * 16 + 8 * (lane >> 5);
+        const bf16x8_t ah = *reinterpret_cast<const bf16x8_t*>(zh + r * RBM_ZS + e * 2);
+        const bf16x8_t al = *reinterpret_cast<const bf16x8_t*>(zl + r * RBM_ZS + e * 2);
+        accx[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw, ah, accx[tb], 0, 0, 0);
+        accx[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw, al, accx[tb], 0, 0, 0);
+      }
+    }
+    // lane holds dx[t0 + 32 tb + lane%32][c0 + 32 wave + 8q + 4(lane/32) + 0..3]
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int t = t0 + tb * 32 + (lane & 31);
+      if (t >= a.T) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        bf16_t* p = dx + (size_t)t * a.d + c0 + wave * 32 + 8 * q + 4 * (lane >> 5);
+        bf16x4_t o;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float v = a.inv_tau * accx[tb][4 * q + u];
+          o[u] = (bf16_t)(a.accumulate_dx ? (float)old[tb][q][u] + v : v);
+        }
+        *reinterpret_cast<bf16x4_t*>(p) = o;
+      }
+    }
+  }
+
+  // lane holds partial[e = 32 eb + lane%32][c0 + 32 wave + 8q + 4(lane/32) + 0..3]
+#pragma unroll
+  for (int eb = 0; eb < 2; ++eb) {
+    const int e = eb * 32 + (lane & 31);
+    if (e >= a.E) continue;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float* p = a.part_w + ((size_t)chunk * a.E + e) * a.d + c0 + wave * 32 + 8 * q +
+                 4 * (lane >> 5);
+      const f32x4_t o = {accw[eb][4 * q], accw[eb][4 * q + 1], accw[eb][4 * q + 2],
+                         accw[eb][4 * q + 3]};
+      *reinterpret_cast<f32x4_t*>(p) = o;
+    }
+  }
+  if (blockIdx.x == 0) {
+    if (lane < 64) bpart[wave][lane] = bsum;
+    __syncthreads();
+    if (tid < a.E)
+      a.part_b[(size_t)chunk * a.E + tid] =
+          ((bpart[0][tid] + bpart[1][tid]) + bpart[2][tid]) + bpart[3][tid];
+  }
+}
+
 }  // namespace
 
 hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int bf16, int T,
@@ -425,17 +633,23 @@ hipError_t launch_route_bwd(const void* x, const void* w, int bf16, int T, int d
   RouteBwdArgs a{x, w, idx, tw, logits, dtw, dz, dw_router, d_bias, dx, part_w, part_b,
                  T, d, E, k, gate, accumulate_dx, n_chunks, inv_tau};
   if (T > 0) MOE_TIMED("route_dz", s, route_dz_kernel<<<ceil_div(T, 4), 256, 0, s>>>(a));
+  const bool mfma = bf16 && E <= 64 && d % RBM_COLS == 0;
   if (n_chunks > 0) {
-    const dim3 g(ceil_div(d, 64), ceil_div(E, 64), n_chunks);
-    if (bf16) MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<bf16_t><<<g, 256, 0, s>>>(a));
-    else MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<float><<<g, 256, 0, s>>>(a));
+    if (mfma) {
+      const dim3 g(d / RBM_COLS, n_chunks);
+      MOE_TIMED("route_bwd_mfma", s, route_bwd_mfma_kernel<<<g, 256, 0, s>>>(a));
+    } else {
+      const dim3 g(ceil_div(d, 64), ceil_div(E, 64), n_chunks);
+      if (bf16) MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<bf16_t><<<g, 256, 0, s>>>(a));
+      else MOE_TIMED("route_dw_partial", s, route_dw_partial_kernel<float><<<g, 256, 0, s>>>(a));
+    }
   }
   {
     // n_chunks == 0 (T == 0) sums nothing and writes zeros
-    const int blocks = (int)std::min<size_t>(2048, ((size_t)E * d + 255) / 256);
+    const int blocks = (int)std::min<size_t>(4096, ((size_t)E * d + 255) / 256);
     MOE_TIMED("route_dw_reduce", s, route_dw_reduce_kernel<<<blocks, 256, 0, s>>>(a));
   }
-  if (T > 0) {
+  if (T > 0 && !mfma) {
     if (bf16) MOE_TIMED("route_dx", s, route_dx_kernel<bf16_t><<<ceil_div(T, 8), 256, 0, s>>>(a));
     else MOE_TIMED("route_dx", s, route_dx_kernel<float><<<ceil_div(T, 8), 256, 0, s>>>(a));
   }
