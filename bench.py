@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--traffic-calibration", action="store_true",
+                    help="make one plain device-to-device copy of a known size before the "
+                         "steps, the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
     return ap.parse_args()
 
 
@@ -135,6 +138,15 @@ def main():
         if (i + 1) % args.round_every == 0:
             expert_delta(th0, th1, peers, delta_avg=avg)
 
+    if args.traffic_calibration:
+        from paper_2606_19025_amd.profiling import CALIBRATION_BYTES
+        src = torch.ones(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"[bench] calibration copy of {CALIBRATION_BYTES} B done")
+
     log(f"[bench] warmup {args.warmup}")
     for i in range(args.warmup):
         step(i)
@@ -190,11 +202,18 @@ def main():
                   key=lambda nm: kernels[nm]["ms_per_step"])
         kd = kernels[dom]
         kind, per_step = work[dom]
+        # HBM bytes per launch from the committed rocprofv3 counter summary of
+        # this workload, only while the kernel's source is the one measured
+        from paper_2606_19025_amd.profiling import load_traffic, source_digest
+        tr = load_traffic(os.path.join(ROOT, "profiles", f"hbm_traffic_{cfg['name']}.txt"))
+        traffic = None
+        if dom in tr and tr[dom][1] == source_digest(dom):
+            traffic = tr[dom][0]
         roofline = dict(kernel=dom, bound="mfma" if kind == "flop" else "hbm",
                         achieved=kd["achieved"], peak=kd["peak"], unit=kd["unit"],
                         frac=kd["frac"], avg_us=kd["avg_us"],
                         per_launch=per_step / max(1, kd["launches"] // args.steps),
-                        traffic=None)
+                        traffic=traffic)
 
     cpu = None
     if not args.no_cpu_baseline:

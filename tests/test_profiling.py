@@ -1,0 +1,40 @@
+"""Host-side helpers that turn rocprofv3 output into the committed summaries."""
+import csv
+
+from paper_2606_19025_amd import profiling as P
+
+
+def test_symbols_map_to_timing_names():
+    assert P.timing_name("void moe::(anonymous namespace)::gemm_bf16_kernel<5>("
+                         "moe::(anonymous namespace)::GemmArgs)") == "gemm_dwgu"
+    assert P.timing_name("_ZN3moe12_GLOBAL__N_116gemm_bf16_kernelILi2EEEvNS0_8GemmArgsE") \
+        == "gemm_dhh_bwd"
+    assert P.timing_name("_ZN3moe12_GLOBAL__N_118combine_fwd_kernelIDF16bEEvPKT_") == "combine_fwd"
+    assert P.timing_name("moe::(anonymous namespace)::route_bwd_mfma_kernel(x)") == "route_bwd_mfma"
+    assert P.timing_name("__amd_rocclr_copyBuffer") is None
+    assert P.source_digest("gemm_gu_fwd") != P.source_digest("route_fwd")
+
+
+def test_traffic_summary_is_scaled_by_the_calibration_copy(tmp_path):
+    kib = P.CALIBRATION_BYTES / 1024
+
+    def write(path, counter, copy_kib, kern_kib):
+        with open(path, "w", newline="") as f:
+            w = csv.writer(f)
+            w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+            w.writerow([1, "__amd_rocclr_copyBuffer", counter, copy_kib])
+            for i, v in enumerate(kern_kib):  # two dimensions of one dispatch are summed
+                w.writerow([2 + i, "void moe::(anonymous namespace)::gemm_bf16_kernel<0>(a)",
+                            counter, v / 2])
+                w.writerow([2 + i, "void moe::(anonymous namespace)::gemm_bf16_kernel<0>(a)",
+                            counter, v / 2])
+
+    fc, wc, out = tmp_path / "f.csv", tmp_path / "w.csv", tmp_path / "t.txt"
+    write(fc, "FETCH_SIZE", kib / 2, [100.0, 300.0])   # counter reads half of a copy's bytes
+    write(wc, "WRITE_SIZE", kib, [50.0, 50.0])
+    P.traffic(str(fc), str(wc), str(out), "rocprofv3 --pmc {COUNTER} -- prog")
+    t = P.load_traffic(str(out))
+    b, dg = t["gemm_gu_fwd"]
+    assert abs(b - (200.0 * 1024 * 2 + 50.0 * 1024)) < 1.0
+    assert dg == P.source_digest("gemm_gu_fwd")
+    assert "FETCH_SIZE" in out.read_text()
