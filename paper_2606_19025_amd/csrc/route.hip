@@ -16,7 +16,8 @@ namespace moe {
 namespace {
 
 constexpr int RT_TOK = 32;   // tokens per block
-constexpr int RT_THREADS = 256;
+constexpr int RT_WAVES = 8;
+constexpr int RT_THREADS = 64 * RT_WAVES;
 
 struct RouteFwdArgs {
   const void* x;
@@ -57,6 +58,9 @@ DEVI void build_local_map(const uint8_t* resident, int E, int* lmap) {
 }
 
 // bf16 logits of RT_TOK tokens into zl[RT_TOK][ldz] (raw dot products).
+// Wave w reduces the 64-wide slices w, w + RT_WAVES, ... of d, up to two
+// slices per round with all their loads issued before the MFMAs; the per-wave partial
+// sums are then added in wave order through LDS.
 template <int NEB>
 DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   const bf16_t* x = static_cast<const bf16_t*>(a.x);
@@ -70,16 +74,15 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
 #pragma unroll
   for (int eb = 0; eb < NEB; ++eb) acc[eb] = f32x16_t{};
   const bf16x8_t zero8 = {};
-  // wave w handles 64-wide slices w, w+4, w+8, ... of the d reduction; the
-  // lane's 32 consecutive elements of a slice feed the 4 k16 MFMA steps in
-  // the same order for the token and the expert operand
-  for (int kb = wave; kb * 64 < a.d; kb += 4) {
+  const int n_slices = (a.d + 63) / 64;
+  // the lane's 32 consecutive elements of a slice feed the 4 k16 MFMA steps
+  // in the same order for the token and the expert operand
+  auto load_slice = [&](int kb, bf16x8_t* av, bf16x8_t (*bv)[4]) {
     const int c0 = kb * 64 + half * 32;
-    bf16x8_t av[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int c = c0 + q * 8;
-      av[q] = (t < a.T && c + 8 <= a.d)
+      av[q] = (kb < n_slices && t < a.T && c + 8 <= a.d)
                   ? *reinterpret_cast<const bf16x8_t*>(x + (size_t)t * a.d + c) : zero8;
     }
 #pragma unroll
@@ -88,14 +91,27 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int c = c0 + q * 8;
-        bf16x8_t bv = (e < a.E && c + 8 <= a.d)
-                          ? *reinterpret_cast<const bf16x8_t*>(w + (size_t)e * a.d + c) : zero8;
-        acc[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[q], bv, acc[eb], 0, 0, 0);
+        bv[eb][q] = (kb < n_slices && e < a.E && c + 8 <= a.d)
+                        ? *reinterpret_cast<const bf16x8_t*>(w + (size_t)e * a.d + c) : zero8;
       }
     }
+  };
+  // UNR slices per round (fewer for wide expert sets, to stay in registers)
+  constexpr int UNR = NEB <= 2 ? 2 : 1;
+  for (int kb = wave; kb < n_slices; kb += UNR * RT_WAVES) {
+    bf16x8_t av[UNR][4], bv[UNR][NEB][4];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) load_slice(kb + u * RT_WAVES, av[u], bv[u]);  // zeros past the end
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+      for (int eb = 0; eb < NEB; ++eb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          acc[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u][q], bv[u][eb][q], acc[eb], 0, 0, 0);
   }
-  // deterministic cross-wave sum: wave 0 stores, waves 1..3 add in order
-  for (int wv = 0; wv < 4; ++wv) {
+  // deterministic cross-wave sum: wave 0 stores, waves 1.. add in order
+  for (int wv = 0; wv < RT_WAVES; ++wv) {
     if (wave == wv) {
 #pragma unroll
       for (int eb = 0; eb < NEB; ++eb) {
@@ -155,7 +171,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   }
   __syncthreads();
 
-  for (int i = wave; i < RT_TOK; i += 4) {
+  for (int i = wave; i < RT_TOK; i += RT_WAVES) {
     const int t = t0 + i;
     if (t >= a.T) break;
     float v[NQ];
