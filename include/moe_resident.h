@@ -173,6 +173,40 @@ int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const v
                         hipStream_t stream);
 
 /*
+ * Several expert sets in one call.  A set is a group of experts with one
+ * hidden size and one input buffer: the routed resident experts (xp = the
+ * dispatched rows, groups = the dispatch offsets) or the merged shared
+ * experts (Sec. 3.2: dense, always active; xp = x, offsets = {0, T}).  The
+ * sets' tiles of each GEMM share one launch, so the small routed groups and
+ * the large shared group fill the GPU together; the results are those of one
+ * moe_grouped_ffn_fwd / _bwd call per set.  Every field has the meaning and
+ * layout of the matching argument of those calls; fields a direction does
+ * not use may be NULL (forward: dyp, dgu, dxp, dw_gate_up, dw_down; backward:
+ * yp).  gu and h are written by the forward and read by the backward.
+ * n_sets is 1 or 2; all sets share dtype and d.
+ */
+typedef struct moe_ffn_set {
+  const void* xp;          /* [cap, d] */
+  const void* w_gate_up;   /* [n_groups, 2H, d] */
+  const void* w_down;      /* [n_groups, d, H] */
+  const int32_t* offsets;  /* device, [n_groups + 1] */
+  int cap, H, n_groups;
+  void* gu;                /* [cap, 2H] */
+  void* h;                 /* [cap, H] */
+  void* yp;                /* [cap, d] */
+  const void* dyp;         /* [cap, d] */
+  void* dgu;               /* [cap, 2H] */
+  void* dxp;               /* [cap, d] */
+  float* dw_gate_up;       /* [n_groups, 2H, d] fp32 */
+  float* dw_down;          /* [n_groups, d, H] fp32 */
+} moe_ffn_set;
+
+int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
+                             hipStream_t stream);
+int moe_grouped_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
+                             int accumulate_dw, hipStream_t stream);
+
+/*
  * Weighted combine (App. A: y = sum_{i in T(x)} s_i(x) E_i(x)):
  *   y[t,:] = sum_{j: inv_perm[t,j] >= 0} topk_w[t,j] * yp[inv_perm[t,j], :]
  *            (+ y_add[t,:] when y_add != NULL, e.g. the shared experts' output)

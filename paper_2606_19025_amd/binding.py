@@ -22,7 +22,8 @@ GATES = {"softmax_topk": MOE_GATE_SOFTMAX_TOPK, "softmax": MOE_GATE_SOFTMAX,
 EXPORTS = [
     "moe_last_error", "moe_abi_version", "moe_route_mask", "moe_route_bwd_workspace_size",
     "moe_route_bwd", "moe_dispatch_workspace_size", "moe_dispatch", "moe_dispatch_bwd",
-    "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_combine_fwd", "moe_combine_bwd",
+    "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_grouped_ffn_fwd_sets",
+    "moe_grouped_ffn_bwd_sets", "moe_combine_fwd", "moe_combine_bwd",
     "moe_expert_delta", "moe_timing_enable", "moe_timing_collect",
 ]
 
@@ -53,6 +54,8 @@ _SIGS = {
     "moe_grouped_ffn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_grouped_ffn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P,
                                  _I, _P]),
+    "moe_grouped_ffn_fwd_sets": (_I, [_P, _I, _I, _I, _P]),
+    "moe_grouped_ffn_bwd_sets": (_I, [_P, _I, _I, _I, _I, _P]),
     "moe_combine_fwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_combine_bwd": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_expert_delta": (_I, [_P, _P, C.POINTER(C.c_void_p), _I, _Z, _P, _P, _P]),
@@ -64,6 +67,22 @@ _SIGS = {
 class moe_kernel_time(C.Structure):
     _fields_ = [("name", C.c_char_p), ("launches", C.c_int), ("total_ms", C.c_float),
                 ("min_ms", C.c_float), ("max_ms", C.c_float)]
+
+
+class moe_ffn_set(C.Structure):
+    """One expert set (struct moe_ffn_set of include/moe_resident.h)."""
+    _fields_ = [("xp", _P), ("w_gate_up", _P), ("w_down", _P), ("offsets", _P),
+                ("cap", _I), ("H", _I), ("n_groups", _I),
+                ("gu", _P), ("h", _P), ("yp", _P), ("dyp", _P), ("dgu", _P), ("dxp", _P),
+                ("dw_gate_up", _P), ("dw_down", _P)]
+
+
+def ffn_set(xp, w_gate_up, w_down, offsets, cap, H, n_groups, gu, h, yp=None, dyp=None,
+            dgu=None, dxp=None, dw_gate_up=None, dw_down=None):
+    """A moe_ffn_set from tensors (or raw addresses / None)."""
+    return moe_ffn_set(_ptr(xp), _ptr(w_gate_up), _ptr(w_down), _ptr(offsets), cap, H, n_groups,
+                       _ptr(gu), _ptr(h), _ptr(yp), _ptr(dyp), _ptr(dgu), _ptr(dxp),
+                       _ptr(dw_gate_up), _ptr(dw_down))
 
 
 def lib(path: str | None = None):
@@ -175,6 +194,18 @@ def moe_grouped_ffn_bwd(dyp, xp, gu, h, w_gate_up, w_down, dtype, cap, d, H, n_g
         _ptr(dyp), _ptr(xp), _ptr(gu), _ptr(h), _ptr(w_gate_up), _ptr(w_down), dtype, cap, d, H,
         n_groups, _ptr(offsets), _ptr(dgu), _ptr(dxp), _ptr(dw_gate_up), _ptr(dw_down),
         accumulate_dw, _stream(stream)))
+
+
+def moe_grouped_ffn_fwd_sets(sets, dtype, d, stream=None):
+    arr = (moe_ffn_set * len(sets))(*sets)
+    return _check("moe_grouped_ffn_fwd_sets", lib().moe_grouped_ffn_fwd_sets(
+        C.cast(arr, C.c_void_p), len(sets), dtype, d, _stream(stream)))
+
+
+def moe_grouped_ffn_bwd_sets(sets, dtype, d, accumulate_dw, stream=None):
+    arr = (moe_ffn_set * len(sets))(*sets)
+    return _check("moe_grouped_ffn_bwd_sets", lib().moe_grouped_ffn_bwd_sets(
+        C.cast(arr, C.c_void_p), len(sets), dtype, d, accumulate_dw, _stream(stream)))
 
 
 def moe_combine_fwd(yp, dtype, T, d, k, cap, topk_w, inv_perm, y_add, y, stream=None):

@@ -265,18 +265,63 @@ static int check_ffn(int dtype, int cap, int d, int H, int n_groups, const int32
   return MOE_OK;
 }
 
+namespace {
+
+int check_set(const moe_ffn_set& f, int dtype, int d, bool fwd) {
+  int r;
+  if ((r = check_ffn(dtype, f.cap, d, f.H, f.n_groups, f.offsets)) != MOE_OK) return r;
+  REQUIRE(f.n_groups == 0 || (f.w_gate_up && f.w_down), "expert weights must not be NULL");
+  if (fwd) {
+    REQUIRE(f.cap == 0 || (f.xp && f.gu && f.h && f.yp), "xp, gu, h and yp must not be NULL");
+  } else {
+    REQUIRE(f.n_groups == 0 || (f.dw_gate_up && f.dw_down),
+            "the expert weight gradients must not be NULL");
+    REQUIRE(f.cap == 0 || (f.dyp && f.xp && f.gu && f.h && f.dgu && f.dxp),
+            "dyp, xp, gu, h, dgu and dxp must not be NULL");
+  }
+  for (const void* p : {f.xp, f.w_gate_up, f.w_down, (const void*)f.gu, (const void*)f.h,
+                        (const void*)f.yp, f.dyp, (const void*)f.dgu, (const void*)f.dxp,
+                        (const void*)f.dw_gate_up, (const void*)f.dw_down})
+    SUPPORT(p == nullptr || aligned16(p), "operands must be 16-byte aligned");
+  return MOE_OK;
+}
+
+int check_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d, bool fwd) {
+  REQUIRE(sets != nullptr && n_sets >= 1 && n_sets <= 2, "n_sets = %d must be 1 or 2", n_sets);
+  for (int i = 0; i < n_sets; ++i) {
+    const int r = check_set(sets[i], dtype, d, fwd);
+    if (r != MOE_OK) return r;
+  }
+  return MOE_OK;
+}
+
+}  // namespace
+
+int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
+                             hipStream_t stream) {
+  int r;
+  if ((r = check_sets(sets, n_sets, dtype, d, true)) != MOE_OK) return r;
+  return hip_status(moe::launch_ffn_fwd_sets(sets, n_sets, dtype == MOE_BF16, d, stream),
+                    "moe_grouped_ffn_fwd_sets");
+}
+
+int moe_grouped_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
+                             int accumulate_dw, hipStream_t stream) {
+  int r;
+  if ((r = check_sets(sets, n_sets, dtype, d, false)) != MOE_OK) return r;
+  return hip_status(
+      moe::launch_ffn_bwd_sets(sets, n_sets, dtype == MOE_BF16, d, accumulate_dw, stream),
+      "moe_grouped_ffn_bwd_sets");
+}
+
 int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_down, int dtype,
                         int cap, int d, int H, int n_groups, const int32_t* offsets, void* gu,
                         void* h, void* yp, hipStream_t stream) {
-  int r;
-  if ((r = check_ffn(dtype, cap, d, H, n_groups, offsets)) != MOE_OK) return r;
-  REQUIRE(n_groups == 0 || (w_gate_up && w_down), "expert weights must not be NULL");
-  REQUIRE(cap == 0 || (xp && gu && h && yp), "xp, gu, h and yp must not be NULL");
-  for (const void* p : {xp, w_gate_up, w_down, (const void*)gu, (const void*)h, (const void*)yp})
-    SUPPORT(p == nullptr || aligned16(p), "operands must be 16-byte aligned");
-  return hip_status(moe::launch_ffn_fwd(xp, w_gate_up, w_down, dtype == MOE_BF16, cap, d, H,
-                                        n_groups, offsets, gu, h, yp, stream),
-                    "moe_grouped_ffn_fwd");
+  moe_ffn_set f{};
+  f.xp = xp; f.w_gate_up = w_gate_up; f.w_down = w_down; f.offsets = offsets;
+  f.cap = cap; f.H = H; f.n_groups = n_groups;
+  f.gu = gu; f.h = h; f.yp = yp;
+  return moe_grouped_ffn_fwd_sets(&f, 1, dtype, d, stream);
 }
 
 int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
@@ -284,18 +329,12 @@ int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const v
                         int H, int n_groups, const int32_t* offsets, void* dgu, void* dxp,
                         float* dw_gate_up, float* dw_down, int accumulate_dw,
                         hipStream_t stream) {
-  int r;
-  if ((r = check_ffn(dtype, cap, d, H, n_groups, offsets)) != MOE_OK) return r;
-  REQUIRE(n_groups == 0 || (w_gate_up && w_down && dw_gate_up && dw_down),
-          "expert weights and their gradients must not be NULL");
-  REQUIRE(cap == 0 || (dyp && xp && gu && h && dgu && dxp),
-          "dyp, xp, gu, h, dgu and dxp must not be NULL");
-  for (const void* p : {dyp, xp, gu, h, w_gate_up, w_down, (const void*)dgu, (const void*)dxp})
-    SUPPORT(p == nullptr || aligned16(p), "operands must be 16-byte aligned");
-  return hip_status(moe::launch_ffn_bwd(dyp, xp, gu, h, w_gate_up, w_down, dtype == MOE_BF16, cap,
-                                        d, H, n_groups, offsets, dgu, dxp, dw_gate_up, dw_down,
-                                        accumulate_dw, stream),
-                    "moe_grouped_ffn_bwd");
+  moe_ffn_set f{};
+  f.xp = xp; f.w_gate_up = w_gate_up; f.w_down = w_down; f.offsets = offsets;
+  f.cap = cap; f.H = H; f.n_groups = n_groups;
+  f.gu = const_cast<void*>(gu); f.h = const_cast<void*>(h);
+  f.dyp = dyp; f.dgu = dgu; f.dxp = dxp; f.dw_gate_up = dw_gate_up; f.dw_down = dw_down;
+  return moe_grouped_ffn_bwd_sets(&f, 1, dtype, d, accumulate_dw, stream);
 }
 
 int moe_combine_fwd(const void* yp, int dtype, int T, int d, int k, int cap, const float* topk_w,

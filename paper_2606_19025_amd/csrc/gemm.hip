@@ -471,23 +471,49 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
 }
 
 template <int KIND>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
+DEVI int col_tiles(const GemmArgs& a) {
+  return ((KIND == GU_FWD ? 2 * a.H : a.N) + GT - 1) / GT;
+}
+
+// Kernel argument of the bf16 kernel: one or two sets of groups of the same
+// GEMM kind (the routed experts and the merged shared experts) in one launch,
+// so that the tiles of both fill the CUs together.
+struct GemmLaunch {
+  GemmArgs s0, s1;
+  int n_sets;
+};
+
+template <int KIND>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
   using K_ = Kind<KIND>;
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const bf16_t* zero16 = reinterpret_cast<const bf16_t*>(&kZero16);
-  const int n_tiles = ((KIND == GU_FWD ? 2 * a.H : a.N) + GT - 1) / GT;
-  const int m_tiles = m_tile_count<KIND>(a);
-  const int total = m_tiles * n_tiles;
-  // XCD-aware assignment (the grid is a multiple of N_XCD blocks)
+  // XCD-aware assignment (the grid is a multiple of N_XCD blocks): XCD x takes
+  // the x-th eighth of every set's tile range (so each XCD gets an equal share
+  // of each set's work), set 0 first; its blocks deal these tiles round-robin.
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
-  const int t_lo = (int)((long)total * xcd / N_XCD);
-  const int t_hi = (int)((long)total * (xcd + 1) / N_XCD);
+  const int nt0 = col_tiles<KIND>(L.s0);
+  const int mt0 = m_tile_count<KIND>(L.s0);
+  const int tot0 = mt0 * nt0;
+  const int nt1 = L.n_sets > 1 ? col_tiles<KIND>(L.s1) : 0;
+  const int mt1 = L.n_sets > 1 ? m_tile_count<KIND>(L.s1) : 0;
+  const int tot1 = mt1 * nt1;
+  const int lo0 = (int)((long)tot0 * xcd / N_XCD);
+  const int cnt0 = (int)((long)tot0 * (xcd + 1) / N_XCD) - lo0;
+  const int lo1 = (int)((long)tot1 * xcd / N_XCD);
+  const int cnt1 = (int)((long)tot1 * (xcd + 1) / N_XCD) - lo1;
 
-  for (int t = t_lo + (int)(blockIdx.x / N_XCD); t < t_hi; t += per_xcd) {
+  for (int i = (int)(blockIdx.x / N_XCD); i < cnt0 + cnt1; i += per_xcd) {
+    const bool second = i >= cnt0;
+    GemmArgs a;
+    if (second) a = L.s1; else a = L.s0;
+    const int t = second ? lo1 + (i - cnt0) : lo0 + i;
+    const int m_tiles = second ? mt1 : mt0;
+    const int n_tiles = second ? nt1 : nt0;
     Tile tl;
     int tile_n;
     tile_decode<KIND>(a, t, m_tiles, n_tiles, tl, tile_n);
@@ -754,95 +780,119 @@ int num_cus() {
 }
 
 template <int KIND>
-hipError_t run_gemm(const GemmArgs& a, int bf16, hipStream_t s) {
-  static constexpr const char* names[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
-                                          "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
-  const int ncols = (KIND == GU_FWD) ? 2 * a.H : a.N;
+long max_tiles(const GemmArgs& a) {
+  const long n_tiles = ceil_div((KIND == GU_FWD) ? 2 * a.H : a.N, GT);
+  return Kind<KIND>::MRAG ? (ceil_div(a.cap, GT) + (long)a.n_groups) * n_tiles
+                          : (long)a.n_groups * ceil_div(a.M, GT) * n_tiles;
+}
+
+constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
+                                      "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
+
+// One launch over the sets sets[0..n_sets) (at most 2) of one GEMM kind.
+template <int KIND>
+hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s) {
   if (bf16) {
     // persistent: at most one block per CU, a multiple of N_XCD blocks
-    const long n_tiles = ceil_div(ncols, GT);
-    const long max_tiles = Kind<KIND>::MRAG ? (ceil_div(a.cap, GT) + (long)a.n_groups) * n_tiles
-                                            : (long)a.n_groups * ceil_div(a.M, GT) * n_tiles;
-    if (max_tiles == 0) return hipSuccess;
-    long blocks = std::min<long>(num_cus(), max_tiles);
+    GemmLaunch L{};
+    L.s0 = sets[0];
+    L.n_sets = n_sets;
+    long tiles = max_tiles<KIND>(sets[0]);
+    if (n_sets > 1) {
+      L.s1 = sets[1];
+      tiles += max_tiles<KIND>(sets[1]);
+    }
+    if (tiles == 0) return hipSuccess;
+    long blocks = std::min<long>(num_cus(), tiles);
     blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
-    MOE_TIMED(names[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(a));
+    MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(L));
     return hipGetLastError();
   }
-  dim3 grid;
-  grid.x = ceil_div(ncols, 64);
-  if (Kind<KIND>::MRAG) {
-    grid.y = ceil_div(a.cap, 64) + a.n_groups;
-    grid.z = 1;
-  } else {
-    grid.y = ceil_div(a.M, 64);
-    grid.z = a.n_groups;
+  for (int i = 0; i < n_sets; ++i) {
+    const GemmArgs& a = sets[i];
+    dim3 grid;
+    grid.x = ceil_div((KIND == GU_FWD) ? 2 * a.H : a.N, 64);
+    if (Kind<KIND>::MRAG) {
+      grid.y = ceil_div(a.cap, 64) + a.n_groups;
+      grid.z = 1;
+    } else {
+      grid.y = ceil_div(a.M, 64);
+      grid.z = a.n_groups;
+    }
+    if (grid.x == 0 || grid.y == 0 || grid.z == 0) continue;
+    MOE_TIMED(kGemmNames[KIND], s, gemm_f32_kernel<KIND><<<grid, 256, 0, s>>>(a));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
-  MOE_TIMED(names[KIND], s, gemm_f32_kernel<KIND><<<grid, 256, 0, s>>>(a));
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace
 
-hipError_t launch_ffn_fwd(const void* xp, const void* wgu, const void* wd, int bf16, int cap,
-                          int d, int H, int n_groups, const int32_t* offsets, void* gu, void* h,
-                          void* yp, hipStream_t s) {
-  GemmArgs g{};
-  g.offsets = offsets;
-  g.n_groups = n_groups;
-  g.cap = cap;
-  g.H = H;
-  // [G|U] = X [Wg;Wu]^T with the SwiGLU epilogue
-  g.A = xp; g.lda = d;
-  g.B = wgu; g.ldb = d; g.b_gs = 2L * H * d;
-  g.C = gu; g.ldc = 2L * H; g.out2 = h;
-  g.N = 2 * H; g.K = d;
-  hipError_t e = run_gemm<GU_FWD>(g, bf16, s);
+hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+                               hipStream_t s) {
+  GemmArgs g[2]{}, o[2]{};
+  for (int i = 0; i < n_sets; ++i) {
+    const moe_ffn_set& f = sets[i];
+    // [G|U] = X [Wg;Wu]^T with the SwiGLU epilogue
+    GemmArgs& a = g[i];
+    a.offsets = f.offsets; a.n_groups = f.n_groups; a.cap = f.cap; a.H = f.H;
+    a.A = f.xp; a.lda = d;
+    a.B = f.w_gate_up; a.ldb = d; a.b_gs = 2L * f.H * d;
+    a.C = f.gu; a.ldc = 2L * f.H; a.out2 = f.h;
+    a.N = 2 * f.H; a.K = d;
+    // Y = Hh Wd^T
+    GemmArgs& b = o[i];
+    b.offsets = f.offsets; b.n_groups = f.n_groups; b.cap = f.cap; b.H = f.H;
+    b.A = f.h; b.lda = f.H;
+    b.B = f.w_down; b.ldb = f.H; b.b_gs = (long)d * f.H;
+    b.C = f.yp; b.ldc = d;
+    b.N = d; b.K = f.H;
+  }
+  hipError_t e = run_gemm<GU_FWD>(g, n_sets, bf16, s);
   if (e != hipSuccess) return e;
-  // Y = Hh Wd^T
-  g.A = h; g.lda = H;
-  g.B = wd; g.ldb = H; g.b_gs = (long)d * H;
-  g.C = yp; g.ldc = d; g.out2 = nullptr;
-  g.N = d; g.K = H;
-  return run_gemm<DOWN_FWD>(g, bf16, s);
+  return run_gemm<DOWN_FWD>(o, n_sets, bf16, s);
 }
 
-hipError_t launch_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
-                          const void* wgu, const void* wd, int bf16, int cap, int d, int H,
-                          int n_groups, const int32_t* offsets, void* dgu, void* dxp,
-                          float* dwgu, float* dwd, int accumulate_dw, hipStream_t s) {
-  GemmArgs g{};
-  g.offsets = offsets;
-  g.n_groups = n_groups;
-  g.cap = cap;
-  g.H = H;
-  g.accumulate = accumulate_dw;
-  // dHh = dY Wd, epilogue -> [dG | dU]
-  g.A = dyp; g.lda = d;
-  g.B = wd; g.ldb = H; g.b_gs = (long)d * H;
-  g.C = dgu; g.ldc = 2L * H; g.aux = gu;
-  g.N = H; g.K = d;
-  hipError_t e = run_gemm<DHH_BWD>(g, bf16, s);
-  if (e != hipSuccess) return e;
-  // dX = [dG|dU] [Wg;Wu]
-  g.A = dgu; g.lda = 2L * H;
-  g.B = wgu; g.ldb = d; g.b_gs = 2L * H * d;
-  g.C = dxp; g.ldc = d; g.aux = nullptr;
-  g.N = d; g.K = 2 * H;
-  if ((e = run_gemm<DX_BWD>(g, bf16, s)) != hipSuccess) return e;
-  // dWd[g] = dY^T Hh
-  g.A = dyp; g.lda = d;
-  g.B = h; g.ldb = H; g.b_gs = 0;
-  g.C = dwd; g.ldc = H; g.c_gs = (long)d * H;
-  g.M = d; g.N = H; g.K = 0;
-  if ((e = run_gemm<DWD>(g, bf16, s)) != hipSuccess) return e;
-  // dWgu[g] = [dG|dU]^T X
-  g.A = dgu; g.lda = 2L * H;
-  g.B = xp; g.ldb = d;
-  g.C = dwgu; g.ldc = d; g.c_gs = 2L * H * d;
-  g.M = 2 * H; g.N = d;
-  return run_gemm<DWGU>(g, bf16, s);
+hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+                               int accumulate_dw, hipStream_t s) {
+  GemmArgs hh[2]{}, dx[2]{}, wd[2]{}, wgu[2]{};
+  for (int i = 0; i < n_sets; ++i) {
+    const moe_ffn_set& f = sets[i];
+    const long H = f.H;
+    GemmArgs base{};
+    base.offsets = f.offsets; base.n_groups = f.n_groups; base.cap = f.cap; base.H = f.H;
+    base.accumulate = accumulate_dw;
+    // dHh = dY Wd, epilogue -> [dG | dU]
+    GemmArgs& a = hh[i] = base;
+    a.A = f.dyp; a.lda = d;
+    a.B = f.w_down; a.ldb = H; a.b_gs = (long)d * H;
+    a.C = f.dgu; a.ldc = 2 * H; a.aux = f.gu;
+    a.N = f.H; a.K = d;
+    // dX = [dG|dU] [Wg;Wu]
+    GemmArgs& b = dx[i] = base;
+    b.A = f.dgu; b.lda = 2 * H;
+    b.B = f.w_gate_up; b.ldb = d; b.b_gs = 2 * H * d;
+    b.C = f.dxp; b.ldc = d;
+    b.N = d; b.K = 2 * f.H;
+    // dWd[g] = dY^T Hh
+    GemmArgs& c = wd[i] = base;
+    c.A = f.dyp; c.lda = d;
+    c.B = f.h; c.ldb = H;
+    c.C = f.dw_down; c.ldc = H; c.c_gs = (long)d * H;
+    c.M = d; c.N = f.H;
+    // dWgu[g] = [dG|dU]^T X
+    GemmArgs& w = wgu[i] = base;
+    w.A = f.dgu; w.lda = 2 * H;
+    w.B = f.xp; w.ldb = d;
+    w.C = f.dw_gate_up; w.ldc = d; w.c_gs = 2 * H * d;
+    w.M = 2 * f.H; w.N = d;
+  }
+  hipError_t e;
+  if ((e = run_gemm<DHH_BWD>(hh, n_sets, bf16, s)) != hipSuccess) return e;
+  if ((e = run_gemm<DX_BWD>(dx, n_sets, bf16, s)) != hipSuccess) return e;
+  if ((e = run_gemm<DWD>(wd, n_sets, bf16, s)) != hipSuccess) return e;
+  return run_gemm<DWGU>(wgu, n_sets, bf16, s);
 }
 
 }  // namespace moe

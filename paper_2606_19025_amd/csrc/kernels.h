@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "moe_resident.h"
+
 namespace moe {
 
 hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int bf16, int T,
@@ -34,13 +36,12 @@ hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, i
                               int cap, const float* tw, const int32_t* inv_perm, void* dyp,
                               float* dtw, hipStream_t s);
 
-hipError_t launch_ffn_fwd(const void* xp, const void* wgu, const void* wd, int bf16, int cap,
-                          int d, int H, int n_groups, const int32_t* offsets, void* gu, void* h,
-                          void* yp, hipStream_t s);
-hipError_t launch_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
-                          const void* wgu, const void* wd, int bf16, int cap, int d, int H,
-                          int n_groups, const int32_t* offsets, void* dgu, void* dxp,
-                          float* dwgu, float* dwd, int accumulate_dw, hipStream_t s);
+// Grouped SwiGLU FFN over 1 or 2 expert sets (moe_ffn_set of the public
+// header), one launch per GEMM kind.
+hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+                               hipStream_t s);
+hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+                               int accumulate_dw, hipStream_t s);
 
 constexpr int kMaxPeers = 16;
 hipError_t launch_expert_delta(const float* start, const float* now, const float* const* peers,

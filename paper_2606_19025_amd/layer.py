@@ -3,12 +3,10 @@
 ``ResidentMoELayer`` owns the device buffers of one layer shape and issues the
 C entry points in order; it computes nothing itself.
 
-Forward:  moe_route_mask -> moe_dispatch -> moe_grouped_ffn_fwd (resident
-          experts) [-> moe_grouped_ffn_fwd (shared experts, identity dispatch)]
-          -> moe_combine_fwd
-Backward: moe_combine_bwd -> moe_grouped_ffn_bwd (resident)
-          [-> moe_grouped_ffn_bwd (shared), writing dx] -> moe_dispatch_bwd
-          -> moe_route_bwd (adds the router's dx)
+Forward:  moe_route_mask -> moe_dispatch -> moe_grouped_ffn_fwd_sets (resident
+          experts [+ shared experts on x, identity dispatch]) -> moe_combine_fwd
+Backward: moe_combine_bwd -> moe_grouped_ffn_bwd_sets (resident [+ shared,
+          writing dx]) -> moe_dispatch_bwd -> moe_route_bwd (adds the router's dx)
 Round boundary: moe_expert_delta over the fp32 master copies.
 """
 from __future__ import annotations
@@ -89,13 +87,15 @@ class ResidentMoELayer:
         B.moe_dispatch(x, dt, T, d, k, self.E_r, self.topk_local, self.counts, self.offsets,
                        self.perm, self.inv_perm, self.xp, self.ws_dispatch, self.ws_dispatch_bytes,
                        stream)
-        B.moe_grouped_ffn_fwd(self.xp, w_gate_up, w_down, dt, cap, d, H, self.E_r, self.offsets,
-                              self.gu, self.h, self.yp, stream)
+        sets = [B.ffn_set(self.xp, w_gate_up, w_down, self.offsets, cap, H, self.E_r, self.gu,
+                          self.h, yp=self.yp)]
         y_add = None
         if self.Hs:
-            B.moe_grouped_ffn_fwd(x, shared_gate_up, shared_down, dt, T, d, self.Hs, 1,
-                                  self.s_offsets, self.s_gu, self.s_h, self.s_y, stream)
+            # the shared experts see every token: their "dispatched rows" are x
+            sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
+                                  self.s_gu, self.s_h, yp=self.s_y))
             y_add = self.s_y
+        B.moe_grouped_ffn_fwd_sets(sets, dt, d, stream)
         B.moe_combine_fwd(self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, y_add, self.y,
                           stream)
         return self.y
@@ -106,14 +106,15 @@ class ResidentMoELayer:
         T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
         B.moe_combine_bwd(dy, self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, self.dyp,
                           self.dtopk_w, stream)
-        B.moe_grouped_ffn_bwd(self.dyp, self.xp, self.gu, self.h, w_gate_up, w_down, dt, cap, d, H,
-                              self.E_r, self.offsets, self.dgu, self.dxp, self.dw_gate_up,
-                              self.dw_down, accumulate_dw, stream)
+        sets = [B.ffn_set(self.xp, w_gate_up, w_down, self.offsets, cap, H, self.E_r, self.gu,
+                          self.h, dyp=self.dyp, dgu=self.dgu, dxp=self.dxp,
+                          dw_gate_up=self.dw_gate_up, dw_down=self.dw_down)]
         if self.Hs:
             # the shared experts see every token with weight 1: their dxp is dx
-            B.moe_grouped_ffn_bwd(dy, x, self.s_gu, self.s_h, shared_gate_up, shared_down, dt, T,
-                                  d, self.Hs, 1, self.s_offsets, self.s_dgu, self.dx,
-                                  self.s_dw_gate_up, self.s_dw_down, accumulate_dw, stream)
+            sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
+                                  self.s_gu, self.s_h, dyp=dy, dgu=self.s_dgu, dxp=self.dx,
+                                  dw_gate_up=self.s_dw_gate_up, dw_down=self.s_dw_down))
+        B.moe_grouped_ffn_bwd_sets(sets, dt, d, accumulate_dw, stream)
         B.moe_dispatch_bwd(self.dxp, dt, T, d, k, cap, self.inv_perm, self.dx, 1 if self.Hs else 0,
                            stream)
         B.moe_route_bwd(x, w_router, dt, T, d, E, k, self.inv_tau, self.gate, self.topk_idx,

@@ -117,3 +117,21 @@ def test_expert_delta_rejects_too_many_peers(lib):
     assert call_status(lib.moe_expert_delta, p, p, arr, 17, 1024, None, p) == ERR_ARG
     arr2 = (C.c_void_p * 1)(p + 4)
     assert call_status(lib.moe_expert_delta, p, p, arr2, 1, 1024, None, p) == ERR_UNSUPPORTED
+
+
+def test_ffn_sets_reject_bad_arguments(lib):
+    p = 256
+    ok = B.ffn_set(p, p, p, p, 64, 128, 2, p, p, yp=p)
+    assert B.lib().moe_grouped_ffn_fwd_sets(None, 1, B.MOE_BF16, 128, None) == ERR_ARG
+    arr = (B.moe_ffn_set * 3)(ok, ok, ok)
+    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 3, B.MOE_BF16, 128, None) \
+        == ERR_ARG
+    bad_h = B.ffn_set(p, p, p, p, 64, 100, 2, p, p, yp=p)
+    arr = (B.moe_ffn_set * 2)(ok, bad_h)
+    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 2, B.MOE_BF16, 128, None) \
+        == ERR_UNSUPPORTED
+    no_grad = B.ffn_set(p, p, p, p, 64, 128, 2, p, p, dyp=p, dgu=p, dxp=p)  # dW pointers NULL
+    arr = (B.moe_ffn_set * 1)(no_grad)
+    assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 128, 0,
+                                            None) == ERR_ARG
+    assert "gradients" in B.moe_last_error()
