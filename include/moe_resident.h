@@ -203,8 +203,19 @@ typedef struct moe_ffn_set {
 
 int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
                              hipStream_t stream);
+/*
+ * ws: device workspace of at least moe_grouped_ffn_bwd_workspace_size(sets,
+ * n_sets, dtype, d) bytes, 256-byte aligned, or NULL with ws_bytes = 0.  Its
+ * contents on entry are ignored.  With a workspace the weight-gradient GEMMs
+ * hand out tiles dynamically (per-XCD counters) and a set with one large
+ * group (the shared experts) may have its rows split into parts whose fp32
+ * partial gradients are summed in a fixed order afterwards; the size depends
+ * on the sets and on the device's compute-unit count.  Results are
+ * run-to-run identical either way.
+ */
+size_t moe_grouped_ffn_bwd_workspace_size(const moe_ffn_set* sets, int n_sets, int dtype, int d);
 int moe_grouped_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
-                             int accumulate_dw, hipStream_t stream);
+                             int accumulate_dw, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Weighted combine (App. A: y = sum_{i in T(x)} s_i(x) E_i(x)):

@@ -305,12 +305,22 @@ int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int
                     "moe_grouped_ffn_fwd_sets");
 }
 
+size_t moe_grouped_ffn_bwd_workspace_size(const moe_ffn_set* sets, int n_sets, int dtype, int d) {
+  if (!sets || n_sets < 1 || n_sets > 2 || d < 1) return 0;
+  return moe::ffn_bwd_ws_bytes(sets, n_sets, dtype == MOE_BF16, d);
+}
+
 int moe_grouped_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
-                             int accumulate_dw, hipStream_t stream) {
+                             int accumulate_dw, void* ws, size_t ws_bytes, hipStream_t stream) {
   int r;
   if ((r = check_sets(sets, n_sets, dtype, d, false)) != MOE_OK) return r;
+  if (ws) {
+    const size_t need = moe::ffn_bwd_ws_bytes(sets, n_sets, dtype == MOE_BF16, d);
+    REQUIRE(ws_bytes >= need, "workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+    SUPPORT((reinterpret_cast<uintptr_t>(ws) & 255u) == 0, "the workspace must be 256-byte aligned");
+  }
   return hip_status(
-      moe::launch_ffn_bwd_sets(sets, n_sets, dtype == MOE_BF16, d, accumulate_dw, stream),
+      moe::launch_ffn_bwd_sets(sets, n_sets, dtype == MOE_BF16, d, accumulate_dw, ws, stream),
       "moe_grouped_ffn_bwd_sets");
 }
 
@@ -334,7 +344,7 @@ int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const v
   f.cap = cap; f.H = H; f.n_groups = n_groups;
   f.gu = const_cast<void*>(gu); f.h = const_cast<void*>(h);
   f.dyp = dyp; f.dgu = dgu; f.dxp = dxp; f.dw_gate_up = dw_gate_up; f.dw_down = dw_down;
-  return moe_grouped_ffn_bwd_sets(&f, 1, dtype, d, accumulate_dw, stream);
+  return moe_grouped_ffn_bwd_sets(&f, 1, dtype, d, accumulate_dw, nullptr, 0, stream);
 }
 
 int moe_combine_fwd(const void* yp, int dtype, int T, int d, int k, int cap, const float* topk_w,

@@ -53,11 +53,13 @@ struct GemmArgs {
   const int32_t* offsets;
   long lda, ldb, ldc;
   long b_gs, c_gs;  // per-group strides (elements) of B and C
+  long c_split;     // K-ragged kinds: stride between the split-K partial outputs
   int n_groups, cap, M, N, K, H, accumulate;
+  int ksplit;       // K-ragged kinds: each group's rows split in ksplit parts (0 = 1)
 };
 
 struct Tile {
-  int g, row0, rows, m0, n0;
+  int g, row0, rows, m0, n0, split;
 };
 
 DEVI int clamp_row(int v, int cap) { return v < 0 ? 0 : (v > cap ? cap : v); }
@@ -80,6 +82,7 @@ DEVI bool decode_tile(const GemmArgs& a, Tile& t) {
         t.row0 = b + mt * BM;
         t.rows = min(BM, e - t.row0);
         t.m0 = 0;
+        t.split = 0;
         return true;
       }
       mt -= tiles;
@@ -88,6 +91,7 @@ DEVI bool decode_tile(const GemmArgs& a, Tile& t) {
     return false;
   } else {
     t.g = blockIdx.z;
+    t.split = 0;
     t.m0 = blockIdx.y * BM;
     const int b = clamp_row(a.offsets[t.g], a.cap);
     const int e = clamp_row(a.offsets[t.g + 1], a.cap);
@@ -427,7 +431,7 @@ DEVI int m_tile_count(const GemmArgs& a) {
     }
     return tiles;
   } else {
-    return a.n_groups * ((a.M + GT - 1) / GT);
+    return a.n_groups * max(1, a.ksplit) * ((a.M + GT - 1) / GT);
   }
 }
 
@@ -453,20 +457,28 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
         tl.row0 = b + mt * GT;
         tl.rows = min(GT, e - tl.row0);
         tl.m0 = 0;
+        tl.split = 0;
         return;
       }
       mt -= tiles;
       b = e;
     }
-    tl.g = 0; tl.row0 = 0; tl.rows = 0; tl.m0 = 0;  // not reached for t < count
+    tl.g = 0; tl.row0 = 0; tl.rows = 0; tl.m0 = 0; tl.split = 0;  // not reached for t < count
   } else {
+    // (group, split part, m-tile); part p of a group of rows [b, e) is
+    // [b + len p / S, b + len (p + 1) / S)
+    const int S = max(1, a.ksplit);
     const int mt_per_g = (a.M + GT - 1) / GT;
-    tl.g = q / mt_per_g;
+    const int gs = q / mt_per_g;
+    tl.g = gs / S;
+    tl.split = gs % S;
     tl.m0 = (q % mt_per_g) * GT;
     const int b = clamp_row(a.offsets[tl.g], a.cap);
-    const int e = clamp_row(a.offsets[tl.g + 1], a.cap);
-    tl.row0 = b;
-    tl.rows = e > b ? e - b : 0;
+    int e = clamp_row(a.offsets[tl.g + 1], a.cap);
+    if (e < b) e = b;
+    const long len = e - b;
+    tl.row0 = b + (int)(len * tl.split / S);
+    tl.rows = b + (int)(len * (tl.split + 1) / S) - tl.row0;
   }
 }
 
@@ -481,6 +493,9 @@ DEVI int col_tiles(const GemmArgs& a) {
 struct GemmLaunch {
   GemmArgs s0, s1;
   int n_sets;
+  int* counters;  // non-null: per-XCD tile counters (zero at launch) for dynamic dealing
+  int* zero;      // block 0 zeroes zero[0..n_zero) (the next launches' counters)
+  int n_zero;
 };
 
 template <int KIND>
@@ -493,9 +508,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
   const bf16_t* zero16 = reinterpret_cast<const bf16_t*>(&kZero16);
   // XCD-aware assignment (the grid is a multiple of N_XCD blocks): XCD x takes
   // the x-th eighth of every set's tile range (so each XCD gets an equal share
-  // of each set's work), set 0 first; its blocks deal these tiles round-robin.
+  // of each set's work), set 0 first.  Its blocks deal these tiles
+  // round-robin, or - with counters - each block takes the XCD's next tile
+  // when it finishes one (tiles of unequal K then balance across blocks).
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
+  if (L.zero && blockIdx.x == 0 && threadIdx.x < L.n_zero) L.zero[threadIdx.x] = 0;
   const int nt0 = col_tiles<KIND>(L.s0);
   const int mt0 = m_tile_count<KIND>(L.s0);
   const int tot0 = mt0 * nt0;
@@ -506,8 +524,23 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
   const int cnt0 = (int)((long)tot0 * (xcd + 1) / N_XCD) - lo0;
   const int lo1 = (int)((long)tot1 * xcd / N_XCD);
   const int cnt1 = (int)((long)tot1 * (xcd + 1) / N_XCD) - lo1;
+  const bool dyn = L.counters != nullptr;
+  __shared__ int next_tile[2];  // double-buffered broadcast of the dealt tile
+  int it_parity = 0;
+  int nxt = 0;                  // thread 0: tile prefetched for the next round
+  int i;
+  if (dyn) {
+    if (threadIdx.x == 0) {
+      next_tile[0] = atomicAdd(L.counters + xcd, 1);
+      nxt = atomicAdd(L.counters + xcd, 1);
+    }
+    __syncthreads();
+    i = next_tile[0];
+  } else {
+    i = (int)(blockIdx.x / N_XCD);
+  }
 
-  for (int i = (int)(blockIdx.x / N_XCD); i < cnt0 + cnt1; i += per_xcd) {
+  while (i < cnt0 + cnt1) {
     const bool second = i >= cnt0;
     GemmArgs a;
     if (second) a = L.s1; else a = L.s0;
@@ -661,7 +694,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
             const int col = tl.n0 + wn * 128 + j * 32 + 8 * q + c_in;
             if (col >= a.N) continue;
             float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
-                       (size_t)(tl.m0 + row) * a.ldc + col;
+                       (size_t)tl.split * a.c_split + (size_t)(tl.m0 + row) * a.ldc + col;
             f32x4_t o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                          acc[i][j][4 * q + 3]};
             if (a.accumulate) o += *reinterpret_cast<const f32x4_t*>(c);
@@ -762,7 +795,16 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
         }
       }
     }
+    // next tile: the prefetched counter value (dynamic) or the next stride
+    if (dyn) {
+      it_parity ^= 1;
+      if (threadIdx.x == 0) {
+        next_tile[it_parity] = nxt;
+        if (nxt < cnt0 + cnt1) nxt = atomicAdd(L.counters + xcd, 1);
+      }
+    }
     __syncthreads();  // LDS is reused by the next tile
+    i = dyn ? next_tile[it_parity] : i + per_xcd;
   }
 }
 
@@ -783,27 +825,42 @@ template <int KIND>
 long max_tiles(const GemmArgs& a) {
   const long n_tiles = ceil_div((KIND == GU_FWD) ? 2 * a.H : a.N, GT);
   return Kind<KIND>::MRAG ? (ceil_div(a.cap, GT) + (long)a.n_groups) * n_tiles
-                          : (long)a.n_groups * ceil_div(a.M, GT) * n_tiles;
+                          : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, GT) * n_tiles;
 }
 
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
                                       "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
 
 // One launch over the sets sets[0..n_sets) (at most 2) of one GEMM kind.
+// counters (bf16 only): zeroed per-XCD tile counters for dynamic dealing;
+// zero[0..n_zero): words the launch's block 0 clears for later launches (the
+// launch then runs even without tiles).
 template <int KIND>
-hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s) {
+hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
+                    int* counters = nullptr, int* zero = nullptr, int n_zero = 0) {
   if (bf16) {
     // persistent: at most one block per CU, a multiple of N_XCD blocks
     GemmLaunch L{};
     L.s0 = sets[0];
     L.n_sets = n_sets;
+    // dynamic dealing: the set with the longer reduction per tile goes first,
+    // so that its tiles do not start last
+    auto k_per_tile = [](const GemmArgs& a) -> long {
+      return Kind<KIND>::MRAG ? a.K
+                              : a.cap / std::max(1, a.n_groups) / std::max(1, a.ksplit);
+    };
+    const bool swap = counters && n_sets > 1 && k_per_tile(sets[1]) > k_per_tile(sets[0]);
+    L.counters = counters;
+    L.zero = zero;
+    L.n_zero = n_zero;
     long tiles = max_tiles<KIND>(sets[0]);
     if (n_sets > 1) {
       L.s1 = sets[1];
       tiles += max_tiles<KIND>(sets[1]);
+      if (swap) std::swap(L.s0, L.s1);
     }
-    if (tiles == 0) return hipSuccess;
-    long blocks = std::min<long>(num_cus(), tiles);
+    if (tiles == 0 && n_zero == 0) return hipSuccess;
+    long blocks = std::min<long>(num_cus(), std::max<long>(tiles, 1));
     blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
     MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(L));
     return hipGetLastError();
@@ -827,6 +884,50 @@ hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s) {
   return hipSuccess;
 }
 
+// dst[i] = (accumulate ? dst[i] : 0) + p_0[i] + p_1[i] + ... (fixed order),
+// n % 4 == 0, all 16-byte aligned
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const float* parts,
+                                                            int n_parts, size_t n,
+                                                            int accumulate) {
+  const size_t n4 = n / 4;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
+    f32x4_t v = accumulate ? reinterpret_cast<const f32x4_t*>(dst)[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < n_parts; ++p) v += reinterpret_cast<const f32x4_t*>(parts + p * n)[i];
+    reinterpret_cast<f32x4_t*>(dst)[i] = v;
+  }
+}
+
+// Split-K factor of a K-ragged (weight-gradient) GEMM of one set: a single
+// large group whose M x N tiles cannot fill the CUs (the merged shared
+// experts: one group over all T tokens) is cut into parts of its rows, each
+// part writing its own fp32 partial, summed afterwards in a fixed order.
+int ksplit_factor(int bf16, long M, long N, const moe_ffn_set& f) {
+  if (!bf16 || f.n_groups != 1 || f.cap < 4096) return 1;
+  const long tiles = ceil_div((int)M, GT) * (long)ceil_div((int)N, GT);
+  const long sp = num_cus() / std::max<long>(tiles, 1);
+  return (int)std::max<long>(1, std::min<long>(4, sp));
+}
+
+constexpr size_t kWsAlign = 256;
+constexpr int kCounterWords = 2 * N_XCD;  // DWD then DWGU per-XCD counters
+size_t align_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+}  // namespace
+
+size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
+  size_t bytes = align_up(kCounterWords * sizeof(int));
+  for (int i = 0; i < n_sets; ++i) {
+    const moe_ffn_set& f = sets[i];
+    const long H = f.H;
+    const int s_wd = ksplit_factor(bf16, d, H, f);
+    const int s_wgu = ksplit_factor(bf16, 2 * H, d, f);
+    if (s_wd > 1) bytes += align_up((size_t)s_wd * d * H * sizeof(float));
+    if (s_wgu > 1) bytes += align_up((size_t)s_wgu * 2 * H * d * sizeof(float));
+  }
+  return bytes;
+}
+
+namespace {
 }  // namespace
 
 hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
@@ -855,8 +956,14 @@ hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
 }
 
 hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
-                               int accumulate_dw, hipStream_t s) {
+                               int accumulate_dw, void* ws, hipStream_t s) {
   GemmArgs hh[2]{}, dx[2]{}, wd[2]{}, wgu[2]{};
+  // workspace: per-XCD counters, then the split-K partials
+  int* counters = static_cast<int*>(ws);
+  char* part = static_cast<char*>(ws) + (ws ? align_up(kCounterWords * sizeof(int)) : 0);
+  struct Reduce { float* dst; const float* parts; int n_parts; size_t n; };
+  Reduce red[4];
+  int n_red = 0;
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
     const long H = f.H;
@@ -887,12 +994,37 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     w.B = f.xp; w.ldb = d;
     w.C = f.dw_gate_up; w.ldc = d; w.c_gs = 2 * H * d;
     w.M = 2 * f.H; w.N = d;
+    if (ws) {
+      for (GemmArgs* g : {&c, &w}) {
+        const int S = ksplit_factor(bf16, g->M, g->N, f);
+        if (S <= 1) continue;
+        const size_t n = (size_t)g->M * g->N;
+        red[n_red++] = Reduce{static_cast<float*>(g->C), reinterpret_cast<const float*>(part), S, n};
+        g->C = part;
+        g->ksplit = S;
+        g->c_split = (long)n;
+        g->accumulate = 0;
+        part += align_up((size_t)S * n * sizeof(float));
+      }
+    }
   }
   hipError_t e;
-  if ((e = run_gemm<DHH_BWD>(hh, n_sets, bf16, s)) != hipSuccess) return e;
+  // the first launch clears the counters of the two weight-gradient launches
+  if ((e = run_gemm<DHH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
+                             ws ? kCounterWords : 0)) != hipSuccess)
+    return e;
   if ((e = run_gemm<DX_BWD>(dx, n_sets, bf16, s)) != hipSuccess) return e;
-  if ((e = run_gemm<DWD>(wd, n_sets, bf16, s)) != hipSuccess) return e;
-  return run_gemm<DWGU>(wgu, n_sets, bf16, s);
+  if ((e = run_gemm<DWD>(wd, n_sets, bf16, s, ws ? counters : nullptr)) != hipSuccess) return e;
+  if ((e = run_gemm<DWGU>(wgu, n_sets, bf16, s, ws ? counters + N_XCD : nullptr)) != hipSuccess)
+    return e;
+  for (int r = 0; r < n_red; ++r) {
+    const int blocks = (int)std::min<size_t>(2048, (red[r].n / 4 + 255) / 256);
+    MOE_TIMED("splitk_reduce", s,
+              splitk_reduce_kernel<<<std::max(blocks, 1), 256, 0, s>>>(
+                  red[r].dst, red[r].parts, red[r].n_parts, red[r].n, accumulate_dw));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace moe

@@ -40,8 +40,11 @@ hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, i
 // header), one launch per GEMM kind.
 hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
                                hipStream_t s);
+// ws: NULL (static tile dealing, no split-K) or ffn_bwd_ws_bytes() bytes,
+// 256-byte aligned; its contents on entry are ignored.
+size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d);
 hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
-                               int accumulate_dw, hipStream_t s);
+                               int accumulate_dw, void* ws, hipStream_t s);
 
 constexpr int kMaxPeers = 16;
 hipError_t launch_expert_delta(const float* start, const float* now, const float* const* peers,

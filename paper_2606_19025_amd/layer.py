@@ -67,6 +67,7 @@ class ResidentMoELayer:
         self.d_bias = e(E, dt=f32)
         self.ws_route_bytes = B.moe_route_bwd_workspace_size(T, d, E)
         self.ws_route = e(self.ws_route_bytes, dt=torch.uint8)
+        self.ws_ffn, self.ws_ffn_bytes = None, 0  # sized on the first backward
         if self.Hs:
             Hs = self.Hs
             self.s_offsets = torch.tensor([0, T], dtype=i32, device=dev)
@@ -114,7 +115,11 @@ class ResidentMoELayer:
             sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
                                   self.s_gu, self.s_h, dyp=dy, dgu=self.s_dgu, dxp=self.dx,
                                   dw_gate_up=self.s_dw_gate_up, dw_down=self.s_dw_down))
-        B.moe_grouped_ffn_bwd_sets(sets, dt, d, accumulate_dw, stream)
+        if self.ws_ffn is None:
+            self.ws_ffn_bytes = B.moe_grouped_ffn_bwd_workspace_size(sets, dt, d)
+            self.ws_ffn = torch.empty(self.ws_ffn_bytes, dtype=torch.uint8, device=self.device)
+        B.moe_grouped_ffn_bwd_sets(sets, dt, d, accumulate_dw, self.ws_ffn, self.ws_ffn_bytes,
+                                   stream)
         B.moe_dispatch_bwd(self.dxp, dt, T, d, k, cap, self.inv_perm, self.dx, 1 if self.Hs else 0,
                            stream)
         B.moe_route_bwd(x, w_router, dt, T, d, E, k, self.inv_tau, self.gate, self.topk_idx,

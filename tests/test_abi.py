@@ -133,5 +133,15 @@ def test_ffn_sets_reject_bad_arguments(lib):
     no_grad = B.ffn_set(p, p, p, p, 64, 128, 2, p, p, dyp=p, dgu=p, dxp=p)  # dW pointers NULL
     arr = (B.moe_ffn_set * 1)(no_grad)
     assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 128, 0,
-                                            None) == ERR_ARG
+                                            None, 0, None) == ERR_ARG
     assert "gradients" in B.moe_last_error()
+    good = B.ffn_set(p, p, p, p, 8192, 1408, 1, p, p, dyp=p, dgu=p, dxp=p, dw_gate_up=p,
+                     dw_down=p)
+    need = B.moe_grouped_ffn_bwd_workspace_size([good], B.MOE_BF16, 2048)
+    assert need >= 64  # the tile counters at least
+    arr = (B.moe_ffn_set * 1)(good)
+    assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 2048, 0,
+                                            4096, need - 1, None) == ERR_ARG
+    assert "workspace" in B.moe_last_error()
+    assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 2048, 0,
+                                            4096 + 16, need, None) == ERR_UNSUPPORTED
