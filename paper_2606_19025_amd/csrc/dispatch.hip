@@ -39,34 +39,60 @@ __global__ __launch_bounds__(DB) void dispatch_count_kernel(const int32_t* local
   for (int r = threadIdx.x; r < E_r; r += DB) blk_counts[(size_t)blockIdx.x * E_r + r] = hist[r];
 }
 
-// One block: counts, offsets and blk_base[b][r] = offsets[r] + sum_{b'<b} cnt[b'][r].
-__global__ __launch_bounds__(256) void dispatch_scan_kernel(const int32_t* blk_counts, int nblk,
-                                                           int E_r, int32_t* blk_base,
-                                                           int32_t* counts, int32_t* offsets) {
-  __shared__ int tot[257];
-  const int r = threadIdx.x;
-  int run = 0;
-  if (r < E_r) {
-    for (int b = 0; b < nblk; ++b) {
-      blk_base[(size_t)b * E_r + r] = run;
-      run += blk_counts[(size_t)b * E_r + r];
+// Inclusive prefix sum over the 64 lanes of a wave.
+DEVI int wave_inclusive_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// One block of 16 waves: wave w scans experts w, w + 16, ... over the
+// counting blocks (blk_base[b][r] = offsets[r] + sum_{b'<b} cnt[b'][r]); then
+// wave 0 scans the expert totals into counts and offsets.
+constexpr int SCAN_WAVES = 16;
+__global__ __launch_bounds__(64 * SCAN_WAVES) void dispatch_scan_kernel(const int32_t* blk_counts,
+                                                                       int nblk, int E_r,
+                                                                       int32_t* blk_base,
+                                                                       int32_t* counts,
+                                                                       int32_t* offsets) {
+  __shared__ int tot[256];
+  __shared__ int base[256];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  for (int r = wave; r < E_r; r += SCAN_WAVES) {
+    int carry = 0;
+    for (int b0 = 0; b0 < nblk; b0 += 64) {
+      const int b = b0 + lane;
+      const int c = b < nblk ? blk_counts[(size_t)b * E_r + r] : 0;
+      const int inc = wave_inclusive_scan(c);
+      if (b < nblk) blk_base[(size_t)b * E_r + r] = carry + inc - c;  // relative, fixed below
+      carry += __shfl(inc, 63, 64);
     }
-    counts[r] = run;
-  }
-  tot[r] = (r < E_r) ? run : 0;
-  __syncthreads();
-  if (r == 0) {  // exclusive scan over at most 256 experts, in order
-    int s = 0;
-    for (int i = 0; i < E_r; ++i) { const int c = tot[i]; tot[i] = s; s += c; }
-    tot[256] = s;
+    if (lane == 0) tot[r] = carry;
   }
   __syncthreads();
-  if (r < E_r) {
-    const int base = tot[r];
-    offsets[r] = base;
-    for (int b = 0; b < nblk; ++b) blk_base[(size_t)b * E_r + r] += base;
+  if (wave == 0) {
+    int carry = 0;
+    for (int r0 = 0; r0 < E_r; r0 += 64) {
+      const int r = r0 + lane;
+      const int c = r < E_r ? tot[r] : 0;
+      const int inc = wave_inclusive_scan(c);
+      if (r < E_r) {
+        base[r] = carry + inc - c;
+        counts[r] = c;
+        offsets[r] = carry + inc - c;
+      }
+      carry += __shfl(inc, 63, 64);
+    }
+    if (lane == 0) offsets[E_r] = carry;
   }
-  if (r == 0) offsets[E_r] = tot[256];
+  __syncthreads();
+  for (int r = wave; r < E_r; r += SCAN_WAVES)
+    for (int b = lane; b < nblk; b += 64) blk_base[(size_t)b * E_r + r] += base[r];
 }
 
 __global__ __launch_bounds__(DB) void dispatch_scatter_kernel(const int32_t* local, int T, int k,
@@ -104,19 +130,53 @@ __global__ __launch_bounds__(DB) void dispatch_scatter_kernel(const int32_t* loc
   }
 }
 
-// Slot of route (t, j) (o = t*k): lanes j < k read inv_perm and broadcast;
-// slots outside [0, cap) count as ghost routes.
-DEVI int slot_of(const int32_t* inv_perm, size_t o, int j, int k, int cap) {
-  const int lane = threadIdx.x & 63;
-  int p;
-  if (k <= 64) {
-    const int mine = (lane < k) ? inv_perm[o + lane] : -1;
-    p = __shfl(mine, j & 63, 64);
-  } else {
-    p = inv_perm[o + j];
-  }
+// The resident routes of token t (o = t*k) in route order: up to KR of them
+// as wave-uniform (slot, weight) pairs; slots outside [0, cap) count as ghost
+// routes.  Routes past the KR-th resident one (k > KR) are handled by the
+// callers' generic loop, using slot_of.
+constexpr int KR = 8;
+
+DEVI int slot_of(const int32_t* inv_perm, size_t o, int j, int cap) {
+  const int p = inv_perm[o + j];
   return (p >= 0 && p < cap) ? p : -1;
 }
+
+// Returns the number of resident routes n (all k routes scanned when k <= 64);
+// fills p[0..min(n, KR)) and w[...] (weights from tw, or 1 when tw is NULL).
+// j_rest receives the route index after the KR-th resident route (k if none).
+DEVI int token_routes(const int32_t* inv_perm, const float* tw, size_t o, int k, int cap, int* p,
+                      float* w, int& j_rest) {
+  const int lane = threadIdx.x & 63;
+  int n = 0;
+  j_rest = k;
+  for (int j0 = 0; j0 < k; j0 += 64) {
+    const int j = j0 + lane;
+    int pj = -1;
+    float wj = 1.f;
+    if (j < k) {
+      pj = slot_of(inv_perm, o, j, cap);
+      if (tw) wj = tw[o + j];
+    }
+    uint64_t m = __ballot(pj >= 0);
+    while (m) {
+      const int src = __builtin_ctzll(m);
+      m &= m - 1;
+      if (n < KR) {
+        p[n] = __shfl(pj, src, 64);
+        w[n] = __shfl(wj, src, 64);
+      } else if (n == KR) {
+        j_rest = j0 + src;
+      }
+      ++n;
+    }
+    if (n > KR) break;
+  }
+  return n;
+}
+
+// Columns of a row handled per lane and pass: CPL chunks of 16 bytes, lanes
+// interleaved (chunk cc of lane l is element (cc * 64 + l) * V).
+constexpr int CPL = 4;
 
 template <class T>
 __global__ __launch_bounds__(256) void gather_rows_kernel(const T* x, int T_, int d, int k, int cap,
@@ -126,23 +186,102 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* x, int T_, in
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T_) return;
   const size_t o = (size_t)t * k;
-  int slots[8];
-  int ns = 0;
-  for (int j = 0; j < k; ++j) {
-    const int p = slot_of(inv_perm, o, j, k, cap);
-    if (p >= 0) {
-      if (ns < 8) slots[ns++] = p;
-      else {  // more than 8 resident routes: copy this one directly
-        for (int c = lane * V; c < d; c += 64 * V)
-          *reinterpret_cast<u32x4_t*>(xp + (size_t)p * d + c) =
-              *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
+  int p[KR];
+  float w[KR];
+  int j_rest;
+  const int n = token_routes(inv_perm, nullptr, o, k, cap, p, w, j_rest);
+  if (n == 0) return;
+  const int nr = min(n, KR);
+  for (int c0 = 0; c0 < d; c0 += CPL * 64 * V) {
+    u32x4_t v[CPL];
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc) {
+      const int c = c0 + (cc * 64 + lane) * V;
+      if (c < d) v[cc] = *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
+    }
+#pragma unroll
+    for (int s = 0; s < KR; ++s) {
+      if (s >= nr) break;
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (c < d) *reinterpret_cast<u32x4_t*>(xp + (size_t)p[s] * d + c) = v[cc];
+      }
+    }
+    for (int j = j_rest; j < k; ++j) {  // resident routes beyond the first KR
+      const int q = slot_of(inv_perm, o, j, cap);
+      if (q < 0) continue;
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (c < d) *reinterpret_cast<u32x4_t*>(xp + (size_t)q * d + c) = v[cc];
       }
     }
   }
-  if (ns == 0) return;
-  for (int c = lane * V; c < d; c += 64 * V) {
-    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
-    for (int s = 0; s < ns; ++s) *reinterpret_cast<u32x4_t*>(xp + (size_t)slots[s] * d + c) = v;
+}
+
+// y[t] = sum over resident routes (in route order) of w * rows[slot] (+ add[t]);
+// combine forward (weights tw, add = shared output) and un-permute (tw NULL,
+// add = dx when accumulating, out = dx).
+template <class T>
+DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const float* tw,
+                           const int32_t* inv_perm, const T* add, T* out) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  int p[KR];
+  float w[KR];
+  int j_rest;
+  const int n = token_routes(inv_perm, tw, o, k, cap, p, w, j_rest);
+  const int nr = min(n, KR);
+  for (int c0 = 0; c0 < d; c0 += CPL * 64 * V) {
+    float acc[CPL][V];
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc)
+#pragma unroll
+      for (int u = 0; u < V; ++u) acc[cc][u] = 0.f;
+#pragma unroll
+    for (int s = 0; s < KR; ++s) {
+      if (s >= nr) break;
+      float v[CPL][V];
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (c < d) load16_f32(rows + (size_t)p[s] * d + c, v[cc]);
+      }
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc)
+#pragma unroll
+        for (int u = 0; u < V; ++u) acc[cc][u] = fmaf(w[s], v[cc][u], acc[cc][u]);
+    }
+    for (int j = j_rest; j < k; ++j) {
+      const int q = slot_of(inv_perm, o, j, cap);
+      if (q < 0) continue;
+      const float wq = tw ? tw[o + j] : 1.f;
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (c >= d) continue;
+        float v[V];
+        load16_f32(rows + (size_t)q * d + c, v);
+#pragma unroll
+        for (int u = 0; u < V; ++u) acc[cc][u] = fmaf(wq, v[u], acc[cc][u]);
+      }
+    }
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc) {
+      const int c = c0 + (cc * 64 + lane) * V;
+      if (c >= d) continue;
+      if (add) {
+        float v[V];
+        load16_f32(add + (size_t)t * d + c, v);
+#pragma unroll
+        for (int u = 0; u < V; ++u) acc[cc][u] += v[u];
+      }
+      store16_f32(out + (size_t)t * d + c, acc[cc]);
+    }
   }
 }
 
@@ -150,30 +289,7 @@ template <class T>
 __global__ __launch_bounds__(256) void unpermute_kernel(const T* dxp, int T_, int d, int k, int cap,
                                                         const int32_t* inv_perm, T* dx,
                                                         int accumulate) {
-  constexpr int V = Vec16<T>::N;
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T_) return;
-  const size_t o = (size_t)t * k;
-  // the column loop runs the same number of times in every lane, so the slot
-  // broadcasts (cross-lane) always read active lanes
-  for (int c0 = 0; c0 < d; c0 += 64 * V) {
-    const int c = c0 + lane * V;
-    const bool act = c < d;
-    float acc[V];
-#pragma unroll
-    for (int u = 0; u < V; ++u) acc[u] = 0.f;
-    if (accumulate && act) load16_f32(dx + (size_t)t * d + c, acc);
-    for (int j = 0; j < k; ++j) {
-      const int p = slot_of(inv_perm, o, j, k, cap);
-      if (p < 0 || !act) continue;
-      float v[V];
-      load16_f32(dxp + (size_t)p * d + c, v);
-#pragma unroll
-      for (int u = 0; u < V; ++u) acc[u] += v[u];
-    }
-    if (act) store16_f32(dx + (size_t)t * d + c, acc);
-  }
+  weighted_row_sum<T>(dxp, T_, d, k, cap, nullptr, inv_perm, accumulate ? dx : nullptr, dx);
 }
 
 template <class T>
@@ -181,37 +297,12 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(const T* yp, int T_, i
                                                           const float* tw,
                                                           const int32_t* inv_perm,
                                                           const T* y_add, T* y) {
-  constexpr int V = Vec16<T>::N;
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T_) return;
-  const size_t o = (size_t)t * k;
-  for (int c0 = 0; c0 < d; c0 += 64 * V) {  // same trip count in every lane
-    const int c = c0 + lane * V;
-    const bool act = c < d;
-    float acc[V];
-#pragma unroll
-    for (int u = 0; u < V; ++u) acc[u] = 0.f;
-    for (int j = 0; j < k; ++j) {
-      const int p = slot_of(inv_perm, o, j, k, cap);
-      if (p < 0 || !act) continue;  // ghost route: skipped
-      const float wj = tw[o + j];
-      float v[V];
-      load16_f32(yp + (size_t)p * d + c, v);
-#pragma unroll
-      for (int u = 0; u < V; ++u) acc[u] = fmaf(wj, v[u], acc[u]);
-    }
-    if (!act) continue;
-    if (y_add) {
-      float v[V];
-      load16_f32(y_add + (size_t)t * d + c, v);
-#pragma unroll
-      for (int u = 0; u < V; ++u) acc[u] += v[u];
-    }
-    store16_f32(y + (size_t)t * d + c, acc);
-  }
+  weighted_row_sum<T>(yp, T_, d, k, cap, tw, inv_perm, y_add, y);
 }
 
+// dyp[slot] = w * dy[t] and dtw[t, j] = <dy[t], yp[slot]> for every resident
+// route, one route after the other (0 for ghost routes).  Kept lean on
+// registers: this kernel runs best at full occupancy.
 template <class T>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* dy, const T* yp, int T_, int d,
                                                           int k, int cap, const float* tw,
@@ -222,13 +313,16 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* dy, const T* 
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T_) return;
   const size_t o = (size_t)t * k;
+  // lanes j < 64 hold route j's slot and weight
+  const int my_p = lane < k ? slot_of(inv_perm, o, lane, cap) : -1;
+  const float my_w = lane < k ? tw[o + lane] : 0.f;
   for (int j = 0; j < k; ++j) {
-    const int p = slot_of(inv_perm, o, j, k, cap);
+    const int p = j < 64 ? __shfl(my_p, j, 64) : slot_of(inv_perm, o, j, cap);
     if (p < 0) {  // ghost route: no gradient
       if (lane == 0) dtw[o + j] = 0.f;
       continue;
     }
-    const float wj = tw[o + j];
+    const float wj = j < 64 ? __shfl(my_w, j, 64) : tw[o + j];
     float dot = 0.f;
     for (int c = lane * V; c < d; c += 64 * V) {
       float g[V], v[V], out[V];
@@ -297,8 +391,8 @@ hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r
   if (nblk > 0 && E_r > 0)
     MOE_TIMED("dispatch_count", s, dispatch_count_kernel<<<nblk, DB, 0, s>>>(local, T, k, E_r, blk_counts));
   MOE_TIMED("dispatch_scan", s,
-            dispatch_scan_kernel<<<1, 256, 0, s>>>(blk_counts, E_r > 0 ? nblk : 0, E_r, blk_base,
-                                                   counts, offsets));
+            dispatch_scan_kernel<<<1, 64 * SCAN_WAVES, 0, s>>>(blk_counts, E_r > 0 ? nblk : 0, E_r,
+                                                               blk_base, counts, offsets));
   if (nblk > 0) {
     MOE_TIMED("dispatch_scatter", s,
               dispatch_scatter_kernel<<<nblk, DB, 0, s>>>(local, T, k, E_r, cap, blk_base, perm,

@@ -891,8 +891,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const fl
                                                             int accumulate) {
   const size_t n4 = n / 4;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
+    f32x4_t q[4];  // all loads first (n_parts <= 4)
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      if (p < n_parts) q[p] = reinterpret_cast<const f32x4_t*>(parts + p * n)[i];
     f32x4_t v = accumulate ? reinterpret_cast<const f32x4_t*>(dst)[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int p = 0; p < n_parts; ++p) v += reinterpret_cast<const f32x4_t*>(parts + p * n)[i];
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      if (p < n_parts) v += q[p];
     reinterpret_cast<f32x4_t*>(dst)[i] = v;
   }
 }
@@ -1018,7 +1024,7 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
   if ((e = run_gemm<DWGU>(wgu, n_sets, bf16, s, ws ? counters + N_XCD : nullptr)) != hipSuccess)
     return e;
   for (int r = 0; r < n_red; ++r) {
-    const int blocks = (int)std::min<size_t>(2048, (red[r].n / 4 + 255) / 256);
+    const int blocks = (int)std::min<size_t>(8192, (red[r].n / 4 + 255) / 256);
     MOE_TIMED("splitk_reduce", s,
               splitk_reduce_kernel<<<std::max(blocks, 1), 256, 0, s>>>(
                   red[r].dst, red[r].parts, red[r].n_parts, red[r].n, accumulate_dw));
