@@ -52,10 +52,11 @@ _SYMBOLS = [
     (r"combine_bwd_kernel", lambda m: "combine_bwd"),
     (r"unpermute_kernel", lambda m: "unpermute"),
     (r"expert_delta_kernel", lambda m: "expert_delta"),
+    (r"splitk_reduce_kernel", lambda m: "splitk_reduce"),
 ]
 
 # timing name prefix -> source file that holds the kernel
-_SOURCES = [("gemm_", "gemm.hip"), ("route_", "route.hip"), ("dispatch_", "dispatch.hip"),
+_SOURCES = [("gemm_", "gemm.hip"), ("splitk_", "gemm.hip"), ("route_", "route.hip"), ("dispatch_", "dispatch.hip"),
             ("combine_", "dispatch.hip"), ("unpermute", "dispatch.hip"),
             ("expert_delta", "dispatch.hip")]
 
