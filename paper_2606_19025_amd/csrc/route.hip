@@ -147,6 +147,91 @@ DEVI void logits_f32(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   __syncthreads();
 }
 
+// Logit as read for selection: NaN ranks as -inf (some expert is always
+// picked) and -0 as +0 (they tie, as equal values do).
+DEVI float sel_value(float v) { return (v != v) ? -INFINITY : v + 0.0f; }
+
+// Order-preserving map of a float to uint32 (larger float -> larger key);
+// every float maps above 0, the key of an empty slot.
+DEVI uint32_t sel_key(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int RT_KSEL = 8;
+
+// Insert (kv, e) into slots kept in descending key order.  A strictly larger
+// key is needed to pass a slot, so among equal logits the expert inserted
+// first (the lower id) ranks first.
+DEVI void sel_insert(uint32_t* key, int* id, uint32_t kv, int e) {
+#pragma unroll
+  for (int j = RT_KSEL - 1; j >= 1; --j) {
+    const bool up = kv > key[j - 1];
+    const bool here = kv > key[j];
+    key[j] = up ? key[j - 1] : (here ? kv : key[j]);
+    id[j] = up ? id[j - 1] : (here ? e : id[j]);
+  }
+  if (kv > key[0]) { key[0] = kv; id[0] = e; }
+}
+
+// Top-k, gate weights and local ids of the block's tokens, two lanes per
+// token (run by all 64 lanes of one wave): lane l scans the lower half of
+// token l % 32's experts if l < 32, else the upper half; the upper lane's
+// top RT_KSEL is then merged into the lower lane's (inserted after it, so
+// ties still go to the lower id).  The first k of the top RT_KSEL are the
+// top k.
+template <int LDZ>
+DEVI void select_pairs(const RouteFwdArgs& a, const float* zl, int t0, const int* lmap) {
+  const int lane = threadIdx.x & 63;
+  const int i = lane & 31, half = lane >> 5;
+  const float* z = zl + i * LDZ;
+  const int e_mid = (a.E + 1) / 2;
+  const int eb = half ? e_mid : 0, ee = half ? a.E : e_mid;
+  uint32_t key[RT_KSEL];
+  int id[RT_KSEL];
+#pragma unroll
+  for (int j = 0; j < RT_KSEL; ++j) { key[j] = 0u; id[j] = 0; }
+  for (int e = eb; e < ee; ++e) sel_insert(key, id, sel_key(sel_value(z[e])), e);
+  uint32_t uk[RT_KSEL];
+  int ui[RT_KSEL];
+#pragma unroll
+  for (int j = 0; j < RT_KSEL; ++j) {
+    uk[j] = (uint32_t)__shfl((int)key[j], lane | 32, 64);
+    ui[j] = __shfl(id[j], lane | 32, 64);
+  }
+  const int t = t0 + i;
+  if (half || t >= a.T) return;
+#pragma unroll
+  for (int j = 0; j < RT_KSEL; ++j)
+    if (uk[j] != 0u) sel_insert(key, id, uk[j], ui[j]);
+  float zs[RT_KSEL];
+#pragma unroll
+  for (int j = 0; j < RT_KSEL; ++j) zs[j] = sel_value(z[id[j]]);
+  const float zmax = zs[0];
+  float denom = 1.f;
+  if (a.gate == 0) {  // softmax over the k selected logits
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < RT_KSEL; ++j)
+      if (j < a.k) s += expf(zs[j] - zmax);
+    denom = s;
+  } else if (a.gate == 1) {  // softmax over all E logits
+    float s = 0.f;
+    for (int e = 0; e < a.E; ++e) s += expf(sel_value(z[e]) - zmax);
+    denom = s;
+  }
+#pragma unroll
+  for (int j = 0; j < RT_KSEL; ++j) {
+    if (j < a.k) {
+      const float wj = (a.gate == 2) ? sigmoid_f(zs[j]) : expf(zs[j] - zmax) / denom;
+      const size_t o = (size_t)t * a.k + j;
+      a.idx[o] = id[j];
+      a.tw[o] = wj;
+      a.local[o] = lmap[id[j]];
+    }
+  }
+}
+
 template <int NEB, bool BF16>
 __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   constexpr int LDZ = NEB * 32 + 1;
@@ -171,6 +256,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   }
   __syncthreads();
 
+  if (a.k <= RT_KSEL) {
+    // two lanes per token: running top-RT_KSEL lists in registers
+    static_assert(RT_TOK == 32, "two lanes per token in one wave");
+    if (wave == 0) select_pairs<LDZ>(a, zl, t0, lmap);
+    return;
+  }
   for (int i = wave; i < RT_TOK; i += RT_WAVES) {
     const int t = t0 + i;
     if (t >= a.T) break;

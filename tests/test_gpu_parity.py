@@ -61,6 +61,7 @@ CASES = {
     "no-resident": (128, 64, 8, 2, 64, [], "bf16", 64, False, "softmax_topk", 1.0),
     "many-experts": (300, 64, 256, 8, 64, list(range(0, 256, 5)), "bf16", 0, False, "softmax_topk", 1.0),
     "multi-tile-groups": (1500, 256, 4, 2, 256, [0, 1, 3], "bf16", 0, False, "softmax_topk", 1.0),
+    "k12-wave-select": (200, 64, 32, 12, 64, list(range(0, 32, 3)), "bf16", 0, False, "softmax_topk", 1.0),
 }
 
 
