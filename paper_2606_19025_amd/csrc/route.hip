@@ -455,7 +455,15 @@ __global__ __launch_bounds__(256) void route_dw_reduce_kernel(RouteBwdArgs a) {
   if (a.db && blockIdx.x == 0) {
     for (int e = threadIdx.x; e < a.E; e += 256) {
       float s = 0.f;
-      for (int c = 0; c < a.n_chunks; ++c) s += a.part_b[(size_t)c * a.E + e];
+      int c = 0;
+      for (; c + 8 <= a.n_chunks; c += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = a.part_b[(size_t)(c + u) * a.E + e];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+      }
+      for (; c < a.n_chunks; ++c) s += a.part_b[(size_t)c * a.E + e];
       a.db[e] = s * a.inv_tau;
     }
   }
