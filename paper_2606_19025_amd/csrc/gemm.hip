@@ -17,15 +17,10 @@
 // The first four are ragged in M (tiles are laid over the groups from the
 // device-side offsets; no host read-back), the last two ragged in K.
 //
-// bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Block tile 128x128,
-// k-step 64, 4 waves of 64x64 (2x2 MFMA tiles each).  Both operands are kept
-// in LDS k-contiguous (row = M or N index, 64 bf16 = 128 B per row) with the
-// 16-byte chunks XOR-swizzled by (row & 7); the two stages are double
-// buffered so the global loads of step k+1 overlap the MFMAs of step k.
-// Operands that are contiguous along M/N in memory (the TN weight-gradient
-// GEMMs and the NN weight operand) are loaded as 4 k-rows x 8 elements per
-// thread (16-byte coalesced loads) and transposed in registers before the
-// LDS store.
+// bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulation in a persistent
+// kernel with 256 x 256 block tiles fed from a 4-stage LDS ring by
+// global -> LDS DMA (details at gemm_bf16_kernel).  One launch per GEMM kind
+// covers up to two expert sets (routed and shared experts).
 // fp32: a plain 64x64 SIMT tile (4x4 outputs per thread) with the same
 // epilogues; used for fp32 layers.
 #include "common.h"
@@ -257,8 +252,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 //
 // Tile order (see tile_decode): bands of GROUP_M m-tiles.  Workgroups are
 // dealt to the 8 XCDs round-robin by id, so block b works on tiles of the
-// contiguous range assigned to XCD b % 8: the 32 tiles an XCD runs at a time
-// form a GROUP_M x 8 rectangle whose operand panels its L2 serves.
+// ranges assigned to XCD b % 8 (an eighth of each set's tiles): the 32 tiles
+// an XCD runs at a time form a GROUP_M x 8 rectangle whose operand panels its
+// L2 serves.  Output tiles end in an epilogue: bf16 results are staged
+// through the drained ring so global accesses are whole 16-byte chunks;
+// fp32 weight gradients are stored (or added) straight from the
+// accumulators.
 //
 // LDS layouts (per operand and stage, 16 KB):
 //  k-contiguous operand (rows = M or N index): row r holds 32 k = 64 B; its
