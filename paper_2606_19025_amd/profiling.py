@@ -73,14 +73,23 @@ def timing_name(symbol: str) -> str | None:
     return None
 
 
+def _code_only(src: str) -> str:
+    """C++ source without comments and with whitespace runs collapsed, so that
+    editing a comment does not count as changing the kernel."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def source_digest(name: str) -> str | None:
-    """sha256 (16 hex digits) of the kernel's source file and the shared header."""
+    """sha256 (16 hex digits) of the code of the kernel's source file and the
+    shared header (comments and layout ignored)."""
     for prefix, fname in _SOURCES:
         if name.startswith(prefix):
             h = hashlib.sha256()
             for f in (fname, "common.h"):
-                with open(os.path.join(CSRC, f), "rb") as fh:
-                    h.update(fh.read())
+                with open(os.path.join(CSRC, f)) as fh:
+                    h.update(_code_only(fh.read()).encode())
             return h.hexdigest()[:16]
     return None
 

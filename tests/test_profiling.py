@@ -38,3 +38,11 @@ def test_traffic_summary_is_scaled_by_the_calibration_copy(tmp_path):
     assert abs(b - (200.0 * 1024 * 2 + 50.0 * 1024)) < 1.0
     assert dg == P.source_digest("gemm_gu_fwd")
     assert "FETCH_SIZE" in out.read_text()
+
+
+def test_digest_ignores_comments_and_layout():
+    a = "int f(int x) {  // doubles x\n  return 2 * x; /* no overflow check */\n}\n"
+    b = "// header\nint f(int x) {\n    return 2 * x;\n}"
+    c = "int f(int x) { return 3 * x; }"
+    assert P._code_only(a) == P._code_only(b)
+    assert P._code_only(a) != P._code_only(c)
