@@ -522,7 +522,8 @@ __global__ __launch_bounds__(256) void route_dx_kernel(RouteBwdArgs a) {
 //   dx[t, c] (+)= inv_tau * sum_e (hi + lo)[t, e] W_r[e, c]       (k = experts)
 // with v_mfma_f32_32x32x16_bf16; wave w owns columns 32w..32w+31 of both.
 // The next sub-chunk's x and dz are loaded into registers while the current
-// one is computed.  The per-chunk dW partials (and the d_bias partials of
+// one is computed; the dx result is staged through LDS so that the update of
+// dx reads and writes whole row segments.  The per-chunk dW partials (and the d_bias partials of
 // blockIdx.x == 0) are summed in a fixed order by route_dw_reduce_kernel.
 constexpr int RBM_COLS = 128;
 constexpr int RBM_SUB = 64;                   // tokens per sub-chunk
@@ -532,6 +533,9 @@ constexpr int RBM_ZS = 64 * 2 + 16;           // dz row stride: 16 rows of a 16-
                                               // read on distinct banks
 constexpr int RBM_WS = RBM_COLS * 2 + 64;     // W_r row stride
 constexpr int RBM_LDS = RBM_SUB * RBM_XS + 2 * RBM_SUB * RBM_ZS + 64 * RBM_WS;
+constexpr int RBM_STG = RBM_COLS + 4;  // fp32 row stride of the staged dx update
+static_assert(RBM_SUB * RBM_STG * 4 <= RBM_SUB * RBM_XS + 2 * RBM_SUB * RBM_ZS,
+              "the staged dx update must fit over the x and dz tiles");
 constexpr int RBM_XV = RBM_SUB * RBM_COLS / 8 / 256;  // 16-byte x vectors per thread
 constexpr int RBM_ZV = RBM_SUB * 64 / 8 / 256;        // 8-expert dz groups per thread
 static_assert(RBM_XV * 256 * 8 == RBM_SUB * RBM_COLS && RBM_ZV * 256 * 8 == RBM_SUB * 64,
@@ -629,16 +633,15 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
         if (t < a.T) bsum += a.dz[(size_t)t * a.E + lane];
       }
     }
-    // old dx of this wave's outputs (read before the MFMAs)
-    bf16x4_t old[2][4];
+    // old dx of this thread's 16-byte chunks of the sub-chunk (requested
+    // before the MFMAs; used by the coalesced update below)
+    u32x4_t old[RBM_XV];
     if (a.accumulate_dx) {
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-        const int t = min(t0 + tb * 32 + (lane & 31), a.T - 1);
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          old[tb][q] = *reinterpret_cast<const bf16x4_t*>(
-              dx + (size_t)t * a.d + c0 + wave * 32 + 8 * q + 4 * (lane >> 5));
+      for (int v = 0; v < RBM_XV; ++v) {
+        const int p = tid + 256 * v;
+        const int t = min(t0 + (p >> 4), a.T - 1);
+        old[v] = *reinterpret_cast<const u32x4_t*>(dx + (size_t)t * a.d + c0 + (p & 15) * 8);
       }
     }
 
@@ -670,22 +673,37 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
         accx[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw, al, accx[tb], 0, 0, 0);
       }
     }
-    // lane holds dx[t0 + 32 tb + lane%32][c0 + 32 wave + 8q + 4(lane/32) + 0..3]
+    // lane holds dx[t0 + 32 tb + lane%32][c0 + 32 wave + 8q + 4(lane/32) + 0..3];
+    // staged as fp32 through LDS (over the x and dz tiles, now consumed) so
+    // that the update of dx reads and writes whole 256-byte row segments
+    __syncthreads();
+    float* stg = reinterpret_cast<float*>(lds);
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const int t = t0 + tb * 32 + (lane & 31);
-      if (t >= a.T) continue;
+    for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        bf16_t* p = dx + (size_t)t * a.d + c0 + wave * 32 + 8 * q + 4 * (lane >> 5);
-        bf16x4_t o;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float v = a.inv_tau * accx[tb][4 * q + u];
-          o[u] = (bf16_t)(a.accumulate_dx ? (float)old[tb][q][u] + v : v);
-        }
-        *reinterpret_cast<bf16x4_t*>(p) = o;
+        const f32x4_t v = {accx[tb][4 * q], accx[tb][4 * q + 1], accx[tb][4 * q + 2],
+                           accx[tb][4 * q + 3]};
+        *reinterpret_cast<f32x4_t*>(stg + (tb * 32 + (lane & 31)) * RBM_STG +
+                                    wave * 32 + 8 * q + 4 * (lane >> 5)) = v;
       }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < RBM_XV; ++v) {
+      const int p = tid + 256 * v;
+      const int r = p >> 4, c = (p & 15) * 8;
+      const int t = t0 + r;
+      if (t >= a.T) continue;
+      const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(stg + r * RBM_STG + c);
+      const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(stg + r * RBM_STG + c + 4);
+      const bf16x8_t ob = __builtin_bit_cast(bf16x8_t, old[v]);
+      bf16x8_t o;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float add = a.inv_tau * (u < 4 ? lo[u] : hi[u - 4]);
+        o[u] = (bf16_t)(a.accumulate_dx ? (float)ob[u] + add : add);
+      }
+      *reinterpret_cast<bf16x8_t*>(dx + (size_t)t * a.d + c0 + c) = o;
     }
   }
 
