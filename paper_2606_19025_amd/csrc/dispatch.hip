@@ -220,9 +220,32 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* x, int T_, in
   }
 }
 
+// 16 bytes of T held as raw words, widened to fp32 (exact).
+DEVI void unpack16_f32(const u32x4_t& r, float* out, const float*) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(r[i]);
+}
+DEVI void unpack16_f32(const u32x4_t& r, float* out, const bf16_t*) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(r[i] << 16);
+    out[2 * i + 1] = __uint_as_float(r[i] & 0xffff0000u);
+  }
+}
+
+// Routes whose rows are requested together, before any of them is summed.
+constexpr int RB = 4;
+// 16-byte chunks per lane and column pass of the weighted row sums.
+constexpr int WCPL = 2;
+
 // y[t] = sum over resident routes (in route order) of w * rows[slot] (+ add[t]);
 // combine forward (weights tw, add = shared output) and un-permute (tw NULL,
-// add = dx when accumulating, out = dx).
+// add = dx when accumulating, out = dx).  Per column pass, the add chunks and
+// the rows of up to RB routes are loaded before the first is used, so a token
+// costs one memory round trip per pass rather than one per route; the sums
+// keep the route order.  A separate add row is requested before the route
+// lookup; in place (add == out), a token without resident routes is left as
+// it is.
 template <class T>
 DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const float* tw,
                            const int32_t* inv_perm, const T* add, T* out) {
@@ -231,37 +254,62 @@ DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const f
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T_) return;
   const size_t o = (size_t)t * k;
+  const bool in_place = add == out;
+  const T* add_row = add ? add + (size_t)t * d : nullptr;
+  u32x4_t a_raw[WCPL];
+  auto load_add = [&](int c0) {
+#pragma unroll
+    for (int cc = 0; cc < WCPL; ++cc) {
+      const int c = c0 + (cc * 64 + lane) * V;
+      if (c < d) a_raw[cc] = *reinterpret_cast<const u32x4_t*>(add_row + c);
+    }
+  };
+  const bool early_add = add && !in_place;
+  if (early_add) load_add(0);
   int p[KR];
   float w[KR];
   int j_rest;
   const int n = token_routes(inv_perm, tw, o, k, cap, p, w, j_rest);
+  if (n == 0 && in_place) return;
   const int nr = min(n, KR);
-  for (int c0 = 0; c0 < d; c0 += CPL * 64 * V) {
-    float acc[CPL][V];
+  for (int c0 = 0; c0 < d; c0 += WCPL * 64 * V) {
+    if (add && (c0 > 0 || !early_add)) load_add(c0);
+    float acc[WCPL][V];
 #pragma unroll
-    for (int cc = 0; cc < CPL; ++cc)
+    for (int cc = 0; cc < WCPL; ++cc)
 #pragma unroll
       for (int u = 0; u < V; ++u) acc[cc][u] = 0.f;
 #pragma unroll
-    for (int s = 0; s < KR; ++s) {
-      if (s >= nr) break;
-      float v[CPL][V];
+    for (int s0 = 0; s0 < KR; s0 += RB) {
+      if (s0 >= nr) break;
+      u32x4_t raw[RB][WCPL];
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const int c = c0 + (cc * 64 + lane) * V;
-        if (c < d) load16_f32(rows + (size_t)p[s] * d + c, v[cc]);
+      for (int b = 0; b < RB; ++b) {
+        if (s0 + b >= nr) continue;
+#pragma unroll
+        for (int cc = 0; cc < WCPL; ++cc) {
+          const int c = c0 + (cc * 64 + lane) * V;
+          if (c < d) raw[b][cc] = *reinterpret_cast<const u32x4_t*>(rows + (size_t)p[s0 + b] * d + c);
+        }
       }
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc)
+      for (int b = 0; b < RB; ++b) {
+        if (s0 + b >= nr) continue;
 #pragma unroll
-        for (int u = 0; u < V; ++u) acc[cc][u] = fmaf(w[s], v[cc][u], acc[cc][u]);
+        for (int cc = 0; cc < WCPL; ++cc) {
+          float v[V];
+          unpack16_f32(raw[b][cc], v, rows);
+#pragma unroll
+          for (int u = 0; u < V; ++u) acc[cc][u] = fmaf(w[s0 + b], v[u], acc[cc][u]);
+        }
+      }
     }
     for (int j = j_rest; j < k; ++j) {
       const int q = slot_of(inv_perm, o, j, cap);
       if (q < 0) continue;
       const float wq = tw ? tw[o + j] : 1.f;
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
+      for (int cc = 0; cc < WCPL; ++cc) {
         const int c = c0 + (cc * 64 + lane) * V;
         if (c >= d) continue;
         float v[V];
@@ -271,12 +319,12 @@ DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const f
       }
     }
 #pragma unroll
-    for (int cc = 0; cc < CPL; ++cc) {
+    for (int cc = 0; cc < WCPL; ++cc) {
       const int c = c0 + (cc * 64 + lane) * V;
       if (c >= d) continue;
       if (add) {
         float v[V];
-        load16_f32(add + (size_t)t * d + c, v);
+        unpack16_f32(a_raw[cc], v, rows);
 #pragma unroll
         for (int u = 0; u < V; ++u) acc[cc][u] += v[u];
       }
