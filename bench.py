@@ -19,6 +19,12 @@ Prints ONE JSON line.  Besides the contract fields it carries:
   cpu_baseline  the CPU oracle on a bounded token sample of the same workload.
 
     python bench.py [--gpus 1] [--steps 64] [--warmup 10] [--workload 2]
+
+``--ghost-sweep`` instead measures the layer analogue of the paper's skip-token
+throughput experiment (Sec. 5, "Measured Skip-Token Throughput"): the mid-size
+layer (workload 1 shapes: T=4096, d=1024, E=16, top-2, H=2816, bf16) with 16,
+12, 8 and 4 resident experts, each with the unpartitioned router and
+skip-token and with the partitioned router, as one JSON line.
 """
 from __future__ import annotations
 
@@ -52,6 +58,8 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--ghost-sweep", action="store_true",
+                    help="tokens/s vs number of ghost experts, skip-token and partitioned router")
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="make one plain device-to-device copy of a known size before the "
                          "steps, the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
@@ -95,12 +103,76 @@ def algorithmic_work(cfg, n, t_act, s):
     return w
 
 
+def ghost_sweep(args):
+    """Step time of the mid-size layer at 16, 12, 8 and 4 resident experts of
+    16: skip-token (unpartitioned router, ghost routes skipped) and the
+    partitioned router (routes over the resident experts only, top-min(k, E_r),
+    nothing skipped).  Resident sets are spread evenly over the expert ids."""
+    import numpy as np
+    import torch
+
+    from paper_2606_19025_amd import inputs as I
+    from paper_2606_19025_amd.layer import ResidentMoELayer
+
+    wl = 1
+    base = I.workload(wl, args.seed)
+    E = base["E"]
+    rows = []
+    for Er in (16, 12, 8, 4):
+        resident = sorted({i * E // Er for i in range(Er)})
+        inp = I.make_layer_inputs(wl, seed=args.seed, resident=resident)
+        cfg = inp["cfg"]
+        T, d, k, H = cfg["T"], cfg["d"], cfg["k"], cfg["H"]
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda().to(torch.bfloat16)
+        x, dy, wgu, wd = (dev(inp[n]) for n in ("x", "dy", "w_gate_up", "w_down"))
+        for mode in ("skip-token", "partitioned"):
+            part = mode == "partitioned"
+            wr = dev(inp["w_router"][np.flatnonzero(inp["resident"])] if part else inp["w_router"])
+            L = ResidentMoELayer(T, d, E, k, H, inp["resident"], dtype=torch.bfloat16,
+                                 partitioned=part)
+
+            def step():
+                L.forward(x, wr, wgu, wd)
+                L.backward(dy, x, wr, wgu, wd)
+
+            for _ in range(args.warmup):
+                step()
+            torch.cuda.synchronize()
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ev0.record()
+            for _ in range(args.steps):
+                step()
+            ev1.record()
+            torch.cuda.synchronize()
+            ms = ev0.elapsed_time(ev1) / args.steps
+            n = int(L.offsets[-1].item())
+            rows.append(dict(E_resident=Er, ghost_experts=E - Er, mode=mode, ms_per_step=round(ms, 4),
+                             tokens_per_s=round(T / (ms / 1e3), 1), executed_routes=n))
+            log(f"[sweep] E_r={Er:2d} {mode:11s} {ms:.3f} ms/step n={n}")
+            del L
+    full = {r["mode"]: r["tokens_per_s"] for r in rows if r["ghost_experts"] == 0}
+    for r in rows:
+        r["speedup_vs_no_ghosts"] = round(r["tokens_per_s"] / full[r["mode"]], 3)
+    out = {"metric": "MoE layer fwd+bwd tokens/s vs ghost experts (1 GPU)", "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+           "data": "synthetic (seeded, shapes of the workload)",
+           "config": {"workload": base["name"], "T": base["T"], "d": base["d"], "E": E,
+                      "k": base["k"], "H": base["H"]},
+           "sweep": rows}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               "multi-GPU path", file=sys.stderr)
         sys.exit(2)
+    if args.ghost_sweep:
+        from paper_2606_19025_amd import binding as B
+        B.lib()
+        ghost_sweep(args)
+        return
     import numpy as np
     import torch
 

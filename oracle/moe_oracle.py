@@ -20,6 +20,9 @@ What it computes (arxiv 2606.19025):
   routes are NOT renormalised over the surviving routes (App. B.3: the
   unavailability of an expert must not skew the distribution over the
   remaining ones).
+* Partitioned router (the paper's default mode; Sec. 3.3 opening paragraph,
+  App. D "Router Efficiency"): partition_router() restates a step as the same
+  layer over the resident experts alone, with top-min(k, N_le) routing.
 * The worker holds a resident subset S_m of the experts (Sec. 3.3.1/3.3.2 and
   Alg. 1); routing is strictly local (Sec. 3.3.2 "System context and routing
   logic"), so the dispatch groups routes only by resident expert.
@@ -397,6 +400,36 @@ def layer_bwd(inp, fwd, dy, inv_tau=1.0, gate="softmax_topk"):
     return dict(dYp=cb["dYp"], dw=cb["dw"], dXp=gb["dXp"], dG=gb["dG"], dU=gb["dU"],
                 dW_gate_up=gb["dW_gate_up"], dW_down=gb["dW_down"], shared=sb,
                 dz=rb["dz"], dW_router=rb["dW_router"], d_bias=rb["d_bias"], dx=dx)
+
+
+# --------------------------------------------------------------------------
+# Partitioned router (the paper's default mode, compared with skip-token)
+# --------------------------------------------------------------------------
+
+def partition_router(inp):
+    """The same local step with the router partitioned along with the experts.
+
+    Sec. 3.3 ("Ghost Experts and Skip-Token", opening paragraph): in most of
+    the paper's runs the router is partitioned with the experts, so a token is
+    never routed to an expert the worker does not hold; App. D ("Router
+    Efficiency"): the router then projects onto the N_le resident experts only;
+    Sec. 3.3.1: each token takes min(k, N_le) local routes.  The partitioned
+    step is therefore this layer over the resident experts alone: router rows
+    W_r[S_m] (and bias entries b[S_m]), every expert resident, top-min(k, N_le).
+    Expert ids in its results are local ids (rank in S_m).
+    """
+    res = np.flatnonzero(np.asarray(inp["resident"]))
+    if len(res) == 0:
+        raise ValueError("a partitioned router needs at least one resident expert")
+    cfg = dict(inp["cfg"])
+    out = dict(inp)
+    out["w_router"] = np.asarray(inp["w_router"])[res]
+    if inp.get("router_bias") is not None:
+        out["router_bias"] = np.asarray(inp["router_bias"])[res]
+    out["resident"] = np.ones(len(res), dtype=np.uint8)
+    cfg.update(E=len(res), E_r=len(res), k=min(cfg["k"], len(res)), resident=list(range(len(res))))
+    out["cfg"] = cfg
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -85,10 +85,14 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
     return r.view(np.float32)
 
 
-def workload(wl: int, seed: int = 42) -> dict:
-    """Shape description of workload ``wl`` with its resident set resolved."""
+def workload(wl: int, seed: int = 42, resident=None) -> dict:
+    """Shape description of workload ``wl`` with its resident set resolved
+    (``resident`` replaces the workload's own set, e.g. for a sweep over the
+    number of ghost experts)."""
     cfg = dict(WORKLOADS[wl])
     cfg["id"] = wl
+    if resident is not None:
+        cfg["resident"] = sorted(int(e) for e in resident)
     if cfg["resident"] is None:
         r = rng_for(seed, wl, "resident")
         cfg["resident"] = sorted(int(e) for e in r.choice(cfg["E"], cfg["E"] // 2, replace=False))
@@ -122,7 +126,7 @@ def zipf_logit_bias(cfg: dict, beta: float) -> np.ndarray:
 
 def make_layer_inputs(wl: int, seed: int = 42, T: int | None = None,
                       zipf_beta: float | None = None, ghost_weights: bool = False,
-                      with_experts: bool = True) -> dict:
+                      with_experts: bool = True, resident=None) -> dict:
     """All inputs of one layer step as float32 numpy arrays (bf16-valued for bf16 workloads).
 
     Expert weights are held only for the resident experts, in the layouts the
@@ -130,9 +134,10 @@ def make_layer_inputs(wl: int, seed: int = 42, T: int | None = None,
     w_down [E_r, d, H].  The shared experts are merged along the hidden
     dimension into one expert of hidden n_shared*Hs.  ``T`` truncates the
     token dimension (the first T tokens of the full draw); ``with_experts``
-    False skips drawing the expert weights (routing-only uses).
+    False skips drawing the expert weights (routing-only uses); ``resident``
+    replaces the workload's resident set.
     """
-    cfg = workload(wl, seed)
+    cfg = workload(wl, seed, resident)
     Tf, d, E, H, Er = cfg["T"], cfg["d"], cfg["E"], cfg["H"], cfg["E_r"]
     T = Tf if T is None else int(T)
     rnd = bf16_round if cfg["dtype"] == "bf16" else (lambda a: np.ascontiguousarray(a, np.float32))

@@ -8,6 +8,12 @@ Forward:  moe_route_mask -> moe_dispatch -> moe_grouped_ffn_fwd_sets (resident
 Backward: moe_combine_bwd -> moe_grouped_ffn_bwd_sets (resident [+ shared,
           writing dx]) -> moe_dispatch_bwd -> moe_route_bwd (adds the router's dx)
 Round boundary: moe_expert_delta over the fp32 master copies.
+
+With ``partitioned=True`` the router is partitioned along with the experts
+(the paper's default mode, Sec. 3.3; App. D "Router Efficiency"): it holds
+only the resident experts' rows ``w_router[E_r, d]``, every token takes
+min(k, E_r) routes, all local, and expert ids are local ids.  The same entry
+points run with E := E_r and every expert resident.
 """
 from __future__ import annotations
 
@@ -18,11 +24,19 @@ from . import binding as B
 
 class ResidentMoELayer:
     def __init__(self, T, d, E, k, H, resident, dtype=torch.bfloat16, n_shared_hidden=0,
-                 gate="softmax_topk", inv_tau=1.0, device="cuda"):
+                 gate="softmax_topk", inv_tau=1.0, device="cuda", partitioned=False):
         self.T, self.d, self.E, self.k, self.H = int(T), int(d), int(E), int(k), int(H)
         res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
         assert res.numel() == self.E
         self.E_r = int(res.sum().item())
+        self.partitioned = bool(partitioned)
+        if self.partitioned:
+            if self.E_r == 0:
+                raise ValueError("a partitioned router needs at least one resident expert")
+            # route over the resident experts only: E := E_r, all resident
+            self.E = self.E_r
+            self.k = min(self.k, self.E_r)
+            res = torch.ones(self.E_r, dtype=torch.uint8)
         self.cap = self.T * min(self.k, self.E_r)
         self.dtype = dtype
         self.dt = B.MOE_BF16 if dtype == torch.bfloat16 else B.MOE_F32

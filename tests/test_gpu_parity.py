@@ -81,6 +81,37 @@ def test_layer_parity_edge_cases(gpu_lib, name):
         assert np.all(g["dz"] == 0) and np.all(g["dw"] == 0)
 
 
+PARTITIONED = {
+    # name: inputs (the skip-token problem the partitioned layer is built from)
+    "workload-0-f32": lambda: I.make_layer_inputs(0),
+    "workload-1-bf16": lambda: I.make_layer_inputs(1),
+    "fine-grained-shared-T1024": lambda: I.make_layer_inputs(2, T=1024),
+    "one-resident-k2": lambda: synth_inputs(300, 64, 6, 2, 64, [4], "bf16", seed=3, bias=True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PARTITIONED))
+def test_partitioned_router_parity(gpu_lib, name):
+    """The layer with a partitioned router (routes over the resident experts
+    only) against the oracle's partitioned restatement of the same step."""
+    from paper_2606_19025_amd.layer import ResidentMoELayer
+    from .parity_helpers import torch_dtype
+    say(f"[partitioned] {name}")
+    inp = PARTITIONED[name]()
+    part = O.partition_router(inp)
+    cfg = inp["cfg"]
+    hs = cfg.get("n_shared", 0) * cfg.get("Hs", 0) if inp.get("shared_gate_up") is not None else 0
+    L = ResidentMoELayer(inp["x"].shape[0], cfg["d"], cfg["E"], cfg["k"], cfg["H"], inp["resident"],
+                         dtype=torch_dtype(cfg), n_shared_hidden=hs, partitioned=True)
+    assert (L.E, L.k) == (part["cfg"]["E"], part["cfg"]["k"])
+    L, _ = run_gpu_layer(part, layer=L)
+    g = gpu_outputs(L)
+    errs = check_layer_against_oracle(part, g)
+    assert np.all(g["local"] >= 0), "a partitioned router has no ghost routes"
+    assert g["n"] == inp["x"].shape[0] * part["cfg"]["k"]
+    say(f"[partitioned] {name} n={g['n']} errs={ {k: (round(v, 8) if isinstance(v, float) else v) for k, v in errs.items()} }")
+
+
 def test_topk_ties_go_to_lower_expert_id(gpu_lib):
     # one-hot tokens and repeated router columns give exactly equal logits
     T, d, E, k = 64, 64, 8, 3

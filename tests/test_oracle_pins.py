@@ -363,3 +363,80 @@ def test_expert_delta_within_fp32_bound_of_exact_mean():
     exact = ((s.astype(np.float64) - now) + sum(p.astype(np.float64) for p in peers)) / 4
     mag = (np.abs(s.astype(np.float64) - now) + sum(np.abs(p.astype(np.float64)) for p in peers)) / 4
     assert np.all(np.abs(avg - exact) <= 6 * np.finfo(np.float32).eps * (mag + 1e-30))
+
+
+# ---------------------------------------------------------------- partitioned router
+
+@pytest.mark.parametrize("k,resident", [(2, (1, 2, 4)), (4, (0, 5)), (2, (3,))])
+def test_partitioned_router_brute_force(k, resident):
+    """Partitioned mode: a token's routes are the top-min(k, N_le) of its logits
+    over the resident experts alone (per-token brute-force sort of plain dot
+    products), all routes are local, every token executes exactly min(k, N_le)
+    of them, and the gates are the softmax over the selected resident logits."""
+    T, d = 20, 7
+    inp = tiny_inputs(T=T, d=d, E=6, k=k, H=5, resident=resident, seed=21, bias=True)
+    f = O.layer_fwd(O.partition_router(inp))
+    res = sorted(resident)
+    kk = min(k, len(res))
+    for t in range(T):
+        z = [sum(inp["x"][t, c] * inp["w_router"][e, c] for c in range(d)) + inp["router_bias"][e]
+             for e in res]
+        brute = sorted(range(len(res)), key=lambda i: (-z[i], i))[:kk]
+        assert list(f["idx"][t]) == brute
+        assert list(f["local"][t]) == brute
+        zs = np.array([z[i] for i in brute])
+        wref = np.exp(zs - zs.max())
+        wref /= wref.sum()
+        assert np.allclose(f["w"][t], wref, rtol=1e-12, atol=0)
+    assert int(f["offsets"][-1]) == T * kk
+
+
+def test_partitioned_router_with_every_expert_resident_is_skip_token():
+    inp = tiny_inputs(T=16, d=6, E=5, k=2, H=4, resident=(0, 1, 2, 3, 4), seed=22, shared=3,
+                      bias=True)
+    a = O.layer_fwd(inp)
+    b = O.layer_fwd(O.partition_router(inp))
+    for key in ("idx", "w", "local", "perm", "inv_perm", "offsets"):
+        assert np.array_equal(a[key], b[key]), key
+    assert np.array_equal(a["y"], b["y"])
+
+
+def test_partitioned_router_single_resident_expert_is_dense_swiglu():
+    """N_le = 1 < k: every token takes its one local route with weight 1, so
+    the routed output is the dense SwiGLU of that expert (checked against
+    torch.nn.functional in fp64)."""
+    torch = pytest.importorskip("torch")
+    inp = tiny_inputs(T=12, d=6, E=4, k=2, H=5, resident=(2,), seed=23)
+    f = O.layer_fwd(O.partition_router(inp))
+    assert np.all(f["w"] == 1.0) and f["w"].shape == (12, 1)
+    x = torch.from_numpy(inp["x"])
+    wg = torch.from_numpy(inp["w_gate_up"][0, :5])
+    wu = torch.from_numpy(inp["w_gate_up"][0, 5:])
+    wd = torch.from_numpy(inp["w_down"][0])
+    ref = (torch.nn.functional.silu(x @ wg.T) * (x @ wu.T)) @ wd.T
+    assert np.allclose(f["y"], ref.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_partitioned_router_backward_matches_central_differences():
+    inp = tiny_inputs(T=9, d=5, E=6, k=2, H=4, resident=(0, 3, 4, 5), seed=24, bias=True)
+    part = O.partition_router(inp)
+    g = np.random.default_rng(25)
+    dy = g.standard_normal((9, 5))
+    fwd = O.layer_fwd(part)
+    bwd = O.layer_bwd(part, fwd, dy)
+    zs = np.sort(fwd["logits"], axis=1)[:, ::-1]
+    assert np.min(zs[:, 1] - zs[:, 2]) > 1e-4
+    assert bwd["dW_router"].shape == (4, 5)
+    for name, grad in [("x", bwd["dx"]), ("w_router", bwd["dW_router"]),
+                       ("router_bias", bwd["d_bias"]), ("w_gate_up", bwd["dW_gate_up"])]:
+        flat = part[name].reshape(-1)
+        for i in g.choice(flat.size, size=min(20, flat.size), replace=False):
+            h = 1e-6 * max(1.0, abs(flat[i]))
+            old = flat[i]
+            flat[i] = old + h
+            lp = _loss(part, dy, "softmax_topk", 1.0, fwd["idx"])
+            flat[i] = old - h
+            lm = _loss(part, dy, "softmax_topk", 1.0, fwd["idx"])
+            flat[i] = old
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - grad.reshape(-1)[i]) <= 1e-6 * max(1.0, abs(fd)), (name, i)
