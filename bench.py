@@ -21,7 +21,7 @@ Prints ONE JSON line.  Besides the contract fields it carries:
     python bench.py [--gpus 1] [--steps 64] [--warmup 10] [--workload 2]
 
 ``--ghost-sweep`` instead measures the layer analogue of the paper's skip-token
-throughput experiment (Sec. 5, "Measured Skip-Token Throughput"): the mid-size
+throughput experiment (Sec. 6.4, "Measured Skip-Token Throughput"): the mid-size
 layer (workload 1 shapes: T=4096, d=1024, E=16, top-2, H=2816, bf16) with 16,
 12, 8 and 4 resident experts, each with the unpartitioned router and
 skip-token and with the partitioned router, as one JSON line.

@@ -453,3 +453,71 @@ def expert_delta(theta_start, theta_now, peers):
         acc = (acc + np.asarray(p, dtype=f32)).astype(f32)
     scale = f32(1.0) / f32(len(peers) + 1)
     return dl, (acc * scale).astype(f32)
+
+
+# --------------------------------------------------------------------------
+# Optimisers of the resident experts (local steps and round boundary)
+# --------------------------------------------------------------------------
+#
+# Sec. 3.4 ("Outer optimization"): workers run AdamW locally on their own
+# parameters and keep the optimiser state across rounds, only for their own
+# experts; the aggregated model is updated by a momentum outer optimiser.
+# App. F (reproducibility details): AdamW with weight decay 0, betas (0.9, 0.95),
+# eps 1e-8; the DiLoCo/Nesterov outer step uses learning rate 0.7 and
+# momentum 0.9; LocalAdamW also averages the first and second moments.
+# All of it is fp32 elementwise arithmetic, written here one rounding at a
+# time in a fixed order, so that an fp32 implementation performing the same
+# operations (correctly rounded division and square root, no fused
+# multiply-add) reproduces it bit for bit.
+
+def adamw_bias_corrections(step, beta1, beta2):
+    """fp32 (1 - beta1^t, 1 - beta2^t) for step t >= 1 (evaluated in fp64)."""
+    f32 = np.float32
+    return f32(1.0 - float(beta1) ** int(step)), f32(1.0 - float(beta2) ** int(step))
+
+
+def adamw_step(theta, grad, m, v, step, lr, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0):
+    """One AdamW step (decoupled weight decay, Loshchilov & Hutter) in fp32.
+
+      m' = b1 m + (1 - b1) g;  v' = b2 v + (1 - b2) g^2
+      theta' = theta - lr ((m' / c1) / (sqrt(v' / c2) + eps) + wd theta)
+    with c1, c2 the bias corrections of step t.  Returns (theta', m', v').
+    """
+    f32 = np.float32
+    th, g = np.asarray(theta, f32), np.asarray(grad, f32)
+    m0, v0 = np.asarray(m, f32), np.asarray(v, f32)
+    b1, b2, ep, wd, lr_ = f32(beta1), f32(beta2), f32(eps), f32(weight_decay), f32(lr)
+    c1, c2 = adamw_bias_corrections(step, beta1, beta2)
+    m1 = (b1 * m0).astype(f32) + ((f32(1) - b1) * g).astype(f32)
+    v1 = (b2 * v0).astype(f32) + ((f32(1) - b2) * (g * g).astype(f32)).astype(f32)
+    mh = (m1 / c1).astype(f32)
+    vh = (v1 / c2).astype(f32)
+    den = (np.sqrt(vh).astype(f32) + ep).astype(f32)
+    upd = ((mh / den).astype(f32) + (wd * th).astype(f32)).astype(f32)
+    th1 = (th - (lr_ * upd).astype(f32)).astype(f32)
+    return th1, m1.astype(f32), v1.astype(f32)
+
+
+def outer_nesterov(theta_start, delta_avg, momentum, lr=0.7, mu=0.9):
+    """Outer step on the replica-group average of the pseudo-gradient (Alg. 2,
+    OuterOpt; DiLoCo's Nesterov momentum), in fp32:
+
+      b' = mu b + delta;  theta' = theta_start - lr (delta + mu b')
+    Returns (theta', b').  theta' is where every worker starts the next round.
+    """
+    f32 = np.float32
+    th, dl, b = (np.asarray(a, f32) for a in (theta_start, delta_avg, momentum))
+    mu_, lr_ = f32(mu), f32(lr)
+    b1 = ((mu_ * b).astype(f32) + dl).astype(f32)
+    upd = (dl + (mu_ * b1).astype(f32)).astype(f32)
+    return (th - (lr_ * upd).astype(f32)).astype(f32), b1
+
+
+def replica_mean(local, peers):
+    """Average of a tensor over the expert's replica group (LocalAdamW moment
+    sync): (((x + p_1) + p_2) + ...) * fp32(1 / (n_peers + 1)) in fp32."""
+    f32 = np.float32
+    acc = np.asarray(local, f32).copy()
+    for p in peers:
+        acc = (acc + np.asarray(p, f32)).astype(f32)
+    return (acc * (f32(1.0) / f32(len(peers) + 1))).astype(f32)

@@ -22,6 +22,13 @@ FAST_PINS = [
     lambda: P.test_backward_matches_central_differences("sigmoid"),
     P.test_backward_matches_torch_autograd_dense_formulation, P.test_backward_is_linear_in_dy,
     P.test_expert_delta_closed_forms, P.test_expert_delta_within_fp32_bound_of_exact_mean,
+    lambda: P.test_partitioned_router_brute_force(2, (1, 2, 4)),
+    lambda: P.test_partitioned_router_brute_force(2, (3,)),
+    P.test_partitioned_router_single_resident_expert_is_dense_swiglu,
+    lambda: P.test_adamw_matches_torch_optim_adamw(0.0),
+    lambda: P.test_adamw_matches_torch_optim_adamw(0.1),
+    P.test_adamw_first_step_is_a_sign_step, P.test_outer_nesterov_matches_torch_sgd_nesterov,
+    P.test_outer_nesterov_zero_delta_is_identity, P.test_replica_mean_closed_forms,
 ]
 
 _orig = {name: getattr(O, name) for name in dir(O) if callable(getattr(O, name))}
@@ -99,7 +106,39 @@ def _softmax_topk_full_denominator(z, idx, gate="softmax_topk"):
     return _orig["gate_weights"](z, idx, gate)
 
 
+def _partition_keeps_all_router_rows(inp):
+    out = _orig["partition_router"](inp)
+    out["w_router"] = np.asarray(inp["w_router"])[:out["cfg"]["E"]]
+    return out
+
+
+def _adamw_weight_decay_sign(theta, grad, m, v, step, lr, beta1=0.9, beta2=0.95, eps=1e-8,
+                             weight_decay=0.0):
+    return _orig["adamw_step"](theta, grad, m, v, step, lr, beta1, beta2, eps, -weight_decay)
+
+
+def _nesterov_old_buffer(theta_start, delta_avg, momentum, lr=0.7, mu=0.9):
+    f32 = np.float32
+    th, dl, b = (np.asarray(a, f32) for a in (theta_start, delta_avg, momentum))
+    b1 = (f32(mu) * b + dl).astype(f32)
+    return (th - f32(lr) * (dl + f32(mu) * b)).astype(f32), b1
+
+
+def _replica_mean_over_peers_only(local, peers):
+    f32 = np.float32
+    acc = np.asarray(local, f32).copy()
+    for p in peers:
+        acc = (acc + np.asarray(p, f32)).astype(f32)
+    return (acc * (f32(1.0) / f32(max(len(peers), 1)))).astype(f32)
+
+
 MUTANTS = {
+    "partitioned router keeps the first rows, not the resident ones":
+        ("partition_router", _partition_keeps_all_router_rows),
+    "AdamW without bias correction": ("adamw_bias_corrections", lambda *a: (np.float32(1), np.float32(1))),
+    "AdamW weight decay with the wrong sign": ("adamw_step", _adamw_weight_decay_sign),
+    "Nesterov look-ahead uses the old momentum": ("outer_nesterov", _nesterov_old_buffer),
+    "replica mean divides by the peer count": ("replica_mean", _replica_mean_over_peers_only),
     "topk ties to the higher id": ("topk_select", _topk_ties_high),
     "combine renormalises over surviving routes": ("combine_fwd", _combine_renorm),
     "dG drops the up factor": ("swiglu_bwd", lambda *a: _bwd_variant(*a, drop_u=True)),

@@ -440,3 +440,88 @@ def test_partitioned_router_backward_matches_central_differences():
             flat[i] = old
             fd = (lp - lm) / (2 * h)
             assert abs(fd - grad.reshape(-1)[i]) <= 1e-6 * max(1.0, abs(fd)), (name, i)
+
+
+# ---------------------------------------------------------------- optimisers
+
+@pytest.mark.parametrize("wd", [0.0, 0.1])
+def test_adamw_matches_torch_optim_adamw(wd):
+    """Three AdamW steps against torch.optim.AdamW on the CPU (fp32); the two
+    order their fp32 operations differently, so they agree to a few ulps."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(31)
+    n = 4096
+    theta = (g.standard_normal(n) * 0.02).astype(np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(theta.copy()))
+    opt = torch.optim.AdamW([p], lr=0.01, betas=(0.9, 0.95), eps=1e-8, weight_decay=wd)
+    m = np.zeros(n, np.float32)
+    v = np.zeros(n, np.float32)
+    th = theta.copy()
+    for t in range(1, 4):
+        grad = (g.standard_normal(n) * 0.1).astype(np.float32)
+        p.grad = torch.from_numpy(grad.copy())
+        opt.step()
+        th, m, v = O.adamw_step(th, grad, m, v, t, 0.01, 0.9, 0.95, 1e-8, wd)
+        ref = p.detach().numpy()
+        assert np.max(np.abs(th - ref)) <= 4e-7 * np.max(np.abs(ref)), t
+        st = opt.state[p]
+        # torch updates m by lerp, v by mul + addcmul: a few ulps apart
+        # (normwise: single entries may cancel to near zero)
+        for mine, theirs in ((m, st["exp_avg"].numpy()), (v, st["exp_avg_sq"].numpy())):
+            assert np.max(np.abs(mine - theirs)) <= 1e-6 * np.max(np.abs(theirs))
+
+
+def test_adamw_first_step_is_a_sign_step():
+    """From zero moments, step 1 gives m/c1 = g and v/c2 = g^2 (up to
+    rounding), so the update is lr * g / (|g| + eps), i.e. lr * sign(g)."""
+    g = np.random.default_rng(32)
+    theta = g.standard_normal(1000).astype(np.float32)
+    grad = (g.standard_normal(1000) + np.sign(g.standard_normal(1000)) * 0.5).astype(np.float32)
+    z = np.zeros(1000, np.float32)
+    th, m, v = O.adamw_step(theta, grad, z, z, 1, 1e-3)
+    # exact difference in fp64; theta' carries one rounding of |theta| ~ 1
+    step = theta.astype(np.float64) - th.astype(np.float64)
+    assert np.allclose(step, 1e-3 * np.sign(grad), rtol=1e-5, atol=2.5e-7)
+    assert np.allclose(m, 0.1 * grad, rtol=1e-6) and np.allclose(v, 0.05 * grad * grad, rtol=1e-6)
+
+
+def test_outer_nesterov_matches_torch_sgd_nesterov():
+    """The outer step equals torch.optim.SGD(momentum=0.9, nesterov=True,
+    lr=0.7) applied to the averaged pseudo-gradient, round after round."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(33)
+    n = 2048
+    theta = (g.standard_normal(n) * 0.02).astype(np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(theta.copy()))
+    opt = torch.optim.SGD([p], lr=0.7, momentum=0.9, nesterov=True)
+    b = np.zeros(n, np.float32)
+    th = theta.copy()
+    for _ in range(3):
+        delta = (g.standard_normal(n) * 1e-3).astype(np.float32)
+        p.grad = torch.from_numpy(delta.copy())
+        opt.step()
+        th, b = O.outer_nesterov(th, delta, b, 0.7, 0.9)
+        ref = p.detach().numpy()
+        assert np.max(np.abs(th - ref)) <= 2e-7 * np.max(np.abs(ref))
+        assert np.allclose(b, opt.state[p]["momentum_buffer"].numpy(), rtol=1e-6, atol=1e-12)
+
+
+def test_outer_nesterov_zero_delta_is_identity():
+    th = np.random.default_rng(34).standard_normal(100).astype(np.float32)
+    z = np.zeros(100, np.float32)
+    th1, b1 = O.outer_nesterov(th, z, z)
+    assert np.array_equal(th1, th) and np.array_equal(b1, z)
+
+
+def test_replica_mean_closed_forms():
+    g = np.random.default_rng(35)
+    x = g.standard_normal(999).astype(np.float32)
+    # identical copies over a power-of-two group: the mean is the copy, exactly
+    assert np.array_equal(O.replica_mean(x, [x, x, x]), x)
+    assert np.array_equal(O.replica_mean(x, [x]), x)
+    # any copies: within the fp32 bound of the exact mean
+    peers = [g.standard_normal(999).astype(np.float32) for _ in range(3)]
+    exact = (x.astype(np.float64) + sum(p.astype(np.float64) for p in peers)) / 4
+    got = O.replica_mean(x, peers)
+    bound = 4 * 2.0 ** -24 * (np.abs(x) + sum(np.abs(p) for p in peers)).astype(np.float64)
+    assert np.all(np.abs(got - exact) <= bound)
