@@ -255,6 +255,54 @@ int moe_expert_delta(const float* theta_start, const float* theta_now,
                      float* delta_local, float* delta_avg, hipStream_t stream);
 
 /*
+ * Optimisers of the resident experts' fp32 master parameters (Sec. 3.4
+ * "Outer optimization": AdamW on the worker's own parameters during the local
+ * steps, with the state kept across rounds and only for its own experts; a
+ * momentum outer step on the replica-group average at the round boundary;
+ * App. F: AdamW weight decay 0, betas (0.9, 0.95), eps 1e-8, Nesterov outer
+ * step with learning rate 0.7 and momentum 0.9, LocalAdamW averaging of the
+ * moments).  All arrays are device fp32 [n] (theta_bf16: bf16 [n]), 16-byte
+ * aligned, owned by the caller, updated in place.  Each element is computed
+ * in fp32 one rounding at a time in the order written below (no fused
+ * multiply-add; correctly rounded division and square root), so results are
+ * reproducible bit for bit.  theta_bf16 (may be NULL) receives the updated
+ * parameters rounded to bf16 (nearest even): the working copy the bf16
+ * grouped GEMMs read (w_gate_up / w_down share the fp32 masters' layout).
+ * Returns MOE_ERR_ARG for NULL required arrays or bad hyper-parameters,
+ * MOE_ERR_UNSUPPORTED for misaligned arrays.
+ *
+ * moe_adamw_step, step t >= 1 (c1 = 1 - beta1^t, c2 = 1 - beta2^t, evaluated
+ * in double and rounded to fp32):
+ *   m = beta1 m + (1 - beta1) g;   v = beta2 v + (1 - beta2) (g g)
+ *   theta = theta - lr ((m / c1) / (sqrt(v / c2) + eps) + weight_decay theta)
+ */
+int moe_adamw_step(float* theta, const float* grad, float* m, float* v, size_t n, int step,
+                   float lr, float beta1, float beta2, float eps, float weight_decay,
+                   void* theta_bf16, hipStream_t stream);
+
+/*
+ * moe_outer_nesterov: the outer step of a round on the replica-group average
+ * delta_avg (from moe_expert_delta) with momentum buffer b (zero before the
+ * first round):
+ *   b = mu b + delta_avg;   theta = theta_start - lr (delta_avg + mu b)
+ * and theta is written to theta_start and theta_now (where every replica
+ * starts the next round) and, if non-NULL, to theta_bf16.
+ */
+int moe_outer_nesterov(float* theta_start, float* theta_now, const float* delta_avg,
+                       float* momentum, size_t n, float lr, float mu, void* theta_bf16,
+                       hipStream_t stream);
+
+/*
+ * moe_replica_mean: the replica-group average of a tensor (LocalAdamW's
+ * moment synchronisation):
+ *   out = (((local + peers[0]) + peers[1]) + ...) * fp32(1 / (n_peers + 1))
+ * peers is a HOST array of n_peers device pointers; 0 <= n_peers <= 16; out
+ * may alias local.
+ */
+int moe_replica_mean(const float* local, const float* const* peers, int n_peers, size_t n,
+                     float* out, hipStream_t stream);
+
+/*
  * Measurement support for benchmarks and profilers (not part of the layer).
  * moe_timing_enable(capacity > 0) creates a pool of 2*capacity HIP events on
  * the current device and from then on brackets every kernel this library

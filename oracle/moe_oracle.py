@@ -471,9 +471,12 @@ def expert_delta(theta_start, theta_now, peers):
 # multiply-add) reproduces it bit for bit.
 
 def adamw_bias_corrections(step, beta1, beta2):
-    """fp32 (1 - beta1^t, 1 - beta2^t) for step t >= 1 (evaluated in fp64)."""
+    """fp32 (1 - beta1^t, 1 - beta2^t) for step t >= 1: the betas are fp32
+    hyper-parameters like every other operand here, the power is evaluated
+    in fp64 from their fp32 values and the result rounded to fp32."""
     f32 = np.float32
-    return f32(1.0 - float(beta1) ** int(step)), f32(1.0 - float(beta2) ** int(step))
+    b1, b2 = float(f32(beta1)), float(f32(beta2))
+    return f32(1.0 - b1 ** int(step)), f32(1.0 - b2 ** int(step))
 
 
 def adamw_step(theta, grad, m, v, step, lr, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0):

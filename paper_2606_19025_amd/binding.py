@@ -25,7 +25,8 @@ EXPORTS = [
     "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_grouped_ffn_fwd_sets",
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
-    "moe_expert_delta", "moe_timing_enable", "moe_timing_collect",
+    "moe_expert_delta", "moe_adamw_step", "moe_outer_nesterov", "moe_replica_mean",
+    "moe_timing_enable", "moe_timing_collect",
 ]
 
 
@@ -61,6 +62,9 @@ _SIGS = {
     "moe_combine_fwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_combine_bwd": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_expert_delta": (_I, [_P, _P, C.POINTER(C.c_void_p), _I, _Z, _P, _P, _P]),
+    "moe_adamw_step": (_I, [_P, _P, _P, _P, _Z, _I, _F, _F, _F, _F, _F, _P, _P]),
+    "moe_outer_nesterov": (_I, [_P, _P, _P, _P, _Z, _F, _F, _P, _P]),
+    "moe_replica_mean": (_I, [_P, C.POINTER(C.c_void_p), _I, _Z, _P, _P]),
     "moe_timing_enable": (_I, [_I]),
     "moe_timing_collect": (_I, [_P, _I, C.POINTER(C.c_int)]),
 }
@@ -235,6 +239,27 @@ def moe_expert_delta(theta_start, theta_now, peers, n_peers, n_params, delta_loc
     return _check("moe_expert_delta", lib().moe_expert_delta(
         _ptr(theta_start), _ptr(theta_now), arr, n_peers, n_params, _ptr(delta_local),
         _ptr(delta_avg), _stream(stream)))
+
+
+def moe_adamw_step(theta, grad, m, v, n, step, lr, beta1=0.9, beta2=0.95, eps=1e-8,
+                   weight_decay=0.0, theta_bf16=None, stream=None):
+    return _check("moe_adamw_step", lib().moe_adamw_step(
+        _ptr(theta), _ptr(grad), _ptr(m), _ptr(v), n, step, lr, beta1, beta2, eps, weight_decay,
+        _ptr(theta_bf16), _stream(stream)))
+
+
+def moe_outer_nesterov(theta_start, theta_now, delta_avg, momentum, n, lr=0.7, mu=0.9,
+                       theta_bf16=None, stream=None):
+    return _check("moe_outer_nesterov", lib().moe_outer_nesterov(
+        _ptr(theta_start), _ptr(theta_now), _ptr(delta_avg), _ptr(momentum), n, lr, mu,
+        _ptr(theta_bf16), _stream(stream)))
+
+
+def moe_replica_mean(local, peers, n_peers, n, out, stream=None):
+    arr = (C.c_void_p * max(1, n_peers))(*[_ptr(p) for p in (peers or [])][:n_peers]) \
+        if n_peers else None
+    return _check("moe_replica_mean", lib().moe_replica_mean(
+        _ptr(local), arr, n_peers, n, _ptr(out), _stream(stream)))
 
 
 def moe_timing_enable(capacity):

@@ -398,4 +398,51 @@ int moe_expert_delta(const float* theta_start, const float* theta_now,
                     "moe_expert_delta");
 }
 
+int moe_adamw_step(float* theta, const float* grad, float* m, float* v, size_t n, int step,
+                   float lr, float beta1, float beta2, float eps, float weight_decay,
+                   void* theta_bf16, hipStream_t stream) {
+  REQUIRE(n == 0 || (theta && grad && m && v), "theta, grad, m and v must not be NULL");
+  REQUIRE(step >= 1, "step = %d must be >= 1", step);
+  REQUIRE(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f && eps >= 0.f,
+          "betas must lie in [0, 1) and eps must be >= 0");
+  for (const void* p : {(const void*)theta, (const void*)grad, (const void*)m, (const void*)v,
+                        (const void*)theta_bf16})
+    SUPPORT(p == nullptr || aligned16(p), "arrays must be 16-byte aligned");
+  const float c1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+  const float c2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+  REQUIRE(c1 > 0.f && c2 > 0.f, "bias corrections must be positive (betas > 0 at step %d)", step);
+  return hip_status(moe::launch_adamw(theta, grad, m, v, n, lr, beta1, beta2, eps, weight_decay,
+                                      c1, c2, theta_bf16, stream),
+                    "moe_adamw_step");
+}
+
+int moe_outer_nesterov(float* theta_start, float* theta_now, const float* delta_avg,
+                       float* momentum, size_t n, float lr, float mu, void* theta_bf16,
+                       hipStream_t stream) {
+  REQUIRE(n == 0 || (theta_start && theta_now && delta_avg && momentum),
+          "theta_start, theta_now, delta_avg and momentum must not be NULL");
+  for (const void* p : {(const void*)theta_start, (const void*)theta_now,
+                        (const void*)delta_avg, (const void*)momentum, (const void*)theta_bf16})
+    SUPPORT(p == nullptr || aligned16(p), "arrays must be 16-byte aligned");
+  return hip_status(moe::launch_outer_nesterov(theta_start, theta_now, delta_avg, momentum, n, lr,
+                                               mu, theta_bf16, stream),
+                    "moe_outer_nesterov");
+}
+
+int moe_replica_mean(const float* local, const float* const* peers, int n_peers, size_t n,
+                     float* out, hipStream_t stream) {
+  REQUIRE(n_peers >= 0 && n_peers <= moe::kMaxPeers, "n_peers = %d must be in [0, %d]", n_peers,
+          moe::kMaxPeers);
+  REQUIRE(n == 0 || (local && out), "local and out must not be NULL");
+  REQUIRE(n_peers == 0 || peers, "peers must not be NULL when n_peers > 0");
+  for (int p = 0; p < n_peers; ++p) {
+    REQUIRE(n == 0 || peers[p], "peers[%d] must not be NULL", p);
+    SUPPORT(peers[p] == nullptr || aligned16(peers[p]), "peers[%d] must be 16-byte aligned", p);
+  }
+  SUPPORT((local == nullptr || aligned16(local)) && (out == nullptr || aligned16(out)),
+          "arrays must be 16-byte aligned");
+  return hip_status(moe::launch_replica_mean(local, peers, n_peers, n, out, stream),
+                    "moe_replica_mean");
+}
+
 }  // extern "C"

@@ -50,4 +50,13 @@ constexpr int kMaxPeers = 16;
 hipError_t launch_expert_delta(const float* start, const float* now, const float* const* peers,
                                int n_peers, size_t n, float* dl, float* avg, hipStream_t s);
 
+// Optimisers (optim.hip); c1, c2 = the step's AdamW bias corrections.
+hipError_t launch_adamw(float* theta, const float* grad, float* m, float* v, size_t n, float lr,
+                        float beta1, float beta2, float eps, float wd, float c1, float c2,
+                        void* theta_bf16, hipStream_t s);
+hipError_t launch_outer_nesterov(float* start, float* now, const float* delta, float* mom,
+                                 size_t n, float lr, float mu, void* theta_bf16, hipStream_t s);
+hipError_t launch_replica_mean(const float* local, const float* const* peers, int n_peers,
+                               size_t n, float* out, hipStream_t s);
+
 }  // namespace moe

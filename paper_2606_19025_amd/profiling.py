@@ -53,12 +53,16 @@ _SYMBOLS = [
     (r"unpermute_kernel", lambda m: "unpermute"),
     (r"expert_delta_kernel", lambda m: "expert_delta"),
     (r"splitk_reduce_kernel", lambda m: "splitk_reduce"),
+    (r"adamw_kernel", lambda m: "adamw_step"),
+    (r"outer_nesterov_kernel", lambda m: "outer_nesterov"),
+    (r"replica_mean_kernel", lambda m: "replica_mean"),
 ]
 
 # timing name prefix -> source file that holds the kernel
 _SOURCES = [("gemm_", "gemm.hip"), ("splitk_", "gemm.hip"), ("route_", "route.hip"), ("dispatch_", "dispatch.hip"),
             ("combine_", "dispatch.hip"), ("unpermute", "dispatch.hip"),
-            ("expert_delta", "dispatch.hip")]
+            ("expert_delta", "dispatch.hip"), ("adamw", "optim.hip"), ("outer_", "optim.hip"),
+            ("replica_", "optim.hip")]
 
 
 def timing_name(symbol: str) -> str | None:

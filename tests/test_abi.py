@@ -145,3 +145,24 @@ def test_ffn_sets_reject_bad_arguments(lib):
     assert "workspace" in B.moe_last_error()
     assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 2048, 0,
                                             4096 + 16, need, None) == ERR_UNSUPPORTED
+
+
+def test_optimiser_entry_points_reject_bad_arguments(lib):
+    p = 256
+    # AdamW: NULL arrays, step 0, betas out of range, misalignment
+    assert call_status(lib.moe_adamw_step, None, p, p, p, 10, 1, 0.01, 0.9, 0.95, 1e-8, 0.0,
+                       None) == ERR_ARG
+    assert call_status(lib.moe_adamw_step, p, p, p, p, 10, 0, 0.01, 0.9, 0.95, 1e-8, 0.0,
+                       None) == ERR_ARG
+    assert call_status(lib.moe_adamw_step, p, p, p, p, 10, 1, 0.01, 1.0, 0.95, 1e-8, 0.0,
+                       None) == ERR_ARG
+    assert call_status(lib.moe_adamw_step, p, p, p, p + 4, 10, 1, 0.01, 0.9, 0.95, 1e-8, 0.0,
+                       None) == ERR_UNSUPPORTED
+    # outer step: NULL momentum, misaligned bf16 copy
+    assert call_status(lib.moe_outer_nesterov, p, p, p, None, 10, 0.7, 0.9, None) == ERR_ARG
+    assert call_status(lib.moe_outer_nesterov, p, p, p, p, 10, 0.7, 0.9, p + 2) == ERR_UNSUPPORTED
+    # replica mean: too many peers, NULL peer
+    arr = (C.c_void_p * 17)(*([p] * 17))
+    assert call_status(lib.moe_replica_mean, p, arr, 17, 10, p) == ERR_ARG
+    arr1 = (C.c_void_p * 1)(None)
+    assert call_status(lib.moe_replica_mean, p, arr1, 1, 10, p) == ERR_ARG
