@@ -58,6 +58,10 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--optimizer", action="store_true",
+                    help="time whole training steps: fwd + bwd + AdamW on the resident and shared "
+                         "experts every step, and at the round cadence the delta average and the "
+                         "outer Nesterov step")
     ap.add_argument("--ghost-sweep", action="store_true",
                     help="tokens/s vs number of ghost experts, skip-token and partitioned router")
     ap.add_argument("--traffic-calibration", action="store_true",
@@ -101,6 +105,16 @@ def algorithmic_work(cfg, n, t_act, s):
     w["route_bwd_mfma"] = ("byte", T * E * 4 + 3 * T * d * s + E * d * s
                            + -(-T // 256) * E * d * 4)
     return w
+
+
+def optimizer_work(n_step_params, n_round_params, n_peers):
+    """Per-step bytes of the optimiser kernels: AdamW reads theta, g, m, v and
+    writes theta, m, v and the bf16 copy (30 B per parameter); the outer step
+    reads start, delta, momentum and writes momentum, start, now and the bf16
+    copy (26 B); the replica mean reads 1 + peers copies and writes one."""
+    return {"adamw_step": ("byte", 30.0 * n_step_params),
+            "outer_nesterov": ("byte", 26.0 * n_round_params),
+            "replica_mean": ("byte", 4.0 * (n_peers + 2) * n_round_params)}
 
 
 def ghost_sweep(args):
@@ -203,11 +217,62 @@ def main():
     peers = [dev(p, torch.float32) for p in dpar["peers"]]
     avg = torch.empty_like(th0)
     del dpar
+    opt = None
+    if args.optimizer:
+        # the resident experts' fp32 masters (theta_now) in the weights'
+        # layout: w_gate_up then w_down, each expert contiguous; the bf16
+        # weights the GEMMs read are views of one buffer of the same layout
+        n_gu = Er * 2 * H * d
+        w_lp = torch.empty(n_params, dtype=dt, device="cuda")
+        w_lp[:n_gu].copy_(wgu.reshape(-1))
+        w_lp[n_gu:].copy_(wd.reshape(-1))
+        wgu, wd = w_lp[:n_gu].view(Er, 2 * H, d), w_lp[n_gu:].view(Er, d, H)
+        th1.copy_(w_lp.float())
+        th0.copy_(th1)
+        opt = dict(m=torch.zeros_like(th1), v=torch.zeros_like(th1), mom=torch.zeros_like(th1),
+                   t=0, gu=th1[:n_gu], down=th1[n_gu:])
+        if Hs:
+            n_s = 3 * Hs * d
+            s_lp = torch.empty(n_s, dtype=dt, device="cuda")
+            s_lp[:2 * Hs * d].copy_(sgu.reshape(-1))
+            s_lp[2 * Hs * d:].copy_(sd.reshape(-1))
+            sgu, sd = s_lp[:2 * Hs * d].view(1, 2 * Hs, d), s_lp[2 * Hs * d:].view(1, d, Hs)
+            opt.update(s_master=s_lp.float(), s_m=torch.zeros(n_s, device="cuda"),
+                       s_v=torch.zeros(n_s, device="cuda"), s_lp=s_lp)
+        opt["lp"] = w_lp
+        log(f"[bench] optimiser state: AdamW m, v and outer momentum of {n_params / 1e6:.1f} M "
+            f"expert params" + (f" (+{3 * Hs * d / 1e6:.1f} M shared)" if Hs else ""))
+
+    def optimizer_step(i):
+        o = opt
+        o["t"] += 1
+        lr = 3e-4
+        # local AdamW on the resident experts (gradients of the layer's last
+        # backward), writing the bf16 weights in the same pass
+        n_gu = o["gu"].numel()
+        B.moe_adamw_step(o["gu"], L.dw_gate_up, o["m"][:n_gu], o["v"][:n_gu], n_gu, o["t"], lr,
+                         theta_bf16=o["lp"][:n_gu])
+        n_dn = o["down"].numel()
+        B.moe_adamw_step(o["down"], L.dw_down, o["m"][n_gu:], o["v"][n_gu:], n_dn, o["t"], lr,
+                         theta_bf16=o["lp"][n_gu:])
+        if Hs:
+            n_sg = 2 * Hs * d
+            B.moe_adamw_step(o["s_master"][:n_sg], L.s_dw_gate_up, o["s_m"][:n_sg],
+                             o["s_v"][:n_sg], n_sg, o["t"], lr, theta_bf16=o["s_lp"][:n_sg])
+            B.moe_adamw_step(o["s_master"][n_sg:], L.s_dw_down, o["s_m"][n_sg:], o["s_v"][n_sg:],
+                             Hs * d, o["t"], lr, theta_bf16=o["s_lp"][n_sg:])
+        if (i + 1) % args.round_every == 0:
+            # round boundary: replica-group average of the pseudo-gradient,
+            # outer Nesterov step, every replica restarts from its result
+            expert_delta(th0, th1, peers, delta_avg=avg)
+            B.moe_outer_nesterov(th0, th1, avg, o["mom"], n_params, 0.7, 0.9, theta_bf16=o["lp"])
 
     def step(i):
         L.forward(x, wr, wgu, wd, bias, sgu, sd)
         L.backward(dy, x, wr, wgu, wd, sgu, sd)
-        if (i + 1) % args.round_every == 0:
+        if opt is not None:
+            optimizer_step(i)
+        elif (i + 1) % args.round_every == 0:
             expert_delta(th0, th1, peers, delta_avg=avg)
 
     if args.traffic_calibration:
@@ -256,9 +321,12 @@ def main():
         work = algorithmic_work(cfg, n, t_act, s_bytes)
         n_delta = args.steps // args.round_every
         work["expert_delta"] = ("byte", 4.0 * n_params * (3 + len(peers)))
+        if opt is not None:
+            work.update(optimizer_work(n_params + 3 * Hs * d, n_params, len(peers)))
+        per_round = ("expert_delta", "outer_nesterov", "replica_mean")
         for name, (launches, tot, mn, mx) in stats.items():
             kind, per_step = work.get(name, ("byte", 0.0))
-            steps_with = n_delta if name == "expert_delta" else args.steps
+            steps_with = n_delta if name in per_round else args.steps
             amount = per_step * steps_with
             rate = amount / (tot / 1e3) if tot > 0 else 0.0
             if kind == "flop":
@@ -270,7 +338,7 @@ def main():
             ent.update(launches=launches, avg_us=1e3 * tot / max(launches, 1),
                        ms_per_step=tot / args.steps)
             kernels[name] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in ent.items()}
-        dom = max((nm for nm in kernels if nm != "expert_delta"),
+        dom = max((nm for nm in kernels if nm not in per_round),
                   key=lambda nm: kernels[nm]["ms_per_step"])
         kd = kernels[dom]
         kind, per_step = work[dom]
@@ -314,7 +382,8 @@ def main():
                           f"{cores} cores in the affinity mask, BLAS threads {blas_threads}")
 
     out = {
-        "metric": "MoE layer fwd+bwd tokens/s (1 GPU)",
+        "metric": ("MoE layer training step (fwd+bwd+AdamW) tokens/s (1 GPU)" if opt is not None
+                   else "MoE layer fwd+bwd tokens/s (1 GPU)"),
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -328,7 +397,8 @@ def main():
         "data": "synthetic (seeded, shapes of the workload)",
         "config": {"workload": cfg["name"], "T": T, "d": d, "E": E, "E_resident": Er, "k": k,
                    "H": H, "shared_hidden": Hs, "round_every": args.round_every,
-                   "executed_routes": n, "skip_fraction": round(1 - n / (T * k), 4)},
+                   "executed_routes": n, "skip_fraction": round(1 - n / (T * k), 4),
+                   "optimizer": "adamw+outer-nesterov" if opt is not None else None},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -403,13 +403,15 @@ __global__ __launch_bounds__(256) void expert_delta_kernel(DeltaArgs a) {
   const size_t n4 = a.n / 4;
   const size_t stride = (size_t)gridDim.x * 256;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
-    const f32x4_t s = reinterpret_cast<const f32x4_t*>(a.start)[i];
-    const f32x4_t w = reinterpret_cast<const f32x4_t*>(a.now)[i];
+    // a stream: nothing is read twice, so the accesses are nontemporal
+    const f32x4_t s = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(a.start) + i);
+    const f32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(a.now) + i);
     const f32x4_t dl = s - w;
     f32x4_t acc = dl;
-    for (int p = 0; p < a.n_peers; ++p) acc = acc + reinterpret_cast<const f32x4_t*>(a.peers[p])[i];
-    if (a.dl) reinterpret_cast<f32x4_t*>(a.dl)[i] = dl;
-    reinterpret_cast<f32x4_t*>(a.avg)[i] = acc * a.scale;
+    for (int p = 0; p < a.n_peers; ++p)
+      acc = acc + __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(a.peers[p]) + i);
+    if (a.dl) __builtin_nontemporal_store(dl, reinterpret_cast<f32x4_t*>(a.dl) + i);
+    __builtin_nontemporal_store(acc * a.scale, reinterpret_cast<f32x4_t*>(a.avg) + i);
   }
   // scalar tail
   for (size_t i = n4 * 4 + (size_t)blockIdx.x * 256 + threadIdx.x; i < a.n; i += stride) {
