@@ -246,7 +246,7 @@ constexpr int WCPL = 2;
 // keep the route order.  A separate add row is requested before the route
 // lookup; in place (add == out), a token without resident routes is left as
 // it is.
-template <class T>
+template <class T, bool STREAM_ROWS>
 DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const float* tw,
                            const int32_t* inv_perm, const T* add, T* out) {
   constexpr int V = Vec16<T>::N;
@@ -289,7 +289,10 @@ DEVI void weighted_row_sum(const T* rows, int T_, int d, int k, int cap, const f
 #pragma unroll
         for (int cc = 0; cc < WCPL; ++cc) {
           const int c = c0 + (cc * 64 + lane) * V;
-          if (c < d) raw[b][cc] = *reinterpret_cast<const u32x4_t*>(rows + (size_t)p[s0 + b] * d + c);
+          if (c < d) {
+            const u32x4_t* src = reinterpret_cast<const u32x4_t*>(rows + (size_t)p[s0 + b] * d + c);
+            raw[b][cc] = STREAM_ROWS ? __builtin_nontemporal_load(src) : *src;
+          }
         }
       }
 #pragma unroll
@@ -337,7 +340,8 @@ template <class T>
 __global__ __launch_bounds__(256) void unpermute_kernel(const T* dxp, int T_, int d, int k, int cap,
                                                         const int32_t* inv_perm, T* dx,
                                                         int accumulate) {
-  weighted_row_sum<T>(dxp, T_, d, k, cap, nullptr, inv_perm, accumulate ? dx : nullptr, dx);
+  // dxp is read only here: streamed past the caches
+  weighted_row_sum<T, true>(dxp, T_, d, k, cap, nullptr, inv_perm, accumulate ? dx : nullptr, dx);
 }
 
 template <class T>
@@ -345,7 +349,8 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(const T* yp, int T_, i
                                                           const float* tw,
                                                           const int32_t* inv_perm,
                                                           const T* y_add, T* y) {
-  weighted_row_sum<T>(yp, T_, d, k, cap, tw, inv_perm, y_add, y);
+  // yp stays cached: the backward's combine reads it again
+  weighted_row_sum<T, false>(yp, T_, d, k, cap, tw, inv_perm, y_add, y);
 }
 
 // dyp[slot] = w * dy[t] and dtw[t, j] = <dy[t], yp[slot]> for every resident
