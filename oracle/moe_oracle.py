@@ -26,8 +26,9 @@ What it computes (arxiv 2606.19025):
 * The worker holds a resident subset S_m of the experts (Sec. 3.3.1/3.3.2 and
   Alg. 1); routing is strictly local (Sec. 3.3.2 "System context and routing
   logic"), so the dispatch groups routes only by resident expert.
-* Expert FFN: SwiGLU without biases, hidden H (the workloads' choice; the
-  paper's own expert is a single projection followed by SiLU, App. B.3.1).
+* Expert FFN: SwiGLU without biases, hidden H (the workloads' choice), or,
+  with cfg["expert"] = "silu", the paper's own expert (App. B.3.1): a
+  projection to H followed by SiLU and the projection back.
   Shared experts are dense, always active, weight 1 (Sec. 3.2).
 * Round boundary (Alg. 2 "Simplified View"; Sec. 3.4): the expert-wise
   pseudo-gradient delta theta_start - theta_now of each resident expert,
@@ -217,33 +218,74 @@ def swiglu_bwd(dY, X, G, U, Hh, w_gate_up, w_down):
     return dict(dHh=dHh, dG=dG, dU=dU, dX=dX, dW_gate_up=dWgu, dW_down=dWd)
 
 
-def grouped_ffn_fwd(Xp, offsets, w_gate_up, w_down):
+def silu_mlp_fwd(X, w_up, w_down):
+    """The paper's own expert (App. B.3.1): a projection to the expert's hidden
+    size followed by SiLU, then the projection back (no biases):
+    A = X W1^T, Hh = silu(A), Y = Hh W2^T; w_up [H, d], w_down [d, H].
+    Returned in the SwiGLU layout with G = A and no U."""
+    X = _f64(X)
+    A = X @ _f64(w_up).T
+    Hh = silu(A)
+    return dict(G=A, U=None, Hh=Hh, Y=Hh @ _f64(w_down).T)
+
+
+def silu_mlp_bwd(dY, X, A, Hh, w_up, w_down):
+    """Chain rule of silu_mlp_fwd: dHh = dY W2; dW2 = dY^T Hh;
+    dA = dHh silu'(A); dX = dA W1; dW1 = dA^T X."""
+    dY, X, A, Hh = map(_f64, (dY, X, A, Hh))
+    dHh = dY @ _f64(w_down)
+    sg = 1.0 / (1.0 + np.exp(-A))
+    dA = dHh * (sg * (1.0 + A * (1.0 - sg)))
+    return dict(dHh=dHh, dG=dA, dU=None, dX=dA @ _f64(w_up), dW_gate_up=dA.T @ X,
+                dW_down=dY.T @ Hh)
+
+
+EXPERTS = ("swiglu", "silu")
+
+
+def expert_hidden(w_gate_up, expert):
+    """Hidden size H of one expert's first weight: [2H, d] (SwiGLU) or [H, d]."""
+    return w_gate_up.shape[-2] // (2 if expert == "swiglu" else 1)
+
+
+def grouped_ffn_fwd(Xp, offsets, w_gate_up, w_down, expert="swiglu"):
     """Per resident group r: rows [offsets[r], offsets[r+1]) of Xp through expert r."""
     Xp = _f64(Xp)
     n = int(offsets[-1])
-    H = w_gate_up.shape[1] // 2
+    H = expert_hidden(w_gate_up, expert)
     d = w_down.shape[1]
-    G = np.zeros((n, H)); U = np.zeros((n, H)); Hh = np.zeros((n, H)); Y = np.zeros((n, d))
+    G = np.zeros((n, H)); Hh = np.zeros((n, H)); Y = np.zeros((n, d))
+    U = np.zeros((n, H)) if expert == "swiglu" else None
     for r in range(len(offsets) - 1):
         a, b = int(offsets[r]), int(offsets[r + 1])
         if b > a:
-            o = swiglu_fwd(Xp[a:b], w_gate_up[r], w_down[r])
-            G[a:b], U[a:b], Hh[a:b], Y[a:b] = o["G"], o["U"], o["Hh"], o["Y"]
+            if expert == "swiglu":
+                o = swiglu_fwd(Xp[a:b], w_gate_up[r], w_down[r])
+                U[a:b] = o["U"]
+            else:
+                o = silu_mlp_fwd(Xp[a:b], w_gate_up[r], w_down[r])
+            G[a:b], Hh[a:b], Y[a:b] = o["G"], o["Hh"], o["Y"]
     return dict(G=G, U=U, Hh=Hh, Y=Y)
 
 
-def grouped_ffn_bwd(dYp, Xp, G, U, Hh, offsets, w_gate_up, w_down):
+def grouped_ffn_bwd(dYp, Xp, G, U, Hh, offsets, w_gate_up, w_down, expert="swiglu"):
     n = int(offsets[-1])
     Er = len(offsets) - 1
-    H = w_gate_up.shape[1] // 2
+    H = expert_hidden(w_gate_up, expert)
     d = w_down.shape[1]
-    dXp = np.zeros((n, d)); dG = np.zeros((n, H)); dU = np.zeros((n, H))
-    dWgu = np.zeros((Er, 2 * H, d)); dWd = np.zeros((Er, d, H))
+    rows_w1 = 2 * H if expert == "swiglu" else H
+    dXp = np.zeros((n, d)); dG = np.zeros((n, H))
+    dU = np.zeros((n, H)) if expert == "swiglu" else None
+    dWgu = np.zeros((Er, rows_w1, d)); dWd = np.zeros((Er, d, H))
     for r in range(Er):
         a, b = int(offsets[r]), int(offsets[r + 1])
         if b > a:
-            o = swiglu_bwd(dYp[a:b], Xp[a:b], G[a:b], U[a:b], Hh[a:b], w_gate_up[r], w_down[r])
-            dXp[a:b], dG[a:b], dU[a:b] = o["dX"], o["dG"], o["dU"]
+            if expert == "swiglu":
+                o = swiglu_bwd(dYp[a:b], Xp[a:b], G[a:b], U[a:b], Hh[a:b], w_gate_up[r], w_down[r])
+                dU[a:b] = o["dU"]
+            else:
+                o = silu_mlp_bwd(dYp[a:b], Xp[a:b], G[a:b], Hh[a:b], w_gate_up[r], w_down[r])
+            dXp[a:b], dG[a:b] = o["dX"], o["dG"]
             dWgu[r], dWd[r] = o["dW_gate_up"], o["dW_down"]
     return dict(dXp=dXp, dG=dG, dU=dU, dW_gate_up=dWgu, dW_down=dWd)
 
@@ -369,11 +411,13 @@ def layer_fwd(inp, inv_tau=1.0, gate="softmax_topk", logits=None):
     local = mask_routes(idx, inp["resident"])
     plan = dispatch_plan(local, E_r)
     Xp = gather_rows(x, plan["perm"], k)
-    f = grouped_ffn_fwd(Xp, plan["offsets"], inp["w_gate_up"], inp["w_down"])
+    expert = cfg.get("expert", "swiglu")
+    f = grouped_ffn_fwd(Xp, plan["offsets"], inp["w_gate_up"], inp["w_down"], expert)
     ys = None
     shared = None
     if inp.get("shared_gate_up") is not None:
-        shared = swiglu_fwd(x, inp["shared_gate_up"][0], inp["shared_down"][0])
+        one = swiglu_fwd if expert == "swiglu" else silu_mlp_fwd
+        shared = one(x, inp["shared_gate_up"][0], inp["shared_down"][0])
         ys = shared["Y"]
     y = combine_fwd(f["Y"], w, plan["inv_perm"], ys)
     return dict(logits=z, idx=idx, w=w, local=local, **plan, Xp=Xp, G=f["G"], U=f["U"],
@@ -386,13 +430,19 @@ def layer_bwd(inp, fwd, dy, inv_tau=1.0, gate="softmax_topk"):
     d = cfg["d"]
     x = _f64(inp["x"])
     cb = combine_bwd(dy, fwd["Yp"], fwd["w"], fwd["inv_perm"])
+    expert = cfg.get("expert", "swiglu")
     gb = grouped_ffn_bwd(cb["dYp"], fwd["Xp"], fwd["G"], fwd["U"], fwd["Hh"], fwd["offsets"],
-                         inp["w_gate_up"], inp["w_down"])
+                         inp["w_gate_up"], inp["w_down"], expert)
     dx_shared = None
     sb = None
     if fwd["shared"] is not None:
         s = fwd["shared"]
-        sb = swiglu_bwd(dy, x, s["G"], s["U"], s["Hh"], inp["shared_gate_up"][0], inp["shared_down"][0])
+        if expert == "swiglu":
+            sb = swiglu_bwd(dy, x, s["G"], s["U"], s["Hh"], inp["shared_gate_up"][0],
+                            inp["shared_down"][0])
+        else:
+            sb = silu_mlp_bwd(dy, x, s["G"], s["Hh"], inp["shared_gate_up"][0],
+                              inp["shared_down"][0])
         dx_shared = sb["dX"]
     dx = dispatch_bwd(gb["dXp"], fwd["inv_perm"], d, dx_shared)
     rb = route_bwd(x, inp["w_router"], fwd["idx"], fwd["w"], fwd["logits"], cb["dw"], inv_tau, gate)

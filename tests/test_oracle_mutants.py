@@ -17,9 +17,12 @@ FAST_PINS = [
     P.test_dispatch_empty_resident_set, P.test_single_expert_reduces_to_dense_swiglu_torch,
     P.test_swiglu_closed_form, P.test_full_replica_identity_no_renormalisation_over_survivors,
     P.test_fully_skipped_tokens_get_exact_zero, P.test_empty_resident_set_gives_zero_routed_output,
-    lambda: P.test_backward_matches_central_differences("softmax_topk"),
-    lambda: P.test_backward_matches_central_differences("softmax"),
-    lambda: P.test_backward_matches_central_differences("sigmoid"),
+    lambda: P.test_backward_matches_central_differences("softmax_topk", "swiglu"),
+    lambda: P.test_backward_matches_central_differences("softmax", "swiglu"),
+    lambda: P.test_backward_matches_central_differences("sigmoid", "swiglu"),
+    lambda: P.test_backward_matches_central_differences("sigmoid", "silu"),
+    P.test_silu_expert_matches_torch_dense_and_autograd,
+    P.test_silu_expert_single_resident_layer_is_dense_mlp,
     P.test_backward_matches_torch_autograd_dense_formulation, P.test_backward_is_linear_in_dy,
     P.test_expert_delta_closed_forms, P.test_expert_delta_within_fp32_bound_of_exact_mean,
     lambda: P.test_partitioned_router_brute_force(2, (1, 2, 4)),
@@ -132,7 +135,17 @@ def _replica_mean_over_peers_only(local, peers):
     return (acc * (f32(1.0) / f32(max(len(peers), 1)))).astype(f32)
 
 
+def _silu_bwd_sigmoid_derivative(dY, X, A, Hh, w_up, w_down):
+    o = _orig["silu_mlp_bwd"](dY, X, A, Hh, w_up, w_down)
+    A = np.asarray(A, np.float64)
+    o["dG"] = o["dHh"] / (1 + np.exp(-A))  # sigma(A) instead of silu'(A)
+    o["dX"] = o["dG"] @ np.asarray(w_up, np.float64)
+    o["dW_gate_up"] = o["dG"].T @ np.asarray(X, np.float64)
+    return o
+
+
 MUTANTS = {
+    "SiLU expert backward uses sigma instead of silu'": ("silu_mlp_bwd", _silu_bwd_sigmoid_derivative),
     "partitioned router keeps the first rows, not the resident ones":
         ("partition_router", _partition_keeps_all_router_rows),
     "AdamW without bias correction": ("adamw_bias_corrections", lambda *a: (np.float32(1), np.float32(1))),

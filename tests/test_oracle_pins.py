@@ -18,18 +18,20 @@ from paper_2606_19025_amd import inputs as I
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def tiny_inputs(T=24, d=16, E=6, k=2, H=8, resident=(1, 2, 4), seed=0, shared=0, bias=False):
+def tiny_inputs(T=24, d=16, E=6, k=2, H=8, resident=(1, 2, 4), seed=0, shared=0, bias=False,
+                expert="swiglu"):
     g = np.random.default_rng(seed)
     Er = len(resident)
     res = np.zeros(E, np.uint8)
     res[list(resident)] = 1
-    inp = dict(cfg=dict(T=T, d=d, E=E, k=k, H=H, E_r=Er, resident=sorted(resident)),
+    r1 = 2 if expert == "swiglu" else 1  # rows of the first weight per hidden unit
+    inp = dict(cfg=dict(T=T, d=d, E=E, k=k, H=H, E_r=Er, resident=sorted(resident), expert=expert),
                x=g.standard_normal((T, d)), w_router=g.standard_normal((E, d)) * 0.5,
-               w_gate_up=g.standard_normal((Er, 2 * H, d)) * 0.3,
+               w_gate_up=g.standard_normal((Er, r1 * H, d)) * 0.3,
                w_down=g.standard_normal((Er, d, H)) * 0.3, resident=res,
                router_bias=g.standard_normal(E) * 0.3 if bias else None)
     if shared:
-        inp["shared_gate_up"] = g.standard_normal((1, 2 * shared, d)) * 0.3
+        inp["shared_gate_up"] = g.standard_normal((1, r1 * shared, d)) * 0.3
         inp["shared_down"] = g.standard_normal((1, d, shared)) * 0.3
     return inp
 
@@ -263,9 +265,11 @@ def _loss(inp, dy, gate, inv_tau, idx_ref):
     return float((f["y"] * dy).sum())
 
 
-@pytest.mark.parametrize("gate", ["softmax_topk", "softmax", "sigmoid"])
-def test_backward_matches_central_differences(gate):
-    inp = tiny_inputs(T=10, d=6, E=5, k=2, H=4, resident=(0, 2, 3), shared=3, bias=True, seed=11)
+@pytest.mark.parametrize("gate,expert", [("softmax_topk", "swiglu"), ("softmax", "swiglu"),
+                                          ("sigmoid", "swiglu"), ("sigmoid", "silu")])
+def test_backward_matches_central_differences(gate, expert):
+    inp = tiny_inputs(T=10, d=6, E=5, k=2, H=4, resident=(0, 2, 3), shared=3, bias=True, seed=11,
+                      expert=expert)
     inv_tau = 0.7
     g = np.random.default_rng(12)
     dy = g.standard_normal((10, 6))
@@ -525,3 +529,34 @@ def test_replica_mean_closed_forms():
     got = O.replica_mean(x, peers)
     bound = 4 * 2.0 ** -24 * (np.abs(x) + sum(np.abs(p) for p in peers)).astype(np.float64)
     assert np.all(np.abs(got - exact) <= bound)
+
+
+# ---------------------------------------------------------------- SiLU expert
+
+def test_silu_expert_matches_torch_dense_and_autograd():
+    """The paper's own expert (App. B.3.1) on every token of one dense expert:
+    forward against torch.nn.functional.silu and backward against
+    torch.autograd, in fp64 on the CPU."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(41)
+    X, W1, W2 = g.standard_normal((13, 7)), g.standard_normal((5, 7)), g.standard_normal((7, 5))
+    dY = g.standard_normal((13, 7))
+    f = O.silu_mlp_fwd(X, W1, W2)
+    b = O.silu_mlp_bwd(dY, X, f["G"], f["Hh"], W1, W2)
+    tx, t1, t2 = (torch.tensor(a, requires_grad=True) for a in (X, W1, W2))
+    y = torch.nn.functional.silu(tx @ t1.T) @ t2.T
+    y.backward(torch.from_numpy(dY))
+    assert np.allclose(f["Y"], y.detach().numpy(), rtol=1e-12, atol=1e-12)
+    for mine, ref in ((b["dX"], tx.grad), (b["dW_gate_up"], t1.grad), (b["dW_down"], t2.grad)):
+        assert np.allclose(mine, ref.numpy(), rtol=1e-11, atol=1e-11)
+
+
+def test_silu_expert_single_resident_layer_is_dense_mlp():
+    inp = tiny_inputs(T=12, d=6, E=4, k=1, H=5, resident=(0, 1, 2, 3), seed=42, expert="silu")
+    f = O.layer_fwd(inp)
+    x = inp["x"]
+    for t in range(12):
+        e = int(f["idx"][t, 0])
+        a = x[t] @ inp["w_gate_up"][e].T
+        ref = (a / (1 + np.exp(-a))) @ inp["w_down"][e].T
+        assert np.allclose(f["y"][t], f["w"][t, 0] * ref, rtol=1e-12, atol=1e-14)
