@@ -62,6 +62,9 @@ def parse():
                     help="time whole training steps: fwd + bwd + AdamW on the resident and shared "
                          "experts every step, and at the round cadence the delta average and the "
                          "outer Nesterov step")
+    ap.add_argument("--expert", choices=["swiglu", "silu"], default="swiglu",
+                    help="expert form: SwiGLU (the workloads') or the paper's SiLU expert "
+                         "(its first weight is the first H rows of the SwiGLU draw)")
     ap.add_argument("--ghost-sweep", action="store_true",
                     help="tokens/s vs number of ghost experts, skip-token and partitioned router")
     ap.add_argument("--traffic-calibration", action="store_true",
@@ -70,11 +73,12 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_work(cfg, n, t_act, s):
+def algorithmic_work(cfg, n, t_act, s, expert="swiglu"):
     """Per-step algorithmic flops / bytes of every kernel (summed over its launches).
 
     n: executed (resident) routes; t_act: tokens with at least one resident
-    route; s: bytes per activation element.
+    route; s: bytes per activation element; expert: "swiglu" or "silu" (one
+    first projection of width H instead of two).
     """
     T, d, E, k, H = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["H"]
     Hs = cfg["n_shared"] * cfg["Hs"]
@@ -87,6 +91,12 @@ def algorithmic_work(cfg, n, t_act, s):
     w["gemm_dx_bwd"] = ("flop", sum(2.0 * m * 2 * h * d for m, h in rows))
     w["gemm_dwd"] = ("flop", sum(2.0 * m * d * h for m, h in rows))
     w["gemm_dwgu"] = ("flop", sum(2.0 * m * 2 * h * d for m, h in rows))
+    if expert == "silu":
+        w["gemm_up_fwd"] = ("flop", sum(2.0 * m * d * h for m, h in rows))
+        w["gemm_dh_bwd"] = w.pop("gemm_dhh_bwd")
+        w["gemm_dx_bwd"] = ("flop", sum(2.0 * m * h * d for m, h in rows))
+        w["gemm_dwgu"] = ("flop", sum(2.0 * m * h * d for m, h in rows))
+        del w["gemm_gu_fwd"]
     # routing / data movement: bytes (HBM-bound)
     w["route_fwd"] = ("byte", T * d * s + E * d * s + T * E * 4 + 3 * T * k * 4)
     w["dispatch_count"] = ("byte", T * k * 4)
@@ -205,12 +215,19 @@ def main():
     s_bytes = 2 if dt == torch.bfloat16 else 4
     dev = lambda a, t=dt: None if a is None else torch.from_numpy(
         np.ascontiguousarray(a, np.float32)).cuda().to(t)
+    silu = args.expert == "silu"
+    if silu:  # the SiLU expert's W1 [H, d]: the first H rows of the drawn [2H, d]
+        inp["w_gate_up"] = np.ascontiguousarray(inp["w_gate_up"][:, :H])
+        if inp.get("shared_gate_up") is not None:
+            inp["shared_gate_up"] = np.ascontiguousarray(inp["shared_gate_up"][:, :Hs])
     x, dy, wr, wgu, wd = (dev(inp[n]) for n in ("x", "dy", "w_router", "w_gate_up", "w_down"))
     bias = dev(inp.get("router_bias"), torch.float32)
     sgu, sd = dev(inp.get("shared_gate_up")), dev(inp.get("shared_down"))
-    L = ResidentMoELayer(T, d, E, k, H, inp["resident"], dtype=dt, n_shared_hidden=Hs)
+    L = ResidentMoELayer(T, d, E, k, H, inp["resident"], dtype=dt, n_shared_hidden=Hs,
+                         expert=args.expert)
+    r1 = 1 if silu else 2  # rows of the first expert weight per hidden unit
     # round boundary: fp32 master copies of the resident experts
-    n_params = Er * (2 * H * d + d * H)
+    n_params = Er * (r1 * H * d + d * H)
     log(f"[bench] round-boundary state: {n_params / 1e6:.1f} M fp32 params x {2 + max(1, cfg['n_peers'])}")
     dpar = I.make_delta_inputs(wl, n_params, seed=args.seed)
     th0, th1 = dev(dpar["theta_start"], torch.float32), dev(dpar["theta_now"], torch.float32)
@@ -222,26 +239,26 @@ def main():
         # the resident experts' fp32 masters (theta_now) in the weights'
         # layout: w_gate_up then w_down, each expert contiguous; the bf16
         # weights the GEMMs read are views of one buffer of the same layout
-        n_gu = Er * 2 * H * d
+        n_gu = Er * r1 * H * d
         w_lp = torch.empty(n_params, dtype=dt, device="cuda")
         w_lp[:n_gu].copy_(wgu.reshape(-1))
         w_lp[n_gu:].copy_(wd.reshape(-1))
-        wgu, wd = w_lp[:n_gu].view(Er, 2 * H, d), w_lp[n_gu:].view(Er, d, H)
+        wgu, wd = w_lp[:n_gu].view(Er, r1 * H, d), w_lp[n_gu:].view(Er, d, H)
         th1.copy_(w_lp.float())
         th0.copy_(th1)
         opt = dict(m=torch.zeros_like(th1), v=torch.zeros_like(th1), mom=torch.zeros_like(th1),
                    t=0, gu=th1[:n_gu], down=th1[n_gu:])
         if Hs:
-            n_s = 3 * Hs * d
+            n_s = (r1 + 1) * Hs * d
             s_lp = torch.empty(n_s, dtype=dt, device="cuda")
-            s_lp[:2 * Hs * d].copy_(sgu.reshape(-1))
-            s_lp[2 * Hs * d:].copy_(sd.reshape(-1))
-            sgu, sd = s_lp[:2 * Hs * d].view(1, 2 * Hs, d), s_lp[2 * Hs * d:].view(1, d, Hs)
+            s_lp[:r1 * Hs * d].copy_(sgu.reshape(-1))
+            s_lp[r1 * Hs * d:].copy_(sd.reshape(-1))
+            sgu, sd = s_lp[:r1 * Hs * d].view(1, r1 * Hs, d), s_lp[r1 * Hs * d:].view(1, d, Hs)
             opt.update(s_master=s_lp.float(), s_m=torch.zeros(n_s, device="cuda"),
                        s_v=torch.zeros(n_s, device="cuda"), s_lp=s_lp)
         opt["lp"] = w_lp
         log(f"[bench] optimiser state: AdamW m, v and outer momentum of {n_params / 1e6:.1f} M "
-            f"expert params" + (f" (+{3 * Hs * d / 1e6:.1f} M shared)" if Hs else ""))
+            f"expert params" + (f" (+{(r1 + 1) * Hs * d / 1e6:.1f} M shared)" if Hs else ""))
 
     def optimizer_step(i):
         o = opt
@@ -256,7 +273,7 @@ def main():
         B.moe_adamw_step(o["down"], L.dw_down, o["m"][n_gu:], o["v"][n_gu:], n_dn, o["t"], lr,
                          theta_bf16=o["lp"][n_gu:])
         if Hs:
-            n_sg = 2 * Hs * d
+            n_sg = r1 * Hs * d
             B.moe_adamw_step(o["s_master"][:n_sg], L.s_dw_gate_up, o["s_m"][:n_sg],
                              o["s_v"][:n_sg], n_sg, o["t"], lr, theta_bf16=o["s_lp"][:n_sg])
             B.moe_adamw_step(o["s_master"][n_sg:], L.s_dw_down, o["s_m"][n_sg:], o["s_v"][n_sg:],
@@ -318,11 +335,11 @@ def main():
         torch.cuda.synchronize()
         stats = B.moe_timing_collect()
         B.moe_timing_enable(0)
-        work = algorithmic_work(cfg, n, t_act, s_bytes)
+        work = algorithmic_work(cfg, n, t_act, s_bytes, args.expert)
         n_delta = args.steps // args.round_every
         work["expert_delta"] = ("byte", 4.0 * n_params * (3 + len(peers)))
         if opt is not None:
-            work.update(optimizer_work(n_params + 3 * Hs * d, n_params, len(peers)))
+            work.update(optimizer_work(n_params + (r1 + 1) * Hs * d, n_params, len(peers)))
         per_round = ("expert_delta", "outer_nesterov", "replica_mean")
         for name, (launches, tot, mn, mx) in stats.items():
             kind, per_step = work.get(name, ("byte", 0.0))
@@ -398,7 +415,8 @@ def main():
         "config": {"workload": cfg["name"], "T": T, "d": d, "E": E, "E_resident": Er, "k": k,
                    "H": H, "shared_hidden": Hs, "round_every": args.round_every,
                    "executed_routes": n, "skip_fraction": round(1 - n / (T * k), 4),
-                   "optimizer": "adamw+outer-nesterov" if opt is not None else None},
+                   "optimizer": "adamw+outer-nesterov" if opt is not None else None,
+                   "expert": args.expert},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -185,6 +185,18 @@ int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const v
  * yp).  gu and h are written by the forward and read by the backward.
  * n_sets is 1 or 2; all sets share dtype and d.
  */
+/*
+ * Expert form of a set.  MOE_ACT_SWIGLU: the SwiGLU expert above.
+ * MOE_ACT_SILU: the paper's own expert (App. B.3.1), a projection to the
+ * hidden size followed by SiLU and the projection back,
+ *   A = X W1^T;  Hh = silu(A);  Y = Hh Wd^T
+ * with backward dHh = dY Wd, dA = dHh * silu'(A), dX = dA W1, dW1 = dA^T X,
+ * dWd = dY^T Hh.  Then w_gate_up holds W1 [n_groups, H, d], gu holds A
+ * [cap, H], dgu holds dA [cap, H] and dw_gate_up is [n_groups, H, d]; every
+ * other field is as for SwiGLU.
+ */
+enum { MOE_ACT_SWIGLU = 0, MOE_ACT_SILU = 1 };
+
 typedef struct moe_ffn_set {
   const void* xp;          /* [cap, d] */
   const void* w_gate_up;   /* [n_groups, 2H, d] */
@@ -199,6 +211,7 @@ typedef struct moe_ffn_set {
   void* dxp;               /* [cap, d] */
   float* dw_gate_up;       /* [n_groups, 2H, d] fp32 */
   float* dw_down;          /* [n_groups, d, H] fp32 */
+  int activation;          /* MOE_ACT_SWIGLU (0) or MOE_ACT_SILU; the same in every set */
 } moe_ffn_set;
 
 int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,

@@ -80,15 +80,19 @@ class moe_ffn_set(C.Structure):
     _fields_ = [("xp", _P), ("w_gate_up", _P), ("w_down", _P), ("offsets", _P),
                 ("cap", _I), ("H", _I), ("n_groups", _I),
                 ("gu", _P), ("h", _P), ("yp", _P), ("dyp", _P), ("dgu", _P), ("dxp", _P),
-                ("dw_gate_up", _P), ("dw_down", _P)]
+                ("dw_gate_up", _P), ("dw_down", _P), ("activation", _I)]
+
+
+MOE_ACT_SWIGLU, MOE_ACT_SILU = 0, 1
+ACTIVATIONS = {"swiglu": MOE_ACT_SWIGLU, "silu": MOE_ACT_SILU}
 
 
 def ffn_set(xp, w_gate_up, w_down, offsets, cap, H, n_groups, gu, h, yp=None, dyp=None,
-            dgu=None, dxp=None, dw_gate_up=None, dw_down=None):
+            dgu=None, dxp=None, dw_gate_up=None, dw_down=None, activation=MOE_ACT_SWIGLU):
     """A moe_ffn_set from tensors (or raw addresses / None)."""
     return moe_ffn_set(_ptr(xp), _ptr(w_gate_up), _ptr(w_down), _ptr(offsets), cap, H, n_groups,
                        _ptr(gu), _ptr(h), _ptr(yp), _ptr(dyp), _ptr(dgu), _ptr(dxp),
-                       _ptr(dw_gate_up), _ptr(dw_down))
+                       _ptr(dw_gate_up), _ptr(dw_down), activation)
 
 
 def lib(path: str | None = None):

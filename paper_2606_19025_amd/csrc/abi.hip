@@ -156,7 +156,7 @@ int moe_timing_collect(moe_kernel_time* out, int max_out, int* n_out) {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
 
-int moe_abi_version(void) { return 1; }
+int moe_abi_version(void) { return 2; }
 
 int moe_route_mask(const void* x, const void* w_router, const float* router_bias, int dtype,
                    int T, int d, int E, int k, float inv_tau, int gate,
@@ -288,6 +288,11 @@ int check_set(const moe_ffn_set& f, int dtype, int d, bool fwd) {
 
 int check_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d, bool fwd) {
   REQUIRE(sets != nullptr && n_sets >= 1 && n_sets <= 2, "n_sets = %d must be 1 or 2", n_sets);
+  for (int i = 0; i < n_sets; ++i) {
+    REQUIRE(sets[i].activation == MOE_ACT_SWIGLU || sets[i].activation == MOE_ACT_SILU,
+            "sets[%d].activation = %d is not an expert form", i, sets[i].activation);
+    REQUIRE(sets[i].activation == sets[0].activation, "all sets must have the same activation");
+  }
   for (int i = 0; i < n_sets; ++i) {
     const int r = check_set(sets[i], dtype, d, fwd);
     if (r != MOE_OK) return r;

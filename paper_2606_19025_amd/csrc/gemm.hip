@@ -30,13 +30,17 @@
 namespace moe {
 namespace {
 
-enum GemmKind { GU_FWD = 0, DOWN_FWD = 1, DHH_BWD = 2, DX_BWD = 3, DWD = 4, DWGU = 5 };
+// UP_FWD and DH_BWD are GU_FWD and DHH_BWD for the SiLU expert (one first
+// projection W1 [H, d] instead of [Wg; Wu]).
+enum GemmKind {
+  GU_FWD = 0, DOWN_FWD = 1, DHH_BWD = 2, DX_BWD = 3, DWD = 4, DWGU = 5, UP_FWD = 6, DH_BWD = 7
+};
 
 template <int KIND>
 struct Kind {
-  static constexpr bool MRAG = KIND <= DX_BWD;  // ragged in M (else in K)
-  static constexpr bool A_KC = KIND <= DX_BWD;  // A contiguous along k
-  static constexpr bool B_KC = KIND <= DOWN_FWD;  // B contiguous along k
+  static constexpr bool MRAG = KIND <= DX_BWD || KIND >= UP_FWD;  // ragged in M (else in K)
+  static constexpr bool A_KC = MRAG;                                // A contiguous along k
+  static constexpr bool B_KC = KIND <= DOWN_FWD || KIND == UP_FWD;  // B contiguous along k
 };
 
 struct GemmArgs {
@@ -129,6 +133,21 @@ DEVI void epi_store(const GemmArgs& a, const Tile& t, int i, int j, float v) {
       dgu[m * 2 * a.H + h] = from_f32<T>(v * U * dsilu_f(G));
       dgu[m * 2 * a.H + a.H + h] = from_f32<T>(v * silu_f(G));
     }
+  } else if constexpr (KIND == UP_FWD) {
+    const int h = t.n0 + j;
+    if (i < t.rows && h < a.N) {
+      const size_t m = (size_t)(t.row0 + i);
+      const T A = from_f32<T>(v);
+      static_cast<T*>(a.C)[m * a.ldc + h] = A;
+      static_cast<T*>(a.out2)[m * a.H + h] = from_f32<T>(silu_f(to_f32(A)));
+    }
+  } else if constexpr (KIND == DH_BWD) {
+    const int h = t.n0 + j;
+    if (i < t.rows && h < a.N) {
+      const size_t m = (size_t)(t.row0 + i);
+      const float A = to_f32(static_cast<const T*>(a.aux)[m * a.H + h]);
+      static_cast<T*>(a.C)[m * a.ldc + h] = from_f32<T>(v * dsilu_f(A));
+    }
   } else if constexpr (KIND == DWD || KIND == DWGU) {
     const int m = t.m0 + i, n = t.n0 + j;
     if (m < a.M && n < a.N) {
@@ -190,7 +209,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
           bool ok;
           const int br = gu_brow<BN>(blockIdx.x, j, a.H, ok);
           if (ok) v = B[(size_t)br * a.ldb + k];
-        } else if constexpr (KIND == DOWN_FWD) {
+        } else if constexpr (KIND == DOWN_FWD || KIND == UP_FWD) {
           if (tl.n0 + j < a.N) v = B[(size_t)(tl.n0 + j) * a.ldb + k];
         } else if constexpr (Kind<KIND>::MRAG) {  // NN
           if (tl.n0 + j < a.N) v = B[(size_t)k * a.ldb + tl.n0 + j];
@@ -781,6 +800,51 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
                 }
               }
             }
+          } else if constexpr (KIND == DH_BWD) {
+            // dA = dHh * silu'(A); A of a batch of rows is loaded before any
+            // store of it
+            const bf16_t* Ab = static_cast<const bf16_t*>(a.aux);
+            bf16_t* C = static_cast<bf16_t*>(a.C);
+            for (int it0 = 0; it0 < 32; it0 += 8) {
+              if (it0 * 4 >= row_lim) break;
+              bf16x8_t Av[8];
+#pragma unroll
+              for (int b = 0; b < 8; ++b) {
+                const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
+                Av[b] = *reinterpret_cast<const bf16x8_t*>(
+                    Ab + (size_t)(tl.row0 + wm * 128 + row) * a.H + col);
+              }
+#pragma unroll
+              for (int b = 0; b < 8; ++b) {
+                const int row = (it0 + b) * 4 + (lane >> 4);
+                const bf16x8_t v = epi_get(reg, row, c);
+                bf16x8_t dA;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const float g = (float)Av[b][e];
+                  const float sg = sigmoid_fast(g);
+                  dA[e] = (bf16_t)((float)v[e] * (sg * (1.0f + g * (1.0f - sg))));
+                }
+                if (row < row_lim)
+                  *reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * 128 + row) * a.ldc + col) = dA;
+              }
+            }
+          } else if constexpr (KIND == UP_FWD) {
+            // A and h = silu(A) (of the bf16-rounded A)
+            bf16_t* C = static_cast<bf16_t*>(a.C);
+            bf16_t* hh = static_cast<bf16_t*>(a.out2);
+#pragma unroll 8
+            for (int it = 0; it < 32; ++it) {
+              const int row = it * 4 + (lane >> 4);
+              if (row >= row_lim) break;
+              const bf16x8_t A = epi_get(reg, row, c);
+              bf16x8_t Hv;
+#pragma unroll
+              for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)silu_fast((float)A[e]);
+              const size_t m = (size_t)(tl.row0 + wm * 128 + row);
+              *reinterpret_cast<bf16x8_t*>(C + m * a.ldc + col) = A;
+              *reinterpret_cast<bf16x8_t*>(hh + m * a.H + col) = Hv;
+            }
           } else {  // DOWN_FWD / DX_BWD
             bf16_t* C = static_cast<bf16_t*>(a.C);
 #pragma unroll 8
@@ -828,7 +892,8 @@ long max_tiles(const GemmArgs& a) {
 }
 
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
-                                      "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu"};
+                                      "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu",
+                                      "gemm_up_fwd", "gemm_dh_bwd"};
 
 // One launch over the sets sets[0..n_sets) (at most 2) of one GEMM kind.
 // counters (bf16 only): zeroed per-XCD tile counters for dynamic dealing;
@@ -919,34 +984,37 @@ size_t align_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
 }  // namespace
 
+// Rows of an expert's first weight per hidden unit: 2 (gate and up) for
+// SwiGLU, 1 for the SiLU expert.
+long first_rows(const moe_ffn_set& f) { return f.activation == MOE_ACT_SILU ? 1 : 2; }
+
 size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
   size_t bytes = align_up(kCounterWords * sizeof(int));
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
-    const long H = f.H;
+    const long H = f.H, R1 = first_rows(f);
     const int s_wd = ksplit_factor(bf16, d, H, f);
-    const int s_wgu = ksplit_factor(bf16, 2 * H, d, f);
+    const int s_wgu = ksplit_factor(bf16, R1 * H, d, f);
     if (s_wd > 1) bytes += align_up((size_t)s_wd * d * H * sizeof(float));
-    if (s_wgu > 1) bytes += align_up((size_t)s_wgu * 2 * H * d * sizeof(float));
+    if (s_wgu > 1) bytes += align_up((size_t)s_wgu * R1 * H * d * sizeof(float));
   }
   return bytes;
 }
 
-namespace {
-}  // namespace
-
 hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
                                hipStream_t s) {
   GemmArgs g[2]{}, o[2]{};
+  const bool silu = sets[0].activation == MOE_ACT_SILU;  // the same for every set
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
-    // [G|U] = X [Wg;Wu]^T with the SwiGLU epilogue
+    const long R1 = first_rows(f);
+    // [G|U] = X [Wg;Wu]^T with the SwiGLU epilogue, or A = X W1^T with SiLU
     GemmArgs& a = g[i];
     a.offsets = f.offsets; a.n_groups = f.n_groups; a.cap = f.cap; a.H = f.H;
     a.A = f.xp; a.lda = d;
-    a.B = f.w_gate_up; a.ldb = d; a.b_gs = 2L * f.H * d;
-    a.C = f.gu; a.ldc = 2L * f.H; a.out2 = f.h;
-    a.N = 2 * f.H; a.K = d;
+    a.B = f.w_gate_up; a.ldb = d; a.b_gs = R1 * f.H * d;
+    a.C = f.gu; a.ldc = R1 * f.H; a.out2 = f.h;
+    a.N = (int)(R1 * f.H); a.K = d;
     // Y = Hh Wd^T
     GemmArgs& b = o[i];
     b.offsets = f.offsets; b.n_groups = f.n_groups; b.cap = f.cap; b.H = f.H;
@@ -955,7 +1023,7 @@ hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     b.C = f.yp; b.ldc = d;
     b.N = d; b.K = f.H;
   }
-  hipError_t e = run_gemm<GU_FWD>(g, n_sets, bf16, s);
+  hipError_t e = silu ? run_gemm<UP_FWD>(g, n_sets, bf16, s) : run_gemm<GU_FWD>(g, n_sets, bf16, s);
   if (e != hipSuccess) return e;
   return run_gemm<DOWN_FWD>(o, n_sets, bf16, s);
 }
@@ -969,36 +1037,37 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
   struct Reduce { float* dst; const float* parts; int n_parts; size_t n; };
   Reduce red[4];
   int n_red = 0;
+  const bool silu = sets[0].activation == MOE_ACT_SILU;  // the same for every set
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
-    const long H = f.H;
+    const long H = f.H, R1 = first_rows(f);
     GemmArgs base{};
     base.offsets = f.offsets; base.n_groups = f.n_groups; base.cap = f.cap; base.H = f.H;
     base.accumulate = accumulate_dw;
-    // dHh = dY Wd, epilogue -> [dG | dU]
+    // dHh = dY Wd, epilogue -> [dG | dU] (SwiGLU) or dA (SiLU)
     GemmArgs& a = hh[i] = base;
     a.A = f.dyp; a.lda = d;
     a.B = f.w_down; a.ldb = H; a.b_gs = (long)d * H;
-    a.C = f.dgu; a.ldc = 2 * H; a.aux = f.gu;
+    a.C = f.dgu; a.ldc = R1 * H; a.aux = f.gu;
     a.N = f.H; a.K = d;
-    // dX = [dG|dU] [Wg;Wu]
+    // dX = [dG|dU] [Wg;Wu]  (SiLU: dA W1)
     GemmArgs& b = dx[i] = base;
-    b.A = f.dgu; b.lda = 2 * H;
-    b.B = f.w_gate_up; b.ldb = d; b.b_gs = 2 * H * d;
+    b.A = f.dgu; b.lda = R1 * H;
+    b.B = f.w_gate_up; b.ldb = d; b.b_gs = R1 * H * d;
     b.C = f.dxp; b.ldc = d;
-    b.N = d; b.K = 2 * f.H;
+    b.N = d; b.K = (int)(R1 * f.H);
     // dWd[g] = dY^T Hh
     GemmArgs& c = wd[i] = base;
     c.A = f.dyp; c.lda = d;
     c.B = f.h; c.ldb = H;
     c.C = f.dw_down; c.ldc = H; c.c_gs = (long)d * H;
     c.M = d; c.N = f.H;
-    // dWgu[g] = [dG|dU]^T X
+    // dWgu[g] = [dG|dU]^T X  (SiLU: dW1 = dA^T X)
     GemmArgs& w = wgu[i] = base;
-    w.A = f.dgu; w.lda = 2 * H;
+    w.A = f.dgu; w.lda = R1 * H;
     w.B = f.xp; w.ldb = d;
-    w.C = f.dw_gate_up; w.ldc = d; w.c_gs = 2 * H * d;
-    w.M = 2 * f.H; w.N = d;
+    w.C = f.dw_gate_up; w.ldc = d; w.c_gs = R1 * H * d;
+    w.M = (int)(R1 * f.H); w.N = d;
     if (ws) {
       for (GemmArgs* g : {&c, &w}) {
         const int S = ksplit_factor(bf16, g->M, g->N, f);
@@ -1015,9 +1084,11 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
   }
   hipError_t e;
   // the first launch clears the counters of the two weight-gradient launches
-  if ((e = run_gemm<DHH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
-                             ws ? kCounterWords : 0)) != hipSuccess)
-    return e;
+  e = silu ? run_gemm<DH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
+                              ws ? kCounterWords : 0)
+           : run_gemm<DHH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
+                               ws ? kCounterWords : 0);
+  if (e != hipSuccess) return e;
   if ((e = run_gemm<DX_BWD>(dx, n_sets, bf16, s)) != hipSuccess) return e;
   if ((e = run_gemm<DWD>(wd, n_sets, bf16, s, ws ? counters : nullptr)) != hipSuccess) return e;
   if ((e = run_gemm<DWGU>(wgu, n_sets, bf16, s, ws ? counters + N_XCD : nullptr)) != hipSuccess)

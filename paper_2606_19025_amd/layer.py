@@ -24,12 +24,17 @@ from . import binding as B
 
 class ResidentMoELayer:
     def __init__(self, T, d, E, k, H, resident, dtype=torch.bfloat16, n_shared_hidden=0,
-                 gate="softmax_topk", inv_tau=1.0, device="cuda", partitioned=False):
+                 gate="softmax_topk", inv_tau=1.0, device="cuda", partitioned=False,
+                 expert="swiglu"):
         self.T, self.d, self.E, self.k, self.H = int(T), int(d), int(E), int(k), int(H)
         res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
         assert res.numel() == self.E
         self.E_r = int(res.sum().item())
         self.partitioned = bool(partitioned)
+        # expert form: SwiGLU ([Wg; Wu] and [G | U], 2H wide) or the paper's
+        # SiLU expert (W1 and A, H wide)
+        self.act = B.ACTIVATIONS[expert]
+        r1 = 2 if self.act == B.MOE_ACT_SWIGLU else 1
         if self.partitioned:
             if self.E_r == 0:
                 raise ValueError("a partitioned router needs at least one resident expert")
@@ -64,16 +69,16 @@ class ResidentMoELayer:
         # experts
         rows = max(cap, 1)
         self.xp = e(rows, d)
-        self.gu = e(rows, 2 * H)
+        self.gu = e(rows, r1 * H)
         self.h = e(rows, H)
         self.yp = e(rows, d)
         self.y = e(T, d)
         # backward
         self.dyp = e(rows, d)
         self.dtopk_w = e(T, k, dt=f32)
-        self.dgu = e(rows, 2 * H)
+        self.dgu = e(rows, r1 * H)
         self.dxp = e(rows, d)
-        self.dw_gate_up = e(max(self.E_r, 1), 2 * H, d, dt=f32)
+        self.dw_gate_up = e(max(self.E_r, 1), r1 * H, d, dt=f32)
         self.dw_down = e(max(self.E_r, 1), d, H, dt=f32)
         self.dx = e(T, d)
         self.dz = e(T, E, dt=f32)
@@ -85,11 +90,11 @@ class ResidentMoELayer:
         if self.Hs:
             Hs = self.Hs
             self.s_offsets = torch.tensor([0, T], dtype=i32, device=dev)
-            self.s_gu = e(T, 2 * Hs)
+            self.s_gu = e(T, r1 * Hs)
             self.s_h = e(T, Hs)
             self.s_y = e(T, d)
-            self.s_dgu = e(T, 2 * Hs)
-            self.s_dw_gate_up = e(1, 2 * Hs, d, dt=f32)
+            self.s_dgu = e(T, r1 * Hs)
+            self.s_dw_gate_up = e(1, r1 * Hs, d, dt=f32)
             self.s_dw_down = e(1, d, Hs, dt=f32)
 
     # ------------------------------------------------------------------ forward
@@ -103,12 +108,12 @@ class ResidentMoELayer:
                        self.perm, self.inv_perm, self.xp, self.ws_dispatch, self.ws_dispatch_bytes,
                        stream)
         sets = [B.ffn_set(self.xp, w_gate_up, w_down, self.offsets, cap, H, self.E_r, self.gu,
-                          self.h, yp=self.yp)]
+                          self.h, yp=self.yp, activation=self.act)]
         y_add = None
         if self.Hs:
             # the shared experts see every token: their "dispatched rows" are x
             sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
-                                  self.s_gu, self.s_h, yp=self.s_y))
+                                  self.s_gu, self.s_h, yp=self.s_y, activation=self.act))
             y_add = self.s_y
         B.moe_grouped_ffn_fwd_sets(sets, dt, d, stream)
         B.moe_combine_fwd(self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, y_add, self.y,
@@ -123,12 +128,13 @@ class ResidentMoELayer:
                           self.dtopk_w, stream)
         sets = [B.ffn_set(self.xp, w_gate_up, w_down, self.offsets, cap, H, self.E_r, self.gu,
                           self.h, dyp=self.dyp, dgu=self.dgu, dxp=self.dxp,
-                          dw_gate_up=self.dw_gate_up, dw_down=self.dw_down)]
+                          dw_gate_up=self.dw_gate_up, dw_down=self.dw_down, activation=self.act)]
         if self.Hs:
             # the shared experts see every token with weight 1: their dxp is dx
             sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
                                   self.s_gu, self.s_h, dyp=dy, dgu=self.s_dgu, dxp=self.dx,
-                                  dw_gate_up=self.s_dw_gate_up, dw_down=self.s_dw_down))
+                                  dw_gate_up=self.s_dw_gate_up, dw_down=self.s_dw_down,
+                                  activation=self.act))
         if self.ws_ffn is None:
             self.ws_ffn_bytes = B.moe_grouped_ffn_bwd_workspace_size(sets, dt, d)
             self.ws_ffn = torch.empty(self.ws_ffn_bytes, dtype=torch.uint8, device=self.device)

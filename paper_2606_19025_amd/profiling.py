@@ -32,7 +32,7 @@ CSRC = os.path.join(PKG, "csrc")
 CALIBRATION_BYTES = 1 << 30  # the plain copy bench.py makes for the counter scale
 
 GEMM_KINDS = ["gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd", "gemm_dx_bwd", "gemm_dwd",
-              "gemm_dwgu"]
+              "gemm_dwgu", "gemm_up_fwd", "gemm_dh_bwd"]
 
 # kernel symbol (demangled, as rocprofv3 prints it) -> timing name
 _SYMBOLS = [

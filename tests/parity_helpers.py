@@ -55,7 +55,7 @@ def make_layer(inp, gate="softmax_topk", inv_tau=1.0):
     hs = cfg.get("n_shared", 0) * cfg.get("Hs", 0) if inp.get("shared_gate_up") is not None else 0
     return ResidentMoELayer(inp["x"].shape[0], cfg["d"], cfg["E"], cfg["k"], cfg["H"],
                             inp["resident"], dtype=torch_dtype(cfg), n_shared_hidden=hs,
-                            gate=gate, inv_tau=inv_tau)
+                            gate=gate, inv_tau=inv_tau, expert=cfg.get("expert", "swiglu"))
 
 
 def run_gpu_layer(inp, gate="softmax_topk", inv_tau=1.0, layer=None):

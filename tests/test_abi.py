@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert B.moe_abi_version() == 1
+    assert B.moe_abi_version() == 2
 
 
 def test_workspace_sizes_are_host_only(lib):

@@ -20,21 +20,22 @@ pytestmark = pytest.mark.gpu
 
 
 def synth_inputs(T, d, E, k, H, resident, dtype="bf16", seed=0, shared_hidden=0, bias=False,
-                 wscale=0.02):
+                 wscale=0.02, expert="swiglu"):
     g = np.random.default_rng(seed)
     rnd = I.bf16_round if dtype == "bf16" else (lambda a: np.asarray(a, np.float32))
     resident = sorted(resident)
     Er = len(resident)
     res = np.zeros(E, np.uint8)
     res[resident] = 1
+    r1 = 2 if expert == "swiglu" else 1
     nrm = lambda *s: g.standard_normal(s, dtype=np.float32)
     inp = dict(cfg=dict(T=T, d=d, E=E, k=k, H=H, E_r=Er, resident=resident, dtype=dtype,
-                        n_shared=1 if shared_hidden else 0, Hs=shared_hidden),
+                        n_shared=1 if shared_hidden else 0, Hs=shared_hidden, expert=expert),
                x=rnd(nrm(T, d)), dy=rnd(nrm(T, d)), w_router=rnd(nrm(E, d) * wscale * 4),
-               w_gate_up=rnd(nrm(Er, 2 * H, d) * wscale), w_down=rnd(nrm(Er, d, H) * wscale),
+               w_gate_up=rnd(nrm(Er, r1 * H, d) * wscale), w_down=rnd(nrm(Er, d, H) * wscale),
                resident=res, router_bias=(nrm(E) * 0.1) if bias else None)
     if shared_hidden:
-        inp["shared_gate_up"] = rnd(nrm(1, 2 * shared_hidden, d) * wscale)
+        inp["shared_gate_up"] = rnd(nrm(1, r1 * shared_hidden, d) * wscale)
         inp["shared_down"] = rnd(nrm(1, d, shared_hidden) * wscale)
     return inp
 
@@ -62,14 +63,21 @@ CASES = {
     "many-experts": (300, 64, 256, 8, 64, list(range(0, 256, 5)), "bf16", 0, False, "softmax_topk", 1.0),
     "multi-tile-groups": (1500, 256, 4, 2, 256, [0, 1, 3], "bf16", 0, False, "softmax_topk", 1.0),
     "k12-wave-select": (200, 64, 32, 12, 64, list(range(0, 32, 3)), "bf16", 0, False, "softmax_topk", 1.0),
+    # the paper's own sigma-MoE layer: sigmoid gates and the SiLU expert
+    "silu-sigmoid": (777, 128, 16, 4, 192, list(range(8)), "bf16", 0, False, "sigmoid", 1.0),
+    "silu-shared-f32": (300, 72, 8, 2, 64, [1, 4, 5], "f32", 64, True, "sigmoid", 0.9),
+    "silu-multi-tile": (2048, 1024, 16, 2, 2816, list(range(0, 16, 2)), "bf16", 1408, False,
+                        "softmax_topk", 1.0),
 }
+EXPERT = {"silu-sigmoid": "silu", "silu-shared-f32": "silu", "silu-multi-tile": "silu"}
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
 def test_layer_parity_edge_cases(gpu_lib, name):
     T, d, E, k, H, res, dt, hs, bias, gate, tau = CASES[name]
     say(f"[edge] {name}")
-    inp = synth_inputs(T, d, E, k, H, res, dt, seed=len(name), shared_hidden=hs, bias=bias)
+    inp = synth_inputs(T, d, E, k, H, res, dt, seed=len(name), shared_hidden=hs, bias=bias,
+                       expert=EXPERT.get(name, "swiglu"))
     if not res:  # no resident expert: weights of zero experts
         inp["w_gate_up"] = np.zeros((0, 2 * H, d), np.float32)
         inp["w_down"] = np.zeros((0, d, H), np.float32)
