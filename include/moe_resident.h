@@ -316,6 +316,57 @@ int moe_replica_mean(const float* local, const float* const* peers, int n_peers,
                      float* out, hipStream_t stream);
 
 /*
+ * Expert placement and migration (Alg. 1; Sec. 3.3 "Expert placement modes").
+ * Every expert lives on exactly O_e of M workers and every worker holds
+ * N_le = O_e N_e / M distinct experts; random placement redraws the map every
+ * T rounds, after which a worker fetches the experts new to it (Delta_in),
+ * keeps the optimiser state of the others and restarts that of the new ones
+ * with a learning-rate warm-up (Sec. 3.4).
+ *
+ * moe_gen_placement (host only): sets [M, N_le] (host) receives each worker's
+ * sorted expert ids.  The (expert, replica) slots in expert order are dealt
+ * to the workers in turn - expert e on workers (e O_e + j) mod M, j < O_e -
+ * after relabelling experts by expert_perm and workers by worker_perm (host
+ * permutations of 0..N_e-1 and 0..M-1; NULL = identity, the fixed placement;
+ * random placement passes uniformly drawn ones).  MOE_ERR_ARG unless
+ * 1 <= O_e <= M, M divides N_e O_e and the permutations are valid.
+ */
+int moe_gen_placement(int N_e, int O_e, int M, const int32_t* expert_perm,
+                      const int32_t* worker_perm, int32_t* sets);
+
+/*
+ * moe_migration_map (host only): for slot i of the new resident set (strictly
+ * ascending ids), map[i] = the slot of the same expert in the previous set,
+ * or -1 if the expert is new to the worker.
+ */
+int moe_migration_map(const int32_t* prev_set, int n_prev, const int32_t* new_set, int n_new,
+                      int32_t* map);
+
+/*
+ * moe_gather_expert_rows: dst[r, :] = src[src_row[r], :] for src_row[r] >= 0,
+ * zeros for src_row[r] = -1; rows of row_len fp32 values (row_len % 4 == 0),
+ * src_row a HOST array of n_rows <= 256 entries.  The migration step: weights
+ * of the new set from the global store, optimiser state from the previous
+ * local layout by moe_migration_map (-1 = restarted).  dst must not overlap
+ * src.
+ */
+int moe_gather_expert_rows(const float* src, const int32_t* src_row, int n_rows, size_t row_len,
+                           float* dst, hipStream_t stream);
+
+/*
+ * moe_adamw_step_rows: moe_adamw_step over n_rows experts of row_len
+ * parameters each, with expert r at its own step count steps[r] >= 1 (its
+ * steps since its state was (re)started) and learning rate lr[r] (the
+ * warm-up of reassigned experts); steps and lr are HOST arrays.  Row r is
+ * bit-for-bit moe_adamw_step(row r, steps[r], lr[r]).  Rows that share
+ * (step, lr) are updated by one launch.
+ */
+int moe_adamw_step_rows(float* theta, const float* grad, float* m, float* v, int n_rows,
+                        size_t row_len, const int* steps, const float* lr, float beta1,
+                        float beta2, float eps, float weight_decay, void* theta_bf16,
+                        hipStream_t stream);
+
+/*
  * Measurement support for benchmarks and profilers (not part of the layer).
  * moe_timing_enable(capacity > 0) creates a pool of 2*capacity HIP events on
  * the current device and from then on brackets every kernel this library

@@ -574,3 +574,53 @@ def replica_mean(local, peers):
     for p in peers:
         acc = (acc + np.asarray(p, f32)).astype(f32)
     return (acc * (f32(1.0) / f32(len(peers) + 1))).astype(f32)
+
+
+# --------------------------------------------------------------------------
+# Expert placement and migration (Alg. 1)
+# --------------------------------------------------------------------------
+#
+# Sec. 3.3 ("Expert placement modes", Alg. 1): every expert of a layer lives on
+# exactly O_e of the M workers and every worker holds N_le = O_e N_e / M
+# distinct experts.  Fixed placement maps experts to workers once; random
+# placement redraws the map every T rounds.  After a redraw a worker fetches
+# the experts new to it (Delta_in = S^t \ S^(t-1)), keeps the optimiser state
+# of the experts it already held, and restarts the state of the new ones with a
+# learning-rate warm-up applied only to them (Sec. 3.4, "Outer optimization").
+#
+# Reading (the paper gives the constraints, not a construction): the
+# placement lays the N_e O_e (expert, replica) slots out in expert order and
+# deals them to the workers in turn, so expert e sits on workers
+# (e O_e + j) mod M, j < O_e; random placement relabels the experts and the
+# workers by two uniformly drawn permutations (passed in, so that both
+# implementations see the same draw).
+
+def gen_placement(N_e, O_e, M, expert_perm=None, worker_perm=None):
+    """[M, N_le] int array: row m = the sorted expert ids worker m holds."""
+    if not (1 <= O_e <= M) or (N_e * O_e) % M:
+        raise ValueError("need 1 <= O_e <= M and M | N_e O_e")
+    N_le = N_e * O_e // M
+    ep = np.arange(N_e) if expert_perm is None else np.asarray(expert_perm)
+    wp = np.arange(M) if worker_perm is None else np.asarray(worker_perm)
+    sets = [[] for _ in range(M)]
+    for e in range(N_e):
+        for j in range(O_e):
+            sets[int(wp[(e * O_e + j) % M])].append(int(ep[e]))
+    out = np.array([sorted(s) for s in sets], dtype=np.int64).reshape(M, N_le)
+    return out
+
+
+def migration_map(prev_set, new_set):
+    """For each slot of the new resident set (ascending expert id): the slot
+    the expert had in the previous set (its state is kept), or -1 if the
+    expert is new to the worker (Delta_in: fetched, state restarted)."""
+    prev = {int(e): i for i, e in enumerate(prev_set)}
+    return np.array([prev.get(int(e), -1) for e in new_set], dtype=np.int64)
+
+
+def warmup_scale(steps_since_reset, warmup_steps):
+    """Learning-rate factor of a reassigned expert: linear warm-up over
+    warmup_steps local steps (reading: the paper does not give the shape)."""
+    if warmup_steps <= 0:
+        return 1.0
+    return min(1.0, float(steps_since_reset) / float(warmup_steps))

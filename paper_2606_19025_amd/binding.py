@@ -26,6 +26,7 @@ EXPORTS = [
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
     "moe_expert_delta", "moe_adamw_step", "moe_outer_nesterov", "moe_replica_mean",
+    "moe_gen_placement", "moe_migration_map", "moe_gather_expert_rows", "moe_adamw_step_rows",
     "moe_timing_enable", "moe_timing_collect",
 ]
 
@@ -65,6 +66,10 @@ _SIGS = {
     "moe_adamw_step": (_I, [_P, _P, _P, _P, _Z, _I, _F, _F, _F, _F, _F, _P, _P]),
     "moe_outer_nesterov": (_I, [_P, _P, _P, _P, _Z, _F, _F, _P, _P]),
     "moe_replica_mean": (_I, [_P, C.POINTER(C.c_void_p), _I, _Z, _P, _P]),
+    "moe_gen_placement": (_I, [_I, _I, _I, _P, _P, _P]),
+    "moe_migration_map": (_I, [_P, _I, _P, _I, _P]),
+    "moe_gather_expert_rows": (_I, [_P, _P, _I, _Z, _P, _P]),
+    "moe_adamw_step_rows": (_I, [_P, _P, _P, _P, _I, _Z, _P, _P, _F, _F, _F, _F, _P, _P]),
     "moe_timing_enable": (_I, [_I]),
     "moe_timing_collect": (_I, [_P, _I, C.POINTER(C.c_int)]),
 }
@@ -264,6 +269,51 @@ def moe_replica_mean(local, peers, n_peers, n, out, stream=None):
         if n_peers else None
     return _check("moe_replica_mean", lib().moe_replica_mean(
         _ptr(local), arr, n_peers, n, _ptr(out), _stream(stream)))
+
+
+def _host_i32(a):
+    import numpy as np
+    arr = np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+    return arr, arr.ctypes.data_as(C.c_void_p)
+
+
+def moe_gen_placement(N_e, O_e, M, expert_perm=None, worker_perm=None):
+    """[M, N_le] numpy int32 array of each worker's sorted expert ids."""
+    import numpy as np
+    N_le = N_e * O_e // M if M else 0
+    out = np.zeros((max(M, 1), max(N_le, 1)), np.int32)
+    ep = _host_i32(expert_perm) if expert_perm is not None else (None, None)
+    wp = _host_i32(worker_perm) if worker_perm is not None else (None, None)
+    _check("moe_gen_placement", lib().moe_gen_placement(
+        N_e, O_e, M, ep[1], wp[1], out.ctypes.data_as(C.c_void_p)))
+    return out[:M, :N_le]
+
+
+def moe_migration_map(prev_set, new_set):
+    import numpy as np
+    prev, pp = _host_i32(prev_set)
+    new, npp = _host_i32(new_set)
+    out = np.zeros(max(len(new), 1), np.int32)
+    _check("moe_migration_map", lib().moe_migration_map(
+        pp, len(prev), npp, len(new), out.ctypes.data_as(C.c_void_p)))
+    return out[:len(new)]
+
+
+def moe_gather_expert_rows(src, src_row, n_rows, row_len, dst, stream=None):
+    rows, rp = _host_i32(src_row)
+    return _check("moe_gather_expert_rows", lib().moe_gather_expert_rows(
+        _ptr(src), rp, n_rows, row_len, _ptr(dst), _stream(stream)))
+
+
+def moe_adamw_step_rows(theta, grad, m, v, n_rows, row_len, steps, lr, beta1=0.9, beta2=0.95,
+                        eps=1e-8, weight_decay=0.0, theta_bf16=None, stream=None):
+    import numpy as np
+    st, sp = _host_i32(steps)
+    lr_arr = np.ascontiguousarray(np.asarray(lr, np.float32))
+    return _check("moe_adamw_step_rows", lib().moe_adamw_step_rows(
+        _ptr(theta), _ptr(grad), _ptr(m), _ptr(v), n_rows, row_len, sp,
+        lr_arr.ctypes.data_as(C.c_void_p), beta1, beta2, eps, weight_decay, _ptr(theta_bf16),
+        _stream(stream)))
 
 
 def moe_timing_enable(capacity):

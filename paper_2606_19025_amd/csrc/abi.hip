@@ -450,4 +450,86 @@ int moe_replica_mean(const float* local, const float* const* peers, int n_peers,
                     "moe_replica_mean");
 }
 
+static bool is_permutation(const int32_t* p, int n) {
+  if (!p) return true;
+  std::vector<char> seen(n, 0);
+  for (int i = 0; i < n; ++i) {
+    if (p[i] < 0 || p[i] >= n || seen[p[i]]) return false;
+    seen[p[i]] = 1;
+  }
+  return true;
+}
+
+int moe_gen_placement(int N_e, int O_e, int M, const int32_t* expert_perm,
+                      const int32_t* worker_perm, int32_t* sets) {
+  REQUIRE(sets, "sets must not be NULL");
+  REQUIRE(N_e >= 1 && M >= 1 && O_e >= 1 && O_e <= M,
+          "need N_e >= 1 and 1 <= O_e <= M (N_e = %d, O_e = %d, M = %d)", N_e, O_e, M);
+  REQUIRE(((long)N_e * O_e) % M == 0, "M = %d must divide N_e O_e = %ld", M, (long)N_e * O_e);
+  REQUIRE(is_permutation(expert_perm, N_e), "expert_perm is not a permutation of 0..N_e-1");
+  REQUIRE(is_permutation(worker_perm, M), "worker_perm is not a permutation of 0..M-1");
+  REQUIRE(moe::gen_placement(N_e, O_e, M, expert_perm, worker_perm, sets), "placement failed");
+  return MOE_OK;
+}
+
+int moe_migration_map(const int32_t* prev_set, int n_prev, const int32_t* new_set, int n_new,
+                      int32_t* map) {
+  REQUIRE(n_prev >= 0 && n_new >= 0, "set sizes must be >= 0");
+  REQUIRE((n_prev == 0 || prev_set) && (n_new == 0 || (new_set && map)),
+          "sets and map must not be NULL");
+  for (int i = 0; i < n_new; ++i) {
+    REQUIRE(i == 0 || new_set[i] > new_set[i - 1], "new_set must be strictly ascending");
+    map[i] = -1;
+    for (int j = 0; j < n_prev; ++j)
+      if (prev_set[j] == new_set[i]) map[i] = j;
+  }
+  return MOE_OK;
+}
+
+int moe_gather_expert_rows(const float* src, const int32_t* src_row, int n_rows, size_t row_len,
+                           float* dst, hipStream_t stream) {
+  REQUIRE(n_rows >= 0 && n_rows <= 256, "n_rows = %d must be in [0, 256]", n_rows);
+  REQUIRE(n_rows == 0 || row_len == 0 || (src_row && dst), "src_row and dst must not be NULL");
+  bool any_src = false;
+  for (int r = 0; r < n_rows; ++r) any_src = any_src || src_row[r] >= 0;
+  REQUIRE(!any_src || src, "src must not be NULL when a row is copied");
+  SUPPORT((!src || aligned16(src)) && (!dst || aligned16(dst)) && row_len % 4 == 0,
+          "src and dst must be 16-byte aligned and row_len a multiple of 4");
+  return hip_status(moe::launch_gather_expert_rows(src, src_row, n_rows, row_len, dst, stream),
+                    "moe_gather_expert_rows");
+}
+
+int moe_adamw_step_rows(float* theta, const float* grad, float* m, float* v, int n_rows,
+                        size_t row_len, const int* steps, const float* lr, float beta1,
+                        float beta2, float eps, float weight_decay, void* theta_bf16,
+                        hipStream_t stream) {
+  REQUIRE(n_rows >= 0 && (n_rows == 0 || (steps && lr)), "steps and lr must not be NULL");
+  REQUIRE(n_rows == 0 || row_len == 0 || (theta && grad && m && v),
+          "theta, grad, m and v must not be NULL");
+  REQUIRE(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f && eps >= 0.f,
+          "betas must lie in [0, 1) and eps must be >= 0");
+  SUPPORT(row_len % 4 == 0, "row_len must be a multiple of 4");
+  for (const void* p : {(const void*)theta, (const void*)grad, (const void*)m, (const void*)v,
+                        (const void*)theta_bf16})
+    SUPPORT(p == nullptr || aligned16(p), "arrays must be 16-byte aligned");
+  for (int r = 0; r < n_rows; ++r) REQUIRE(steps[r] >= 1, "steps[%d] = %d must be >= 1", r, steps[r]);
+  // one launch per run of rows that share (step, lr)
+  for (int r0 = 0; r0 < n_rows;) {
+    int r1 = r0 + 1;
+    while (r1 < n_rows && steps[r1] == steps[r0] && lr[r1] == lr[r0]) ++r1;
+    const float c1 = (float)(1.0 - std::pow((double)beta1, (double)steps[r0]));
+    const float c2 = (float)(1.0 - std::pow((double)beta2, (double)steps[r0]));
+    REQUIRE(c1 > 0.f && c2 > 0.f, "bias corrections must be positive");
+    const size_t o = (size_t)r0 * row_len, n = (size_t)(r1 - r0) * row_len;
+    void* lp = theta_bf16 ? static_cast<uint16_t*>(theta_bf16) + o : nullptr;  // bf16 elements
+    const int st = hip_status(moe::launch_adamw(theta + o, grad + o, m + o, v + o, n, lr[r0],
+                                                beta1, beta2, eps, weight_decay, c1, c2, lp,
+                                                stream),
+                              "moe_adamw_step_rows");
+    if (st != MOE_OK) return st;
+    r0 = r1;
+  }
+  return MOE_OK;
+}
+
 }  // extern "C"

@@ -94,3 +94,39 @@ def test_adamw_full_size_resident_experts(gpu_lib):
     torch.cuda.synchronize()
     assert np.array_equal(th_d.cpu().numpy(), th)
     assert np.array_equal(m_d.cpu().numpy(), m) and np.array_equal(v_d.cpu().numpy(), v)
+
+
+def test_gather_expert_rows_bit_exact(gpu_lib):
+    """Migration copy: rows from a store by index, zeros for -1."""
+    g = np.random.default_rng(51)
+    row_len, n_store = 3 * 64 * 128 + 4, 12
+    store = g.standard_normal((n_store, row_len)).astype(np.float32)
+    idx = np.array([3, -1, 0, 11, -1, 7], np.int32)
+    out = torch.empty(len(idx), row_len, device="cuda")
+    B.moe_gather_expert_rows(dev(store), idx, len(idx), row_len, out)
+    torch.cuda.synchronize()
+    ref = np.where(idx[:, None] >= 0, store[np.maximum(idx, 0)], 0.0).astype(np.float32)
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_adamw_rows_with_own_steps_and_rates(gpu_lib):
+    """Per-expert step counts and learning rates (restarted experts with a
+    warm-up) give row by row the single-array AdamW of the oracle."""
+    g = np.random.default_rng(52)
+    n_rows, row_len = 6, 4100
+    theta = (g.standard_normal((n_rows, row_len)) * 0.02).astype(np.float32)
+    m0 = (g.standard_normal((n_rows, row_len)) * 1e-3).astype(np.float32)
+    v0 = (g.standard_normal((n_rows, row_len)) ** 2 * 1e-6).astype(np.float32)
+    grad = (g.standard_normal((n_rows, row_len)) * 0.1).astype(np.float32)
+    steps = np.array([7, 7, 1, 1, 7, 3], np.int32)
+    lr = np.array([1e-3, 1e-3, 1e-3 * O.warmup_scale(1, 4), 1e-3 * O.warmup_scale(1, 4), 1e-3,
+                   1e-3 * O.warmup_scale(3, 4)], np.float32)
+    th_d, m_d, v_d = dev(theta), dev(m0), dev(v0)
+    lp = torch.empty(n_rows, row_len, dtype=torch.bfloat16, device="cuda")
+    B.moe_adamw_step_rows(th_d, dev(grad), m_d, v_d, n_rows, row_len, steps, lr, theta_bf16=lp)
+    torch.cuda.synchronize()
+    for r in range(n_rows):
+        th, m, v = O.adamw_step(theta[r], grad[r], m0[r], v0[r], int(steps[r]), float(lr[r]))
+        assert np.array_equal(th_d[r].cpu().numpy(), th), r
+        assert np.array_equal(m_d[r].cpu().numpy(), m) and np.array_equal(v_d[r].cpu().numpy(), v)
+        assert np.array_equal(lp[r].float().cpu().numpy(), rne_bf16(th))

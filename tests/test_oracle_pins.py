@@ -560,3 +560,41 @@ def test_silu_expert_single_resident_layer_is_dense_mlp():
         a = x[t] @ inp["w_gate_up"][e].T
         ref = (a / (1 + np.exp(-a))) @ inp["w_down"][e].T
         assert np.allclose(f["y"][t], f["w"][t, 0] * ref, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- placement (Alg. 1)
+
+@pytest.mark.parametrize("N_e,O_e,M", [(64, 4, 8), (16, 1, 4), (16, 4, 4), (12, 2, 8), (8, 3, 6)])
+def test_placement_meets_the_constraints(N_e, O_e, M):
+    """Every expert on exactly O_e workers, every worker N_le distinct experts,
+    for the fixed map and for random relabelings."""
+    g = np.random.default_rng(N_e * 100 + O_e * 10 + M)
+    for draw in range(4):
+        ep = None if draw == 0 else g.permutation(N_e)
+        wp = None if draw == 0 else g.permutation(M)
+        P = O.gen_placement(N_e, O_e, M, ep, wp)
+        N_le = N_e * O_e // M
+        assert P.shape == (M, N_le)
+        for m in range(M):
+            assert len(set(P[m])) == N_le and list(P[m]) == sorted(P[m])
+        hosts = np.zeros(N_e, int)
+        for m in range(M):
+            hosts[P[m]] += 1
+        assert np.all(hosts == O_e)
+
+
+def test_placement_limits():
+    # O_e = M: full replication; O_e = 1: a disjoint partition
+    assert np.array_equal(O.gen_placement(8, 4, 4), np.tile(np.arange(8), (4, 1)))
+    P = O.gen_placement(16, 1, 4)
+    assert sorted(P.reshape(-1).tolist()) == list(range(16))
+    with pytest.raises(ValueError):
+        O.gen_placement(10, 3, 4)  # 4 does not divide 30
+
+
+def test_migration_map_and_warmup():
+    prev, new = np.array([1, 4, 6, 9]), np.array([0, 4, 9, 11])
+    assert list(O.migration_map(prev, new)) == [-1, 1, 3, -1]
+    assert list(O.migration_map(new, new)) == [0, 1, 2, 3]  # fixed placement keeps all state
+    assert O.warmup_scale(0, 10) == 0.0 and O.warmup_scale(5, 10) == 0.5
+    assert O.warmup_scale(25, 10) == 1.0 and O.warmup_scale(3, 0) == 1.0
