@@ -343,15 +343,20 @@ int moe_migration_map(const int32_t* prev_set, int n_prev, const int32_t* new_se
                       int32_t* map);
 
 /*
- * moe_gather_expert_rows: dst[r, :] = src[src_row[r], :] for src_row[r] >= 0,
- * zeros for src_row[r] = -1; rows of row_len fp32 values (row_len % 4 == 0),
- * src_row a HOST array of n_rows <= 256 entries.  The migration step: weights
- * of the new set from the global store, optimiser state from the previous
- * local layout by moe_migration_map (-1 = restarted).  dst must not overlap
- * src.
+ * moe_copy_expert_rows: dst[dst_row[r], :] = src[src_row[r], :] for
+ * src_row[r] >= 0, zeros for src_row[r] = -1, r < n_rows <= 256; rows of
+ * row_len fp32 values (row_len % 4 == 0); src_row and dst_row are HOST arrays
+ * (dst_row NULL = 0..n_rows-1, otherwise distinct).  The migration step:
+ * weights of the new set from the global store, optimiser state from the
+ * previous local layout by moe_migration_map (-1 = restarted), and the
+ * resident rows back into the global store.  The rows read must not overlap
+ * the rows written.  dst_bf16 (may be NULL) receives the written rows rounded
+ * to bf16 (nearest even) in dst's layout: the working copy of migrated
+ * weights.
  */
-int moe_gather_expert_rows(const float* src, const int32_t* src_row, int n_rows, size_t row_len,
-                           float* dst, hipStream_t stream);
+int moe_copy_expert_rows(const float* src, const int32_t* src_row, float* dst,
+                         const int32_t* dst_row, int n_rows, size_t row_len, void* dst_bf16,
+                         hipStream_t stream);
 
 /*
  * moe_adamw_step_rows: moe_adamw_step over n_rows experts of row_len

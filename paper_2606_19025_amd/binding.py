@@ -26,7 +26,7 @@ EXPORTS = [
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
     "moe_expert_delta", "moe_adamw_step", "moe_outer_nesterov", "moe_replica_mean",
-    "moe_gen_placement", "moe_migration_map", "moe_gather_expert_rows", "moe_adamw_step_rows",
+    "moe_gen_placement", "moe_migration_map", "moe_copy_expert_rows", "moe_adamw_step_rows",
     "moe_timing_enable", "moe_timing_collect",
 ]
 
@@ -68,7 +68,7 @@ _SIGS = {
     "moe_replica_mean": (_I, [_P, C.POINTER(C.c_void_p), _I, _Z, _P, _P]),
     "moe_gen_placement": (_I, [_I, _I, _I, _P, _P, _P]),
     "moe_migration_map": (_I, [_P, _I, _P, _I, _P]),
-    "moe_gather_expert_rows": (_I, [_P, _P, _I, _Z, _P, _P]),
+    "moe_copy_expert_rows": (_I, [_P, _P, _P, _P, _I, _Z, _P, _P]),
     "moe_adamw_step_rows": (_I, [_P, _P, _P, _P, _I, _Z, _P, _P, _F, _F, _F, _F, _P, _P]),
     "moe_timing_enable": (_I, [_I]),
     "moe_timing_collect": (_I, [_P, _I, C.POINTER(C.c_int)]),
@@ -299,10 +299,12 @@ def moe_migration_map(prev_set, new_set):
     return out[:len(new)]
 
 
-def moe_gather_expert_rows(src, src_row, n_rows, row_len, dst, stream=None):
+def moe_copy_expert_rows(src, src_row, dst, n_rows, row_len, dst_row=None, dst_bf16=None,
+                         stream=None):
     rows, rp = _host_i32(src_row)
-    return _check("moe_gather_expert_rows", lib().moe_gather_expert_rows(
-        _ptr(src), rp, n_rows, row_len, _ptr(dst), _stream(stream)))
+    drows, dp = _host_i32(dst_row) if dst_row is not None else (None, None)
+    return _check("moe_copy_expert_rows", lib().moe_copy_expert_rows(
+        _ptr(src), rp, _ptr(dst), dp, n_rows, row_len, _ptr(dst_bf16), _stream(stream)))
 
 
 def moe_adamw_step_rows(theta, grad, m, v, n_rows, row_len, steps, lr, beta1=0.9, beta2=0.95,

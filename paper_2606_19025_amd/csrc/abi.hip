@@ -486,17 +486,27 @@ int moe_migration_map(const int32_t* prev_set, int n_prev, const int32_t* new_se
   return MOE_OK;
 }
 
-int moe_gather_expert_rows(const float* src, const int32_t* src_row, int n_rows, size_t row_len,
-                           float* dst, hipStream_t stream) {
+int moe_copy_expert_rows(const float* src, const int32_t* src_row, float* dst,
+                         const int32_t* dst_row, int n_rows, size_t row_len, void* dst_bf16,
+                         hipStream_t stream) {
   REQUIRE(n_rows >= 0 && n_rows <= 256, "n_rows = %d must be in [0, 256]", n_rows);
   REQUIRE(n_rows == 0 || row_len == 0 || (src_row && dst), "src_row and dst must not be NULL");
   bool any_src = false;
-  for (int r = 0; r < n_rows; ++r) any_src = any_src || src_row[r] >= 0;
+  for (int r = 0; r < n_rows; ++r) {
+    any_src = any_src || src_row[r] >= 0;
+    REQUIRE(src_row[r] >= -1, "src_row[%d] = %d must be >= -1", r, src_row[r]);
+    if (dst_row) {
+      REQUIRE(dst_row[r] >= 0, "dst_row[%d] = %d must be >= 0", r, dst_row[r]);
+      for (int q = 0; q < r; ++q) REQUIRE(dst_row[q] != dst_row[r], "dst_row repeats %d", dst_row[r]);
+    }
+  }
   REQUIRE(!any_src || src, "src must not be NULL when a row is copied");
-  SUPPORT((!src || aligned16(src)) && (!dst || aligned16(dst)) && row_len % 4 == 0,
-          "src and dst must be 16-byte aligned and row_len a multiple of 4");
-  return hip_status(moe::launch_gather_expert_rows(src, src_row, n_rows, row_len, dst, stream),
-                    "moe_gather_expert_rows");
+  SUPPORT((!src || aligned16(src)) && (!dst || aligned16(dst)) &&
+              (!dst_bf16 || aligned16(dst_bf16)) && row_len % 4 == 0,
+          "src, dst and dst_bf16 must be 16-byte aligned and row_len a multiple of 4");
+  return hip_status(moe::launch_copy_expert_rows(src, src_row, dst, dst_row, n_rows, row_len,
+                                                 dst_bf16, stream),
+                    "moe_copy_expert_rows");
 }
 
 int moe_adamw_step_rows(float* theta, const float* grad, float* m, float* v, int n_rows,

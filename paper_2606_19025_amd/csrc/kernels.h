@@ -60,11 +60,12 @@ hipError_t launch_replica_mean(const float* local, const float* const* peers, in
                                size_t n, float* out, hipStream_t s);
 
 // Placement and migration (placement.hip).  gen_placement: false when the
-// constraints cannot be met.  launch_gather_expert_rows: src_row is a host
-// array of n_rows <= 256 entries.
+// constraints cannot be met.  launch_copy_expert_rows: src_row / dst_row are
+// host arrays of n_rows <= 256 entries (dst_row NULL = 0..n_rows-1).
 bool gen_placement(int N_e, int O_e, int M, const int32_t* expert_perm,
                    const int32_t* worker_perm, int32_t* sets);
-hipError_t launch_gather_expert_rows(const float* src, const int32_t* src_row, int n_rows,
-                                     size_t row_len, float* dst, hipStream_t s);
+hipError_t launch_copy_expert_rows(const float* src, const int32_t* src_row, float* dst,
+                                   const int32_t* dst_row, int n_rows, size_t row_len,
+                                   void* dst_bf16, hipStream_t s);
 
 }  // namespace moe

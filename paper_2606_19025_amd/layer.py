@@ -30,6 +30,7 @@ class ResidentMoELayer:
         res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
         assert res.numel() == self.E
         self.E_r = int(res.sum().item())
+        self.E_full = self.E
         self.partitioned = bool(partitioned)
         # expert form: SwiGLU ([Wg; Wu] and [G | U], 2H wide) or the paper's
         # SiLU expert (W1 and A, H wide)
@@ -96,6 +97,16 @@ class ResidentMoELayer:
             self.s_dgu = e(T, r1 * Hs)
             self.s_dw_gate_up = e(1, r1 * Hs, d, dt=f32)
             self.s_dw_down = e(1, d, Hs, dt=f32)
+
+    def set_resident(self, resident):
+        """Switch to another resident set of the same size (a new placement,
+        Alg. 1).  The caller migrates the expert weights and optimiser state;
+        with a partitioned router it also passes the new router rows."""
+        res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
+        if res.numel() != self.E_full or int(res.sum().item()) != self.E_r:
+            raise ValueError("a new resident set must hold the same number of experts")
+        if not self.partitioned:
+            self.resident.copy_(res.to(self.resident.device))
 
     # ------------------------------------------------------------------ forward
     def forward(self, x, w_router, w_gate_up, w_down, router_bias=None, shared_gate_up=None,

@@ -56,7 +56,7 @@ _SYMBOLS = [
     (r"adamw_kernel", lambda m: "adamw_step"),
     (r"outer_nesterov_kernel", lambda m: "outer_nesterov"),
     (r"replica_mean_kernel", lambda m: "replica_mean"),
-    (r"gather_expert_rows_kernel", lambda m: "gather_expert_rows"),
+    (r"copy_expert_rows_kernel", lambda m: "copy_expert_rows"),
 ]
 
 # timing name prefix -> source file that holds the kernel
@@ -64,7 +64,7 @@ _SOURCES = [("gemm_", "gemm.hip"), ("splitk_", "gemm.hip"), ("route_", "route.hi
             ("combine_", "dispatch.hip"), ("unpermute", "dispatch.hip"),
             ("expert_delta", "dispatch.hip"), ("adamw", "optim.hip"), ("outer_", "optim.hip"),
             ("replica_", "optim.hip"),
-            ("gather_expert_rows", "placement.hip")]
+            ("copy_expert_rows", "placement.hip")]
 
 
 def timing_name(symbol: str) -> str | None:

@@ -96,17 +96,26 @@ def test_adamw_full_size_resident_experts(gpu_lib):
     assert np.array_equal(m_d.cpu().numpy(), m) and np.array_equal(v_d.cpu().numpy(), v)
 
 
-def test_gather_expert_rows_bit_exact(gpu_lib):
-    """Migration copy: rows from a store by index, zeros for -1."""
+def test_copy_expert_rows_bit_exact(gpu_lib):
+    """Migration copies: rows from a store by index (zeros for -1) into
+    consecutive rows, and rows back into chosen rows of a store."""
     g = np.random.default_rng(51)
     row_len, n_store = 3 * 64 * 128 + 4, 12
     store = g.standard_normal((n_store, row_len)).astype(np.float32)
     idx = np.array([3, -1, 0, 11, -1, 7], np.int32)
     out = torch.empty(len(idx), row_len, device="cuda")
-    B.moe_gather_expert_rows(dev(store), idx, len(idx), row_len, out)
+    B.moe_copy_expert_rows(dev(store), idx, out, len(idx), row_len)
     torch.cuda.synchronize()
     ref = np.where(idx[:, None] >= 0, store[np.maximum(idx, 0)], 0.0).astype(np.float32)
     assert np.array_equal(out.cpu().numpy(), ref)
+    back = dev(store)
+    rows = np.array([0, 2, 3, 5], np.int32)
+    dst_rows = np.array([9, 1, 4, 6], np.int32)
+    B.moe_copy_expert_rows(out, rows, back, len(rows), row_len, dst_row=dst_rows)
+    torch.cuda.synchronize()
+    ref_back = store.copy()
+    ref_back[dst_rows] = ref[rows]
+    assert np.array_equal(back.cpu().numpy(), ref_back)
 
 
 def test_adamw_rows_with_own_steps_and_rates(gpu_lib):
