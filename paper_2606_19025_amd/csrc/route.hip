@@ -110,23 +110,46 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
         for (int q = 0; q < 4; ++q)
           acc[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u][q], bv[u][eb][q], acc[eb], 0, 0, 0);
   }
-  // deterministic cross-wave sum: wave 0 stores, waves 1.. add in order
-  for (int wv = 0; wv < RT_WAVES; ++wv) {
-    if (wave == wv) {
+  // deterministic cross-wave sum (wave order).  Up to 64 experts: every wave
+  // stores its partial tile, then each thread adds its entries' RT_WAVES
+  // partials; wider expert sets add wave by wave into zl.
+  if constexpr (NEB <= 2) {
+    __shared__ float part[RT_WAVES][RT_TOK * NEB * 32];
 #pragma unroll
-      for (int eb = 0; eb < NEB; ++eb) {
+    for (int eb = 0; eb < NEB; ++eb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = (r >> 2) * 8 + half * 4 + (r & 3);
-          const int e = eb * 32 + row;
-          if (e < a.E) {
-            float* p = zl + i * ldz + e;
-            *p = (wv == 0) ? acc[eb][r] : *p + acc[eb][r];
-          }
-        }
+      for (int r = 0; r < 16; ++r) {
+        const int i = (r >> 2) * 8 + half * 4 + (r & 3);
+        part[wave][i * NEB * 32 + eb * 32 + row] = acc[eb][r];
       }
     }
     __syncthreads();
+    for (int p = threadIdx.x; p < RT_TOK * NEB * 32; p += RT_THREADS) {
+      const int i = p / (NEB * 32), e = p % (NEB * 32);
+      float v = part[0][p];
+#pragma unroll
+      for (int wv = 1; wv < RT_WAVES; ++wv) v += part[wv][p];
+      if (e < a.E) zl[i * ldz + e] = v;
+    }
+    __syncthreads();
+  } else {
+    for (int wv = 0; wv < RT_WAVES; ++wv) {
+      if (wave == wv) {
+#pragma unroll
+        for (int eb = 0; eb < NEB; ++eb) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = (r >> 2) * 8 + half * 4 + (r & 3);
+            const int e = eb * 32 + row;
+            if (e < a.E) {
+              float* p = zl + i * ldz + e;
+              *p = (wv == 0) ? acc[eb][r] : *p + acc[eb][r];
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
   }
 }
 
