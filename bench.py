@@ -62,6 +62,11 @@ def parse():
                     help="time whole training steps: fwd + bwd + AdamW on the resident and shared "
                          "experts every step, and at the round cadence the delta average and the "
                          "outer Nesterov step")
+    ap.add_argument("--placement", choices=["fixed", "random"], default="fixed",
+                    help="with --optimizer: random placement (Alg. 1) redraws the worker's "
+                         "resident set every --reshuffle-every rounds and migrates weights and "
+                         "optimiser state")
+    ap.add_argument("--reshuffle-every", type=int, default=1)
     ap.add_argument("--expert", choices=["swiglu", "silu"], default="swiglu",
                     help="expert form: SwiGLU (the workloads') or the paper's SiLU expert "
                          "(its first weight is the first H rows of the SwiGLU draw)")
@@ -257,8 +262,62 @@ def main():
             opt.update(s_master=s_lp.float(), s_m=torch.zeros(n_s, device="cuda"),
                        s_v=torch.zeros(n_s, device="cuda"), s_lp=s_lp)
         opt["lp"] = w_lp
+        opt["rows"] = [(0, n_gu, r1 * H * d), (n_gu, n_params, d * H)]  # (begin, end, row_len)
+        opt["steps"] = np.zeros(Er, np.int64)
+        if args.placement == "random":
+            # the server's store of every expert (weights and outer momentum),
+            # a placement with replica groups of n_peers + 1 workers, and
+            # spare state buffers for the migration copies
+            O_e = len(peers) + 1
+            M_w = E * O_e // Er
+            gs = np.random.default_rng([args.seed, 99])
+            store = [torch.from_numpy(gs.standard_normal((E, row), dtype=np.float32)
+                                      * np.float32(0.02)).cuda() for _, _, row in opt["rows"]]
+            opt.update(O_e=O_e, M=M_w, rng=gs, store_th=store,
+                       store_mom=[torch.zeros_like(t) for t in store], m2=torch.empty_like(th1),
+                       v2=torch.empty_like(th1), set=np.array(inp["cfg"]["resident"]),
+                       copy_bytes=0.0)
+            log(f"[bench] random placement: {E} experts on {M_w} workers, O_e = {O_e}, "
+                f"reshuffle every {args.reshuffle_every} round(s)")
         log(f"[bench] optimiser state: AdamW m, v and outer momentum of {n_params / 1e6:.1f} M "
             f"expert params" + (f" (+{(r1 + 1) * Hs * d / 1e6:.1f} M shared)" if Hs else ""))
+
+    def part_view(t, p):
+        b, e, row = opt["rows"][p]
+        return t[b:e].view(Er, row)
+
+    def copy_rows(src, src_row, dst, dst_row=None, bf16=None):
+        """Expert-row copy (Alg. 1 migration); counts its algorithmic bytes."""
+        rl = src.shape[1] if src is not None else dst.shape[1]
+        n_src = int(np.sum(np.asarray(src_row) >= 0))
+        opt["copy_bytes"] += rl * (4 * n_src + 4 * len(src_row) + (2 * len(src_row) if bf16 is not None else 0))
+        B.moe_copy_expert_rows(src, src_row, dst, len(src_row), rl, dst_row=dst_row, dst_bf16=bf16)
+
+    def reshuffle():
+        """Round boundary of random placement for this worker: resident rows
+        back to the store, a new placement, migration of weights, outer
+        momentum and AdamW state, restart of the new experts' step counts."""
+        o = opt
+        local = np.arange(Er)
+        for p in range(2):
+            copy_rows(part_view(th1, p), local, o["store_th"][p], o["set"])
+            copy_rows(part_view(o["mom"], p), local, o["store_mom"][p], o["set"])
+        ep, wp = o["rng"].permutation(E), o["rng"].permutation(o["M"])
+        new = B.moe_gen_placement(E, o["O_e"], o["M"], ep, wp)[0]
+        mig = B.moe_migration_map(o["set"], new)
+        for p in range(2):
+            b, e, _ = o["rows"][p]
+            copy_rows(o["store_th"][p], new, part_view(th1, p), bf16=o["lp"][b:e])
+            copy_rows(o["store_th"][p], new, part_view(th0, p))
+            copy_rows(o["store_mom"][p], new, part_view(o["mom"], p))
+            copy_rows(part_view(o["m"], p), mig, part_view(o["m2"], p))
+            copy_rows(part_view(o["v"], p), mig, part_view(o["v2"], p))
+        o["m"], o["m2"], o["v"], o["v2"] = o["m2"], o["m"], o["v2"], o["v"]
+        o["steps"] = np.where(mig >= 0, o["steps"][np.maximum(mig, 0)], 0)
+        mask = np.zeros(E, np.uint8)
+        mask[new] = 1
+        L.set_resident(mask)
+        o["set"] = new
 
     def optimizer_step(i):
         o = opt
@@ -267,11 +326,21 @@ def main():
         # local AdamW on the resident experts (gradients of the layer's last
         # backward), writing the bf16 weights in the same pass
         n_gu = o["gu"].numel()
-        B.moe_adamw_step(o["gu"], L.dw_gate_up, o["m"][:n_gu], o["v"][:n_gu], n_gu, o["t"], lr,
-                         theta_bf16=o["lp"][:n_gu])
-        n_dn = o["down"].numel()
-        B.moe_adamw_step(o["down"], L.dw_down, o["m"][n_gu:], o["v"][n_gu:], n_dn, o["t"], lr,
-                         theta_bf16=o["lp"][n_gu:])
+        if args.placement == "fixed":
+            B.moe_adamw_step(o["gu"], L.dw_gate_up, o["m"][:n_gu], o["v"][:n_gu], n_gu, o["t"],
+                             lr, theta_bf16=o["lp"][:n_gu])
+            n_dn = o["down"].numel()
+            B.moe_adamw_step(o["down"], L.dw_down, o["m"][n_gu:], o["v"][n_gu:], n_dn, o["t"],
+                             lr, theta_bf16=o["lp"][n_gu:])
+        else:
+            # every expert at its own step count; restarted experts warm up
+            # over one round
+            o["steps"] = o["steps"] + 1
+            lrs = np.array([lr * min(1.0, t / args.round_every) for t in o["steps"]], np.float32)
+            for p, grad in ((0, L.dw_gate_up), (1, L.dw_down)):
+                b, e, row = o["rows"][p]
+                B.moe_adamw_step_rows(th1[b:e], grad, o["m"][b:e], o["v"][b:e], Er, row,
+                                      o["steps"], lrs, theta_bf16=o["lp"][b:e])
         if Hs:
             n_sg = r1 * Hs * d
             B.moe_adamw_step(o["s_master"][:n_sg], L.s_dw_gate_up, o["s_m"][:n_sg],
@@ -283,6 +352,8 @@ def main():
             # outer Nesterov step, every replica restarts from its result
             expert_delta(th0, th1, peers, delta_avg=avg)
             B.moe_outer_nesterov(th0, th1, avg, o["mom"], n_params, 0.7, 0.9, theta_bf16=o["lp"])
+            if args.placement == "random" and ((i + 1) // args.round_every) % args.reshuffle_every == 0:
+                reshuffle()
 
     def step(i):
         L.forward(x, wr, wgu, wd, bias, sgu, sd)
@@ -328,10 +399,14 @@ def main():
     kernels = {}
     roofline = None
     if not args.no_kernel_timing:
-        B.moe_timing_enable(64 * (args.steps + 2))
+        B.moe_timing_enable(256 * (args.steps + 2))
         torch.cuda.synchronize()
+        if opt is not None and args.placement == "random":
+            opt["copy_bytes"] = 0.0
         for i in range(args.steps):
             step(i)
+        if opt is not None and args.placement == "random":
+            opt["copy_bytes_timed"] = opt["copy_bytes"]
         torch.cuda.synchronize()
         stats = B.moe_timing_collect()
         B.moe_timing_enable(0)
@@ -340,6 +415,9 @@ def main():
         work["expert_delta"] = ("byte", 4.0 * n_params * (3 + len(peers)))
         if opt is not None:
             work.update(optimizer_work(n_params + (r1 + 1) * Hs * d, n_params, len(peers)))
+            if args.placement == "random":
+                # bytes of the timed pass's migration copies, spread per step
+                work["copy_expert_rows"] = ("byte", opt["copy_bytes_timed"] / args.steps)
         per_round = ("expert_delta", "outer_nesterov", "replica_mean")
         for name, (launches, tot, mn, mx) in stats.items():
             kind, per_step = work.get(name, ("byte", 0.0))
@@ -355,7 +433,7 @@ def main():
             ent.update(launches=launches, avg_us=1e3 * tot / max(launches, 1),
                        ms_per_step=tot / args.steps)
             kernels[name] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in ent.items()}
-        dom = max((nm for nm in kernels if nm not in per_round),
+        dom = max((nm for nm in kernels if nm not in per_round + ("copy_expert_rows",)),
                   key=lambda nm: kernels[nm]["ms_per_step"])
         kd = kernels[dom]
         kind, per_step = work[dom]
@@ -416,6 +494,7 @@ def main():
                    "H": H, "shared_hidden": Hs, "round_every": args.round_every,
                    "executed_routes": n, "skip_fraction": round(1 - n / (T * k), 4),
                    "optimizer": "adamw+outer-nesterov" if opt is not None else None,
+                   "placement": args.placement if opt is not None else None,
                    "expert": args.expert},
         "roofline": roofline,
         "cpu_baseline": cpu,
