@@ -949,7 +949,8 @@ hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
 }
 
 // dst[i] = (accumulate ? dst[i] : 0) + p_0[i] + p_1[i] + ... (fixed order),
-// n % 4 == 0, all 16-byte aligned
+// n % 4 == 0, all 16-byte aligned; the partials are read once and dst is
+// written once, both past the caches (nontemporal)
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const float* parts,
                                                             int n_parts, size_t n,
                                                             int accumulate) {
@@ -958,12 +959,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const fl
     f32x4_t q[4];  // all loads first (n_parts <= 4)
 #pragma unroll
     for (int p = 0; p < 4; ++p)
-      if (p < n_parts) q[p] = reinterpret_cast<const f32x4_t*>(parts + p * n)[i];
+      if (p < n_parts) q[p] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(parts + p * n) + i);
     f32x4_t v = accumulate ? reinterpret_cast<const f32x4_t*>(dst)[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int p = 0; p < 4; ++p)
       if (p < n_parts) v += q[p];
-    reinterpret_cast<f32x4_t*>(dst)[i] = v;
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t*>(dst) + i);
   }
 }
 
