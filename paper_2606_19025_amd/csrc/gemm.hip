@@ -18,8 +18,9 @@
 // device-side offsets; no host read-back), the last two ragged in K.
 //
 // bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulation in a persistent
-// kernel with 256 x 256 block tiles fed from a 4-stage LDS ring by
-// global -> LDS DMA (details at gemm_bf16_kernel).  One launch per GEMM kind
+// kernel with 256 x 256 block tiles (128 x 256 for the kinds with a heavy
+// epilogue) fed from an LDS ring by global -> LDS DMA (details at
+// gemm_bf16_kernel and Cfg).  One launch per GEMM kind
 // covers up to two expert sets (routed and shared experts).
 // fp32: a plain 64x64 SIMT tile (4x4 outputs per thread) with the same
 // epilogues; used for fp32 layers.
@@ -254,7 +255,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // Persistent: one 256-thread block per CU loops over output tiles.  Block tile
 // 256 x 256; the 4 waves form a 2 x 2 grid and each owns a 128 x 128 sub-tile
 // = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane), so
-// LDS read traffic stays at 8 KB per 16 MFMAs.
+// LDS read traffic stays at 8 KB per 16 MFMAs.  (Half-height 128 x 256 tiles,
+// see Cfg: two blocks per CU, 64 x 128 per wave = 2 x 4 MFMA tiles, a ring of
+// 3 stages of 24 KB; the numbers below are those of the full tile.)
 //
 // Operands stream through a ring of NS = 4 LDS stages of one k-step (32) each
 // (32 KB per stage, 128 KB in all), filled with 16-byte global -> LDS DMA.
@@ -269,16 +272,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // last one is loaded again into an unused stage) so vmcnt counting is uniform;
 // the ring is drained (vmcnt(0)) before a block moves to its next tile.
 //
-// Tile order (see tile_decode): bands of GROUP_M m-tiles.  Workgroups are
-// dealt to the 8 XCDs round-robin by id, so block b works on tiles of the
-// ranges assigned to XCD b % 8 (an eighth of each set's tiles): the 32 tiles
-// an XCD runs at a time form a GROUP_M x 8 rectangle whose operand panels its
-// L2 serves.  Output tiles end in an epilogue: bf16 results are staged
-// through the drained ring so global accesses are whole 16-byte chunks;
-// fp32 weight gradients are stored (or added) straight from the
-// accumulators.
+// Tile order (see tile_decode): bands of GROUP_M m-tiles (4 full or 8
+// half-height ones).  Workgroups are dealt to the 8 XCDs round-robin by id,
+// so block b works on tiles of the ranges assigned to XCD b % 8 (an eighth of
+// each set's tiles): the 32 (64 half-height) tiles an XCD runs at a time form
+// a GROUP_M x 8 rectangle whose operand panels its L2 serves.  Output tiles
+// end in an epilogue: bf16 results are staged through the drained ring so
+// global accesses are whole 16-byte chunks; fp32 weight gradients are stored
+// (or added) straight from the accumulators.
 //
-// LDS layouts (per operand and stage, 16 KB):
+// LDS layouts (per operand and stage, 16 KB; 8 KB for the A operand of a
+// half-height tile):
 //  k-contiguous operand (rows = M or N index): row r holds 32 k = 64 B; its
 //    16-byte chunk kc sits at chunk position kc ^ ((r >> 2) & 3), so the 16
 //    lanes of one ds_read_b128 pass (16 consecutive rows, same kc) hit 16
@@ -294,14 +298,39 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // stored); k-rows past a group's last row (ragged K) are loaded from a
 // 16-byte zero block, so they contribute exactly 0.
 
-constexpr int GT = 256;                     // block tile (M and N)
+constexpr int GT = 256;                     // block tile width (N), and height (M) of full tiles
 constexpr int GK = 32;                      // k-step
-constexpr int NS = 4;                       // LDS ring stages
-constexpr int OP_BYTES = GT * GK * 2;       // one operand of one stage: 16 KB
-constexpr int STAGE_BYTES = 2 * OP_BYTES;   // A then B
-constexpr int LDS_BYTES = NS * STAGE_BYTES;
-constexpr int DMA_PER_OP = OP_BYTES / 1024 / 4;  // 16-byte DMA loads per wave per operand
 constexpr int N_XCD = 8;
+
+// Tile configuration per kind.  The kinds with a heavy elementwise epilogue
+// (GU_FWD / UP_FWD write two outputs per element, DHH_BWD / DH_BWD read one or
+// two more) use 128 x 256 tiles, two blocks per CU, each wave 64 x 128 (128
+// accumulators): a ragged expert group then pads at most 127 rows instead of
+// 255 and the epilogue per tile is half as long.  Measured on the
+// fine-grained workload: GU_FWD 7 % and DHH_BWD 6 % faster than with
+// 256 x 256 tiles; DOWN_FWD and DX_BWD (light epilogues, longer K) were 7 %
+// and 3 % slower that way, so they and the K-ragged kinds keep 256 x 256
+// tiles with one block per CU.
+template <int KIND>
+struct Cfg {
+  static constexpr bool HALF = KIND == GU_FWD || KIND == DHH_BWD || KIND == UP_FWD || KIND == DH_BWD;
+  static constexpr int BM = HALF ? 128 : 256;      // block tile rows
+  static constexpr int WM = BM / 2;                // wave sub-tile rows
+  static constexpr int MI = WM / 32;               // 32-row MFMA tiles per wave
+  static constexpr int NS = HALF ? 3 : 4;          // LDS ring stages
+  static constexpr int A_BYTES = BM * GK * 2;      // A operand of one stage
+  static constexpr int B_BYTES = GT * GK * 2;      // B operand of one stage
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int DMA_A = A_BYTES / 4096;     // 16-byte DMA loads per wave and k-step
+  static constexpr int DMA_B = B_BYTES / 4096;
+  static constexpr int DMA_N = DMA_A + DMA_B;
+  static constexpr int DMA_MAX = DMA_A > DMA_B ? DMA_A : DMA_B;
+  static constexpr int EPI_WAVE = WM * 256;        // epilogue staging per wave
+  static constexpr int GROUP = HALF ? 8 : 4;       // m-tiles per band
+  static constexpr int OCC = HALF ? 2 : 1;         // blocks per CU
+  static_assert(4 * EPI_WAVE <= LDS, "epilogue staging exceeds the ring");
+};
 
 
 __device__ const u32x4_t kZero16 = {0u, 0u, 0u, 0u};
@@ -330,17 +359,18 @@ DEVI void load_to_lds(const bf16_t* g, char* lds_base) {
 // lane l writes chunk position l%4 of row 16q + l/4.  m/n-contiguous operand:
 // load q covers k-rows 2q, 2q+1 (512 B each), lane l writes 16-byte slot l%32
 // of row 2q + l/32.
+template <int N>
 struct DmaPtrs {
-  const bf16_t* p[DMA_PER_OP];
+  const bf16_t* p[N];
 };
 
 DEVI int kc_swz(int r) { return (r >> 2) & 3; }
 
-template <class RowPtr>
-DEVI void dma_kc_init(DmaPtrs& d, const RowPtr& row_ptr, int w) {
+template <int N, class RowPtr>
+DEVI void dma_kc_init(DmaPtrs<N>& d, const RowPtr& row_ptr, int w) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int i = 0; i < DMA_PER_OP; ++i) {
+  for (int i = 0; i < N; ++i) {
     const int row = (i * 4 + w) * 16 + (lane >> 2);
     d.p[i] = row_ptr(row) + ((lane & 3) ^ kc_swz(row)) * 8;
   }
@@ -352,10 +382,10 @@ DEVI int mn_col(int row) {
   return (((ps >> 1) ^ (2 * (row & 3))) * 16) + (ps & 1) * 8;
 }
 
-template <class ElemPtr>
-DEVI void dma_mn_init(DmaPtrs& d, const ElemPtr& elem_ptr, int w, int k0) {
+template <int N, class ElemPtr>
+DEVI void dma_mn_init(DmaPtrs<N>& d, const ElemPtr& elem_ptr, int w, int k0) {
 #pragma unroll
-  for (int i = 0; i < DMA_PER_OP; ++i) {
+  for (int i = 0; i < N; ++i) {
     const int row = mn_row(i, w);
     d.p[i] = elem_ptr(k0 + row, mn_col(row));
   }
@@ -404,8 +434,6 @@ DEVI void load4(const bf16_t* p, float* v) {
 // differ in key bit 3, so the SwiGLU reads (8 chunks of two rows per 16
 // lanes) fall on disjoint chunks.  A 16-byte chunk c is read back from chunk
 // c ^ (key >> 1), halves swapped when the key is odd.
-constexpr int EPI_WAVE_BYTES = 128 * 256;
-static_assert(4 * EPI_WAVE_BYTES <= LDS_BYTES, "epilogue staging exceeds the ring");
 
 DEVI int epi_key(int r) { return ((r & 1) << 3) | ((r >> 1) & 7) | (r & 16); }
 
@@ -434,28 +462,29 @@ DEVI float silu_fast(float g) { return g * sigmoid_fast(g); }
 // m varies fastest, then n, so any 32 consecutive tiles cover a GROUP_M x
 // (32 / GROUP_M) rectangle and share GROUP_M A panels and 32 / GROUP_M B
 // panels in L2.
-constexpr int GROUP_M = 4;
 
 template <int KIND>
 DEVI int m_tile_count(const GemmArgs& a) {
+  constexpr int BM = Cfg<KIND>::BM;
   if constexpr (Kind<KIND>::MRAG) {
     int tiles = 0;
     int b = clamp_row(a.offsets[0], a.cap);
     for (int g = 0; g < a.n_groups; ++g) {
       int e = clamp_row(a.offsets[g + 1], a.cap);
       if (e < b) e = b;
-      tiles += (e - b + GT - 1) / GT;
+      tiles += (e - b + BM - 1) / BM;
       b = e;
     }
     return tiles;
   } else {
-    return a.n_groups * max(1, a.ksplit) * ((a.M + GT - 1) / GT);
+    return a.n_groups * max(1, a.ksplit) * ((a.M + BM - 1) / BM);
   }
 }
 
 template <int KIND>
 DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& tl,
                       int& tile_n) {
+  constexpr int BM = Cfg<KIND>::BM, GROUP_M = Cfg<KIND>::GROUP;
   const int band = t / (GROUP_M * n_tiles);
   const int first_m = band * GROUP_M;
   const int band_m = min(GROUP_M, m_tiles - first_m);
@@ -469,11 +498,11 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
     for (int g = 0; g < a.n_groups; ++g) {
       int e = clamp_row(a.offsets[g + 1], a.cap);
       if (e < b) e = b;
-      const int tiles = (e - b + GT - 1) / GT;
+      const int tiles = (e - b + BM - 1) / BM;
       if (mt < tiles) {
         tl.g = g;
-        tl.row0 = b + mt * GT;
-        tl.rows = min(GT, e - tl.row0);
+        tl.row0 = b + mt * BM;
+        tl.rows = min(BM, e - tl.row0);
         tl.m0 = 0;
         tl.split = 0;
         return;
@@ -486,11 +515,11 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
     // (group, split part, m-tile); part p of a group of rows [b, e) is
     // [b + len p / S, b + len (p + 1) / S)
     const int S = max(1, a.ksplit);
-    const int mt_per_g = (a.M + GT - 1) / GT;
+    const int mt_per_g = (a.M + BM - 1) / BM;
     const int gs = q / mt_per_g;
     tl.g = gs / S;
     tl.split = gs % S;
-    tl.m0 = (q % mt_per_g) * GT;
+    tl.m0 = (q % mt_per_g) * BM;
     const int b = clamp_row(a.offsets[tl.g], a.cap);
     int e = clamp_row(a.offsets[tl.g + 1], a.cap);
     if (e < b) e = b;
@@ -517,9 +546,11 @@ struct GemmLaunch {
 };
 
 template <int KIND>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
+__global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaunch L) {
   using K_ = Kind<KIND>;
-  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
+  using C_ = Cfg<KIND>;
+  constexpr int MI = C_::MI, WM = C_::WM, NS = C_::NS;
+  __shared__ __attribute__((aligned(1024))) char lds[C_::LDS];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
@@ -532,6 +563,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
   if (L.zero && blockIdx.x == 0 && threadIdx.x < L.n_zero) L.zero[threadIdx.x] = 0;
+
   const int nt0 = col_tiles<KIND>(L.s0);
   const int mt0 = m_tile_count<KIND>(L.s0);
   const int tot0 = mt0 * nt0;
@@ -608,7 +640,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
     // DMA addresses at k-step 0 (k-contiguous operands advance by GK
     // elements, m/n-contiguous ones by GK rows per k-step) and of the ragged
     // tail k-step
-    DmaPtrs da, db, ta, tb;
+    DmaPtrs<C_::DMA_A> da, ta;
+    DmaPtrs<C_::DMA_B> db, tb;
     if constexpr (K_::A_KC) dma_kc_init(da, a_row, wave); else dma_mn_init(da, a_elem, wave, 0);
     if constexpr (K_::B_KC) dma_kc_init(db, b_row, wave); else dma_mn_init(db, b_elem, wave, 0);
     if constexpr (!K_::MRAG) {
@@ -618,50 +651,59 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
     const long a_step = K_::A_KC ? GK : (long)GK * a.lda;
     const long b_step = K_::B_KC ? GK : (long)GK * a.ldb;
 
-    // DMA load i (of DMA_PER_OP) of both operands for k-step ks into stage st
+    // DMA load i of each operand (A: i < DMA_A, B: i < DMA_B) for k-step ks
+    // into stage st
     auto dma = [&](int ks, int st, int i) {
-      char* la = lds + st * STAGE_BYTES;
+      char* la = lds + st * C_::STAGE;
       const bool tail = !K_::MRAG && ks >= n_full;
-      const bf16_t* pa = da.p[i] + ks * a_step;
-      const bf16_t* pb = db.p[i] + ks * b_step;
-      if constexpr (!K_::MRAG) {
-        pa = tail ? ta.p[i] : pa;
-        pb = tail ? tb.p[i] : pb;
+      if (i < C_::DMA_A) {
+        const int ia = i < C_::DMA_A ? i : 0;
+        const bf16_t* pa = da.p[ia] + ks * a_step;
+        if constexpr (!K_::MRAG) pa = tail ? ta.p[ia] : pa;
+        load_to_lds(pa, la + (i * 4 + wave) * 1024);
       }
-      load_to_lds(pa, la + (i * 4 + wave) * 1024);
-      load_to_lds(pb, la + OP_BYTES + (i * 4 + wave) * 1024);
+      if (i < C_::DMA_B) {
+        const int ib = i < C_::DMA_B ? i : 0;
+        const bf16_t* pb = db.p[ib] + ks * b_step;
+        if constexpr (!K_::MRAG) pb = tail ? tb.p[ib] : pb;
+        load_to_lds(pb, la + C_::A_BYTES + (i * 4 + wave) * 1024);
+      }
     };
 
     auto read_frag = [&](const char* stage, int s, int idx, bf16x8_t* af, bf16x8_t* bfr) {
-      // idx 0..3: A fragment idx; 4..7: B fragment idx-4
-      if (idx < 4) {
-        af[idx] = K_::A_KC ? frag_kc(stage, wm * 128 + idx * 32, s)
-                           : frag_mn(stage, wm * 128 + idx * 32, s);
+      // idx 0..MI-1: A fragment idx; MI..MI+3: B fragment idx-MI
+      if (idx < MI) {
+        af[idx] = K_::A_KC ? frag_kc(stage, wm * WM + idx * 32, s)
+                           : frag_mn(stage, wm * WM + idx * 32, s);
       } else {
-        const int f = idx - 4;
-        const char* lb = stage + OP_BYTES;
+        const int f = idx - MI;
+        const char* lb = stage + C_::A_BYTES;
         bfr[f] = K_::B_KC ? frag_kc(lb, wn * 128 + f * 32, s) : frag_mn(lb, wn * 128 + f * 32, s);
       }
     };
 
-    f32x16_t acc[4][4];
+    f32x16_t acc[MI][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
 
-    // One k16-step: 16 MFMAs on (A_c, B_c) in 8 chunks of two; chunk q also
-    // reads fragment q of the next k16-step (from stage_n) into (A_n, B_n)
-    // and, for q < DMA_PER_OP when dma_ks >= 0, issues DMA load q of k-step
-    // dma_ks into stage dma_st.  sched_barrier(0) fences keep this order, so
-    // each fragment read has a whole k16-step to land and the compiler's waits
-    // fall at the first use in the next k16-step.
+    // One k16-step: 4 MI MFMAs on (A_c, B_c) in 2 MI chunks of two; chunk q
+    // also reads fragments [q NF / NQ, (q + 1) NF / NQ) of the next k16-step
+    // (NF = MI + 4 of them, from stage_n) into (A_n, B_n) and, for
+    // q < DMA_MAX when dma_ks >= 0, issues DMA load q of k-step dma_ks into
+    // stage dma_st.  sched_barrier(0) fences keep this order, so each fragment
+    // read has a whole k16-step to land and the compiler's waits fall at the
+    // first use in the next k16-step.
+    constexpr int NQ = 2 * MI, NF = MI + 4;
+    static_assert(C_::DMA_MAX <= NQ, "DMA loads per k-step exceed the chunks");
     auto kstep = [&](const bf16x8_t* A_c, const bf16x8_t* B_c, const char* stage_n, int s_n,
                      bf16x8_t* A_n, bf16x8_t* B_n, int dma_ks, int dma_st) {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (dma_ks >= 0 && q < DMA_PER_OP) dma(dma_ks, dma_st, q);
-        read_frag(stage_n, s_n, q, A_n, B_n);
+      for (int q = 0; q < NQ; ++q) {
+        if (dma_ks >= 0 && q < C_::DMA_MAX) dma(dma_ks, dma_st, q);
+#pragma unroll
+        for (int f = q * NF / NQ; f < (q + 1) * NF / NQ; ++f) read_frag(stage_n, s_n, f, A_n, B_n);
         const int i = q >> 1, j0 = 2 * (q & 1);
         acc[i][j0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_c[j0], A_c[i], acc[i][j0], 0, 0, 0);
         acc[i][j0 + 1] =
@@ -670,25 +712,25 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
       }
     };
 
-    bf16x8_t af0[4], bf0[4], af1[4], bf1[4];
+    bf16x8_t af0[MI], bf0[4], af1[MI], bf1[4];
     if (nk > 0) {
 #pragma unroll
       for (int p = 0; p < NS; ++p)
 #pragma unroll
-        for (int i = 0; i < DMA_PER_OP; ++i) dma(min(p, nk - 1), p, i);
-      // own DMA of k-step 0 done (3 k-steps' loads may stay in flight)
-      WAIT_VMCNT(2 * DMA_PER_OP * (NS - 1));
+        for (int i = 0; i < C_::DMA_MAX; ++i) dma(min(p, nk - 1), p, i);
+      // own DMA of k-step 0 done (NS - 1 k-steps' loads may stay in flight)
+      WAIT_VMCNT(C_::DMA_N * (NS - 1));
       __syncthreads();
 #pragma unroll
-      for (int q = 0; q < 8; ++q) read_frag(lds, 0, q, af0, bf0);
+      for (int q = 0; q < NF; ++q) read_frag(lds, 0, q, af0, bf0);
     }
     for (int kt = 0; kt < nk; ++kt) {
       const int st = kt % NS;
-      const char* stage = lds + st * STAGE_BYTES;
-      const char* stage_next = lds + ((kt + 1) % NS) * STAGE_BYTES;
+      const char* stage = lds + st * C_::STAGE;
+      const char* stage_next = lds + ((kt + 1) % NS) * C_::STAGE;
       kstep(af0, bf0, stage, 1, af1, bf1, -1, 0);
       WAIT_LGKMCNT(0);
-      WAIT_VMCNT(2 * DMA_PER_OP * (NS - 2));
+      WAIT_VMCNT(C_::DMA_N * (NS - 2));
       __syncthreads();
       kstep(af1, bf1, stage_next, 0, af0, bf0, min(kt + NS, nk - 1), st);
     }
@@ -702,8 +744,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
       const int r_in = lane & 31;
       const int c_in = 4 * (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + i * 32 + r_in;
+      for (int i = 0; i < MI; ++i) {
+        const int row = wm * WM + i * 32 + r_in;
         if (tl.m0 + row >= a.M) continue;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -723,11 +765,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
       // bf16 outputs go through LDS so that every global access is a whole
       // 16-byte chunk and a wave instruction covers 256 contiguous bytes of a
       // row (4 rows) instead of 16 bytes of 32 rows.  Each wave transposes its
-      // 128x128 sub-tile in a private 32 KB region (the drained ring).
+      // 128x128 sub-tile in a private 32 KB region (the drained ring).  The
+      // outputs (and the G/U that the dSwiGLU epilogue reads) are touched
+      // once here, so they go past the caches (nontemporal: measured 2-4 %
+      // faster for DHH_BWD, DX_BWD and DOWN_FWD; the fp32 weight gradients
+      // below are not, they were 1.4-1.7x slower that way).
       __syncthreads();  // every wave is done with the ring
-      char* reg = lds + wave * EPI_WAVE_BYTES;
+      char* reg = lds + wave * C_::EPI_WAVE;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -738,7 +784,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
                     acc[i][j][4 * q + 3]);
           }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region is wave-private
-      const int row_lim = tl.rows - wm * 128;  // rows of this wave's sub-tile to store
+      const int row_lim = tl.rows - wm * WM;  // rows of this wave's sub-tile to store
       if constexpr (KIND == GU_FWD) {
         // region row: [G h0..31 | U h0..31 | G h32..63 | U h32..63] of the
         // wave's 64 hidden units; lane -> (row, 8 hidden units)
@@ -748,7 +794,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
         bf16_t* hh = static_cast<bf16_t*>(a.out2);
         if (h < a.H) {
 #pragma unroll 4
-          for (int it = 0; it < 16; ++it) {
+          for (int it = 0; it < WM / 8; ++it) {
             const int row = it * 8 + (lane >> 3);
             if (row >= row_lim) break;
             const bf16x8_t G = epi_get(reg, row, cg);
@@ -756,10 +802,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
             bf16x8_t Hv;
 #pragma unroll
             for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)(silu_fast((float)G[e]) * (float)U[e]);
-            const size_t m = (size_t)(tl.row0 + wm * 128 + row);
-            *reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + h) = G;
-            *reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + a.H + h) = U;
-            *reinterpret_cast<bf16x8_t*>(hh + m * a.H + h) = Hv;
+            const size_t m = (size_t)(tl.row0 + wm * WM + row);
+            __builtin_nontemporal_store(G, reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + h));
+            __builtin_nontemporal_store(U, reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + a.H + h));
+            __builtin_nontemporal_store(Hv, reinterpret_cast<bf16x8_t*>(hh + m * a.H + h));
           }
         }
       } else {
@@ -771,15 +817,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
             // rows are loaded before any store of it
             const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
             bf16_t* dgu = static_cast<bf16_t*>(a.C);
-            for (int it0 = 0; it0 < 32; it0 += 8) {
+            for (int it0 = 0; it0 < WM / 4; it0 += 8) {
               if (it0 * 4 >= row_lim) break;
               bf16x8_t G[8], U[8];
 #pragma unroll
               for (int b = 0; b < 8; ++b) {
                 const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
-                const size_t m = (size_t)(tl.row0 + wm * 128 + row);
-                G[b] = *reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col);
-                U[b] = *reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col);
+                const size_t m = (size_t)(tl.row0 + wm * WM + row);
+                G[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col));
+                U[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col));
               }
 #pragma unroll
               for (int b = 0; b < 8; ++b) {
@@ -794,9 +840,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
                   dU[e] = (bf16_t)(dh * g * s);
                 }
                 if (row < row_lim) {
-                  const size_t m = (size_t)(tl.row0 + wm * 128 + row);
-                  *reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + col) = dG;
-                  *reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + a.H + col) = dU;
+                  const size_t m = (size_t)(tl.row0 + wm * WM + row);
+                  __builtin_nontemporal_store(dG, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + col));
+                  __builtin_nontemporal_store(dU, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + a.H + col));
                 }
               }
             }
@@ -805,14 +851,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
             // store of it
             const bf16_t* Ab = static_cast<const bf16_t*>(a.aux);
             bf16_t* C = static_cast<bf16_t*>(a.C);
-            for (int it0 = 0; it0 < 32; it0 += 8) {
+            for (int it0 = 0; it0 < WM / 4; it0 += 8) {
               if (it0 * 4 >= row_lim) break;
               bf16x8_t Av[8];
 #pragma unroll
               for (int b = 0; b < 8; ++b) {
                 const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
                 Av[b] = *reinterpret_cast<const bf16x8_t*>(
-                    Ab + (size_t)(tl.row0 + wm * 128 + row) * a.H + col);
+                    Ab + (size_t)(tl.row0 + wm * WM + row) * a.H + col);
               }
 #pragma unroll
               for (int b = 0; b < 8; ++b) {
@@ -826,7 +872,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
                   dA[e] = (bf16_t)((float)v[e] * (sg * (1.0f + g * (1.0f - sg))));
                 }
                 if (row < row_lim)
-                  *reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * 128 + row) * a.ldc + col) = dA;
+                  __builtin_nontemporal_store(dA, reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * WM + row) * a.ldc + col));
               }
             }
           } else if constexpr (KIND == UP_FWD) {
@@ -834,25 +880,24 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmLaunch L) {
             bf16_t* C = static_cast<bf16_t*>(a.C);
             bf16_t* hh = static_cast<bf16_t*>(a.out2);
 #pragma unroll 8
-            for (int it = 0; it < 32; ++it) {
+            for (int it = 0; it < WM / 4; ++it) {
               const int row = it * 4 + (lane >> 4);
               if (row >= row_lim) break;
               const bf16x8_t A = epi_get(reg, row, c);
               bf16x8_t Hv;
 #pragma unroll
               for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)silu_fast((float)A[e]);
-              const size_t m = (size_t)(tl.row0 + wm * 128 + row);
-              *reinterpret_cast<bf16x8_t*>(C + m * a.ldc + col) = A;
-              *reinterpret_cast<bf16x8_t*>(hh + m * a.H + col) = Hv;
+              const size_t m = (size_t)(tl.row0 + wm * WM + row);
+              __builtin_nontemporal_store(A, reinterpret_cast<bf16x8_t*>(C + m * a.ldc + col));
+              __builtin_nontemporal_store(Hv, reinterpret_cast<bf16x8_t*>(hh + m * a.H + col));
             }
           } else {  // DOWN_FWD / DX_BWD
             bf16_t* C = static_cast<bf16_t*>(a.C);
 #pragma unroll 8
-            for (int it = 0; it < 32; ++it) {
+            for (int it = 0; it < WM / 4; ++it) {
               const int row = it * 4 + (lane >> 4);
               if (row >= row_lim) break;
-              *reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * 128 + row) * a.ldc + col) =
-                  epi_get(reg, row, c);
+              __builtin_nontemporal_store(epi_get(reg, row, c), reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * WM + row) * a.ldc + col));
             }
           }
         }
@@ -886,9 +931,10 @@ int num_cus() {
 
 template <int KIND>
 long max_tiles(const GemmArgs& a) {
+  constexpr int BM = Cfg<KIND>::BM;
   const long n_tiles = ceil_div((KIND == GU_FWD) ? 2 * a.H : a.N, GT);
-  return Kind<KIND>::MRAG ? (ceil_div(a.cap, GT) + (long)a.n_groups) * n_tiles
-                          : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, GT) * n_tiles;
+  return Kind<KIND>::MRAG ? (ceil_div(a.cap, BM) + (long)a.n_groups) * n_tiles
+                          : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, BM) * n_tiles;
 }
 
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
@@ -903,7 +949,7 @@ template <int KIND>
 hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
                     int* counters = nullptr, int* zero = nullptr, int n_zero = 0) {
   if (bf16) {
-    // persistent: at most one block per CU, a multiple of N_XCD blocks
+    // persistent: at most Cfg::OCC blocks per CU, a multiple of N_XCD blocks
     GemmLaunch L{};
     L.s0 = sets[0];
     L.n_sets = n_sets;
@@ -924,7 +970,7 @@ hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
       if (swap) std::swap(L.s0, L.s1);
     }
     if (tiles == 0 && n_zero == 0) return hipSuccess;
-    long blocks = std::min<long>(num_cus(), std::max<long>(tiles, 1));
+    long blocks = std::min<long>((long)num_cus() * Cfg<KIND>::OCC, std::max<long>(tiles, 1));
     blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
     MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(L));
     return hipGetLastError();
