@@ -15,7 +15,11 @@ Prints ONE JSON line.  Besides the contract fields it carries:
                 algorithmic flops (or bytes) per launch and its average launch
                 duration measured with HIP events in a second pass of the same
                 steps (the library's moe_timing facility);
-  kernels       the same for every kernel of the step;
+  kernels       the same for every kernel of the step (warm: inputs may sit in
+                L2 or the Infinity Cache from the kernel that wrote them);
+  kernels_cold  the HBM-bound kernels again with a 512 MiB read before every
+                library call (``--cold-steps`` steps), so that each call's first
+                kernel reads its inputs from HBM;
   cpu_baseline  the CPU oracle on a bounded token sample of the same workload.
 
     python bench.py [--gpus 1] [--steps 64] [--warmup 10] [--workload 2]
@@ -41,6 +45,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+FLUSH_BYTES = 512 << 20     # twice the 256 MB Infinity Cache
 
 
 def log(*a):
@@ -58,6 +63,9 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=8,
+                    help="steps of the cold per-kernel pass (a 512 MiB read before every "
+                         "library call evicts L2 and the Infinity Cache); 0 skips it")
     ap.add_argument("--optimizer", action="store_true",
                     help="time whole training steps: fwd + bwd + AdamW on the resident and shared "
                          "experts every step, and at the round cadence the delta average and the "
@@ -450,6 +458,43 @@ def main():
                         per_launch=per_step / max(1, kd["launches"] // args.steps),
                         traffic=traffic)
 
+    kernels_cold = {}
+    if not args.no_kernel_timing and args.cold_steps > 0:
+        # cold per-kernel samples: before every library call a read of a
+        # 512 MiB scratch buffer evicts L2 and the 256 MB Infinity Cache, so
+        # each call's first kernel reads its inputs from HBM (later kernels of
+        # the same call read what the earlier ones just wrote).  A read, not a
+        # write, so that the caches hold clean lines and the timed kernel
+        # does not also pay for the write-back of the scratch data.
+        flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+
+        def evict():
+            flush.sum()
+
+        log(f"[bench] cold pass: {args.cold_steps} steps, cache flush before every call")
+        B.moe_timing_enable(256 * (args.cold_steps + 2))
+        torch.cuda.synchronize()
+        for i in range(args.cold_steps):
+            L.forward(x, wr, wgu, wd, bias, sgu, sd, hook=evict)
+            L.backward(dy, x, wr, wgu, wd, sgu, sd, hook=evict)
+            evict()
+            expert_delta(th0, th1, peers, delta_avg=avg)
+        torch.cuda.synchronize()
+        stats = B.moe_timing_collect()
+        B.moe_timing_enable(0)
+        del flush
+        work = algorithmic_work(cfg, n, t_act, s_bytes, args.expert)
+        work["expert_delta"] = ("byte", 4.0 * n_params * (3 + len(peers)))
+        for name, (launches, tot, mn, mx) in stats.items():
+            kind, per_step = work.get(name, ("byte", 0.0))
+            if kind != "byte" or per_step <= 0:
+                continue
+            amount = per_step * args.cold_steps
+            ach = amount / (tot / 1e3) / 1e9 if tot > 0 else 0.0
+            kernels_cold[name] = dict(unit="GB/s", achieved=round(ach, 3), peak=PEAK_HBM_GBS,
+                                      frac=round(ach / PEAK_HBM_GBS, 5), launches=launches,
+                                      avg_us=round(1e3 * tot / max(launches, 1), 3))
+
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import moe_oracle as O
@@ -499,6 +544,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "kernels_cold": kernels_cold,
     }
     print(json.dumps(out), flush=True)
 

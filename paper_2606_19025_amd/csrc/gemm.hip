@@ -256,18 +256,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // 256 x 256; the 4 waves form a 2 x 2 grid and each owns a 128 x 128 sub-tile
 // = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane), so
 // LDS read traffic stays at 8 KB per 16 MFMAs.  (Half-height 128 x 256 tiles,
-// see Cfg: two blocks per CU, 64 x 128 per wave = 2 x 4 MFMA tiles, a ring of
-// 3 stages of 24 KB; the numbers below are those of the full tile.)
+// see Cfg: two blocks per CU, 64 x 128 per wave = 2 x 4 MFMA tiles.)
 //
-// Operands stream through a ring of NS = 4 LDS stages of one k-step (32) each
-// (32 KB per stage, 128 KB in all), filled with 16-byte global -> LDS DMA.
-// The DMA for k-step kt+4 is issued while k-step kt runs, so every load has
-// three k-steps (~100 MFMAs per wave) to land.  Per k-step and wave:
-//   k16-step 0: 16 MFMAs, interleaved with the LDS reads of k16-step 1
-//   wait for own DMA of k-step kt+1 (vmcnt(16) leaves kt+2, kt+3 in flight)
-//   and for the LDS reads, barrier (stage kt+1 complete, stage kt free)
-//   k16-step 1: 16 MFMAs, interleaved with the LDS reads of k-step kt+1's
-//   k16-step 0 and the DMA of k-step kt+4 into stage kt
+// Operands stream through a ring of NS LDS stages of one k-step (GK) each,
+// filled with 16-byte global -> LDS DMA: full tiles NS = 2 stages of GK = 64
+// (64 KB each), half-height tiles NS = 3 stages of GK = 32 (24 KB each).  A
+// k-step is GK / 16 k16-steps; per k-step and wave:
+//   k16-steps 0 .. GK/16 - 2: 16 MFMAs each (8 for half-height tiles),
+//   interleaved with the LDS reads of the next k16-step
+//   wait for own DMA of k-step kt+1 (vmcnt leaves the later k-steps' loads in
+//   flight) and for the LDS reads, barrier (stage kt+1 complete, stage kt
+//   free)
+//   last k16-step: its MFMAs, interleaved with the LDS reads of k-step kt+1's
+//   k16-step 0 and the DMA of k-step kt+NS into stage kt
+// So every load has NS - 1 k-steps less one k16-step (about 48 MFMAs per wave
+// for full tiles) to land.
 // Every k-step issues the same number of DMA loads (past the last k-step the
 // last one is loaded again into an unused stage) so vmcnt counting is uniform;
 // the ring is drained (vmcnt(0)) before a block moves to its next tile.
@@ -281,13 +284,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // global accesses are whole 16-byte chunks; fp32 weight gradients are stored
 // (or added) straight from the accumulators.
 //
-// LDS layouts (per operand and stage, 16 KB; 8 KB for the A operand of a
-// half-height tile):
-//  k-contiguous operand (rows = M or N index): row r holds 32 k = 64 B; its
-//    16-byte chunk kc sits at chunk position kc ^ ((r >> 2) & 3), so the 16
-//    lanes of one ds_read_b128 pass (16 consecutive rows, same kc) hit 16
-//    distinct 16-byte bank groups of the 64-bank LDS.
-//  m/n-contiguous operand (rows = k): row k holds 256 m = 512 B; its 32-byte
+// LDS layouts (per operand and stage):
+//  k-contiguous operand (rows = M or N index): row r holds GK k (2 GK bytes);
+//    its 16-byte chunk kc sits at chunk position kc ^ swz(r), swz(r) =
+//    (r >> 2) & 3 for GK = 32 and (r >> 1) & 7 for GK = 64, so the 16 lanes of
+//    one ds_read_b128 pass (16 consecutive rows, same kc) hit 16 distinct
+//    16-byte bank groups of the 64-bank LDS.
+//  m/n-contiguous operand (rows = k, GK of them): row k holds 256 m = 512 B; its 32-byte
 //    chunk c sits at position c ^ (2 * (k & 3)).  A fragment is two
 //    ds_read_b64_tr_b16: in each 16-lane group, lane j points at (k0 + j/4,
 //    m0 + 4*(j%4)) and lane i receives m0 + i for k0..k0+3.
@@ -299,7 +302,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // 16-byte zero block, so they contribute exactly 0.
 
 constexpr int GT = 256;                     // block tile width (N), and height (M) of full tiles
-constexpr int GK = 32;                      // k-step
 constexpr int N_XCD = 8;
 
 // Tile configuration per kind.  The kinds with a heavy elementwise epilogue
@@ -311,13 +313,21 @@ constexpr int N_XCD = 8;
 // 256 x 256 tiles; DOWN_FWD and DX_BWD (light epilogues, longer K) were 7 %
 // and 3 % slower that way, so they and the K-ragged kinds keep 256 x 256
 // tiles with one block per CU.
+// Full tiles take k-steps of 64 in a ring of two 64 KB stages: every DMA load
+// then fetches whole 128-byte row pieces (half the L2 requests of 64-byte
+// pieces).  Measured against k-steps of 32 in four stages: DOWN_FWD 6 % and
+// DX_BWD 1-2 % faster, the weight-gradient kinds unchanged.  Half-height tiles
+// keep k-steps of 32 (two blocks of three 24 KB stages fill the LDS).
 template <int KIND>
 struct Cfg {
-  static constexpr bool HALF = KIND == GU_FWD || KIND == DHH_BWD || KIND == UP_FWD || KIND == DH_BWD;
+  static constexpr bool HALF =
+      KIND == GU_FWD || KIND == DHH_BWD || KIND == UP_FWD || KIND == DH_BWD;
+  static constexpr int GK = HALF ? 32 : 64;        // k-step
+  static constexpr int KS = GK / 16;               // k16-steps per k-step
   static constexpr int BM = HALF ? 128 : 256;      // block tile rows
   static constexpr int WM = BM / 2;                // wave sub-tile rows
   static constexpr int MI = WM / 32;               // 32-row MFMA tiles per wave
-  static constexpr int NS = HALF ? 3 : 4;          // LDS ring stages
+  static constexpr int NS = HALF ? 3 : (GK == 64 ? 2 : 4);  // LDS ring stages
   static constexpr int A_BYTES = BM * GK * 2;      // A operand of one stage
   static constexpr int B_BYTES = GT * GK * 2;      // B operand of one stage
   static constexpr int STAGE = A_BYTES + B_BYTES;
@@ -355,8 +365,9 @@ DEVI void load_to_lds(const bf16_t* g, char* lds_base) {
 }
 
 // Per-lane global addresses of the DMA loads a wave issues per operand and
-// k-step.  k-contiguous operand: load q = 4i + w covers rows 16q .. 16q+15,
-// lane l writes chunk position l%4 of row 16q + l/4.  m/n-contiguous operand:
+// k-step.  k-contiguous operand with C = GK / 8 chunks per row: load q = 4i + w
+// covers rows (64 / C) q .. (64 / C) (q + 1) - 1, lane l writes chunk position
+// l % C of row (64 / C) q + l / C.  m/n-contiguous operand:
 // load q covers k-rows 2q, 2q+1 (512 B each), lane l writes 16-byte slot l%32
 // of row 2q + l/32.
 template <int N>
@@ -364,15 +375,20 @@ struct DmaPtrs {
   const bf16_t* p[N];
 };
 
-DEVI int kc_swz(int r) { return (r >> 2) & 3; }
+// k-contiguous rows hold GK k (GK / 8 chunks of 16 bytes); the chunk
+// position is XOR-swizzled by the row so that 16 consecutive rows at one
+// chunk fall on 16 distinct 16-byte bank groups.
+template <int GK>
+DEVI int kc_swz(int r) { return GK == 32 ? (r >> 2) & 3 : (r >> 1) & 7; }
 
-template <int N, class RowPtr>
+template <int GK, int N, class RowPtr>
 DEVI void dma_kc_init(DmaPtrs<N>& d, const RowPtr& row_ptr, int w) {
+  constexpr int CPR = GK / 8;  // chunks per row
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int row = (i * 4 + w) * 16 + (lane >> 2);
-    d.p[i] = row_ptr(row) + ((lane & 3) ^ kc_swz(row)) * 8;
+    const int row = (i * 4 + w) * (64 / CPR) + lane / CPR;
+    d.p[i] = row_ptr(row) + ((lane % CPR) ^ kc_swz<GK>(row)) * 8;
   }
 }
 
@@ -392,11 +408,13 @@ DEVI void dma_mn_init(DmaPtrs<N>& d, const ElemPtr& elem_ptr, int w, int k0) {
 }
 
 // fragment of rows/cols [mb, mb+32) at k16-step s, k-contiguous layout
+template <int GK>
 DEVI bf16x8_t frag_kc(const char* lds_op, int mb, int s) {
   const int lane = threadIdx.x & 63;
   const int row = mb + (lane & 31);
   const int kc = s * 2 + (lane >> 5);
-  return *reinterpret_cast<const bf16x8_t*>(lds_op + row * 64 + ((kc ^ kc_swz(row)) << 4));
+  return *reinterpret_cast<const bf16x8_t*>(lds_op + row * (GK * 2) +
+                                            ((kc ^ kc_swz<GK>(row)) << 4));
 }
 
 // same fragment from the m/n-contiguous layout with two transposing reads
@@ -549,7 +567,7 @@ template <int KIND>
 __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaunch L) {
   using K_ = Kind<KIND>;
   using C_ = Cfg<KIND>;
-  constexpr int MI = C_::MI, WM = C_::WM, NS = C_::NS;
+  constexpr int MI = C_::MI, WM = C_::WM, NS = C_::NS, GK = C_::GK, KS = C_::KS;
   __shared__ __attribute__((aligned(1024))) char lds[C_::LDS];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -642,8 +660,8 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
     // tail k-step
     DmaPtrs<C_::DMA_A> da, ta;
     DmaPtrs<C_::DMA_B> db, tb;
-    if constexpr (K_::A_KC) dma_kc_init(da, a_row, wave); else dma_mn_init(da, a_elem, wave, 0);
-    if constexpr (K_::B_KC) dma_kc_init(db, b_row, wave); else dma_mn_init(db, b_elem, wave, 0);
+    if constexpr (K_::A_KC) dma_kc_init<GK>(da, a_row, wave); else dma_mn_init(da, a_elem, wave, 0);
+    if constexpr (K_::B_KC) dma_kc_init<GK>(db, b_row, wave); else dma_mn_init(db, b_elem, wave, 0);
     if constexpr (!K_::MRAG) {
       dma_mn_init(ta, a_elem, wave, n_full * GK);
       dma_mn_init(tb, b_elem, wave, n_full * GK);
@@ -673,12 +691,13 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
     auto read_frag = [&](const char* stage, int s, int idx, bf16x8_t* af, bf16x8_t* bfr) {
       // idx 0..MI-1: A fragment idx; MI..MI+3: B fragment idx-MI
       if (idx < MI) {
-        af[idx] = K_::A_KC ? frag_kc(stage, wm * WM + idx * 32, s)
+        af[idx] = K_::A_KC ? frag_kc<GK>(stage, wm * WM + idx * 32, s)
                            : frag_mn(stage, wm * WM + idx * 32, s);
       } else {
         const int f = idx - MI;
         const char* lb = stage + C_::A_BYTES;
-        bfr[f] = K_::B_KC ? frag_kc(lb, wn * 128 + f * 32, s) : frag_mn(lb, wn * 128 + f * 32, s);
+        bfr[f] = K_::B_KC ? frag_kc<GK>(lb, wn * 128 + f * 32, s)
+                          : frag_mn(lb, wn * 128 + f * 32, s);
       }
     };
 
@@ -728,11 +747,20 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
       const int st = kt % NS;
       const char* stage = lds + st * C_::STAGE;
       const char* stage_next = lds + ((kt + 1) % NS) * C_::STAGE;
-      kstep(af0, bf0, stage, 1, af1, bf1, -1, 0);
+      // k16-steps 0 .. KS-2 read the next fragments from this stage
+#pragma unroll
+      for (int s = 0; s < KS - 1; ++s) {
+        if (s % 2 == 0) kstep(af0, bf0, stage, s + 1, af1, bf1, -1, 0);
+        else kstep(af1, bf1, stage, s + 1, af0, bf0, -1, 0);
+      }
       WAIT_LGKMCNT(0);
       WAIT_VMCNT(C_::DMA_N * (NS - 2));
       __syncthreads();
-      kstep(af1, bf1, stage_next, 0, af0, bf0, min(kt + NS, nk - 1), st);
+      // the last one reads k16-step 0 of the next stage and refills this one
+      if constexpr ((KS - 1) % 2 == 0)
+        kstep(af0, bf0, stage_next, 0, af1, bf1, min(kt + NS, nk - 1), st);
+      else
+        kstep(af1, bf1, stage_next, 0, af0, bf0, min(kt + NS, nk - 1), st);
     }
     WAIT_VMCNT(0);  // drain the ring before the next tile
 

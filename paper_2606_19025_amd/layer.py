@@ -110,11 +110,16 @@ class ResidentMoELayer:
 
     # ------------------------------------------------------------------ forward
     def forward(self, x, w_router, w_gate_up, w_down, router_bias=None, shared_gate_up=None,
-                shared_down=None, stream=None):
+                shared_down=None, stream=None, hook=None):
+        """hook: called before each library call (e.g. a cache flush between
+        kernels for cold per-kernel timing); None in normal use."""
         T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        hook = hook or (lambda: None)
+        hook()
         B.moe_route_mask(x, w_router, router_bias, dt, T, d, E, k, self.inv_tau, self.gate,
                          self.resident, self.logits, self.topk_idx, self.topk_w, self.topk_local,
                          stream)
+        hook()
         B.moe_dispatch(x, dt, T, d, k, self.E_r, self.topk_local, self.counts, self.offsets,
                        self.perm, self.inv_perm, self.xp, self.ws_dispatch, self.ws_dispatch_bytes,
                        stream)
@@ -126,15 +131,19 @@ class ResidentMoELayer:
             sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
                                   self.s_gu, self.s_h, yp=self.s_y, activation=self.act))
             y_add = self.s_y
+        hook()
         B.moe_grouped_ffn_fwd_sets(sets, dt, d, stream)
+        hook()
         B.moe_combine_fwd(self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, y_add, self.y,
                           stream)
         return self.y
 
     # ----------------------------------------------------------------- backward
     def backward(self, dy, x, w_router, w_gate_up, w_down, shared_gate_up=None, shared_down=None,
-                 accumulate_dw=0, stream=None):
+                 accumulate_dw=0, stream=None, hook=None):
         T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        hook = hook or (lambda: None)
+        hook()
         B.moe_combine_bwd(dy, self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, self.dyp,
                           self.dtopk_w, stream)
         sets = [B.ffn_set(self.xp, w_gate_up, w_down, self.offsets, cap, H, self.E_r, self.gu,
@@ -149,10 +158,13 @@ class ResidentMoELayer:
         if self.ws_ffn is None:
             self.ws_ffn_bytes = B.moe_grouped_ffn_bwd_workspace_size(sets, dt, d)
             self.ws_ffn = torch.empty(self.ws_ffn_bytes, dtype=torch.uint8, device=self.device)
+        hook()
         B.moe_grouped_ffn_bwd_sets(sets, dt, d, accumulate_dw, self.ws_ffn, self.ws_ffn_bytes,
                                    stream)
+        hook()
         B.moe_dispatch_bwd(self.dxp, dt, T, d, k, cap, self.inv_perm, self.dx, 1 if self.Hs else 0,
                            stream)
+        hook()
         B.moe_route_bwd(x, w_router, dt, T, d, E, k, self.inv_tau, self.gate, self.topk_idx,
                         self.topk_w, self.logits, self.dtopk_w, self.dz, self.dw_router,
                         self.d_bias, self.dx, 1, self.ws_route, self.ws_route_bytes, stream)
