@@ -689,12 +689,14 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
     };
 
     auto read_frag = [&](const char* stage, int s, int idx, bf16x8_t* af, bf16x8_t* bfr) {
-      // idx 0..MI-1: A fragment idx; MI..MI+3: B fragment idx-MI
-      if (idx < MI) {
-        af[idx] = K_::A_KC ? frag_kc<GK>(stage, wm * WM + idx * 32, s)
-                           : frag_mn(stage, wm * WM + idx * 32, s);
+      // in the order the next k16-step's MFMAs consume them: idx 0 = A
+      // fragment 0, 1..4 = B fragments 0..3, 5.. = A fragments 1..MI-1
+      if (idx == 0 || idx > 4) {
+        const int f = idx == 0 ? 0 : idx - 4;
+        af[f] = K_::A_KC ? frag_kc<GK>(stage, wm * WM + f * 32, s)
+                         : frag_mn(stage, wm * WM + f * 32, s);
       } else {
-        const int f = idx - MI;
+        const int f = idx - 1;
         const char* lb = stage + C_::A_BYTES;
         bfr[f] = K_::B_KC ? frag_kc<GK>(lb, wn * 128 + f * 32, s)
                           : frag_mn(lb, wn * 128 + f * 32, s);
