@@ -366,8 +366,9 @@ struct RouteBwdArgs {
   float* db;
   void* dx;
   float* part_w;  // [n_chunks][E][d]
-  float* part_b;  // [n_chunks][E]
+  float* part_b;  // [n_chunks][n_bparts][E]
   int T, d, E, k, gate, accumulate_dx, n_chunks;
+  int n_bparts;   // d_bias partial sums per chunk
   float inv_tau;
 };
 
@@ -455,7 +456,7 @@ __global__ __launch_bounds__(256) void route_dw_partial_kernel(RouteBwdArgs a) {
     }
   }
   if (blockIdx.x == 0 && threadIdx.x < 64 && e0 + threadIdx.x < a.E)
-    a.part_b[(size_t)chunk * a.E + e0 + threadIdx.x] = bacc;
+    a.part_b[(size_t)chunk * a.n_bparts * a.E + e0 + threadIdx.x] = bacc;
 }
 
 __global__ __launch_bounds__(256) void route_dw_reduce_kernel(RouteBwdArgs a) {
@@ -476,18 +477,31 @@ __global__ __launch_bounds__(256) void route_dw_reduce_kernel(RouteBwdArgs a) {
     a.dw[i] = s * a.inv_tau;
   }
   if (a.db && blockIdx.x == 0) {
-    for (int e = threadIdx.x; e < a.E; e += 256) {
+    // d_bias[e] = inv_tau * sum of the (chunk, part) partials: four
+    // consecutive ranges summed by four threads, then added in range order
+    __shared__ float q4[4][64];
+    const int np = a.n_chunks * a.n_bparts;
+    for (int e0 = 0; e0 < a.E; e0 += 64) {
+      const int e = e0 + (threadIdx.x & 63), q = threadIdx.x >> 6;
+      const int pb = (int)((long)np * q / 4), pe = (int)((long)np * (q + 1) / 4);
       float s = 0.f;
-      int c = 0;
-      for (; c + 8 <= a.n_chunks; c += 8) {
-        float v[8];
+      if (e < a.E) {
+        int c = pb;
+        for (; c + 8 <= pe; c += 8) {
+          float v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = a.part_b[(size_t)(c + u) * a.E + e];
+          for (int u = 0; u < 8; ++u) v[u] = a.part_b[(size_t)(c + u) * a.E + e];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s += v[u];
+          for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; c < pe; ++c) s += a.part_b[(size_t)c * a.E + e];
       }
-      for (; c < a.n_chunks; ++c) s += a.part_b[(size_t)c * a.E + e];
-      a.db[e] = s * a.inv_tau;
+      q4[q][threadIdx.x & 63] = s;
+      __syncthreads();
+      if (q == 0 && e < a.E)
+        a.db[e] = (((q4[0][threadIdx.x] + q4[1][threadIdx.x]) + q4[2][threadIdx.x]) +
+                   q4[3][threadIdx.x]) * a.inv_tau;
+      __syncthreads();
     }
   }
 }
@@ -546,8 +560,11 @@ __global__ __launch_bounds__(256) void route_dx_kernel(RouteBwdArgs a) {
 // with v_mfma_f32_32x32x16_bf16; wave w owns columns 32w..32w+31 of both.
 // The next sub-chunk's x and dz are loaded into registers while the current
 // one is computed; the dx result is staged through LDS so that the update of
-// dx reads and writes whole row segments.  The per-chunk dW partials (and the d_bias partials of
-// blockIdx.x == 0) are summed in a fixed order by route_dw_reduce_kernel.
+// dx reads and writes whole row segments.  The per-chunk dW partials, and
+// one d_bias partial per block (its column block's share of the chunk's
+// tokens, so that no block carries the whole chunk's bias sum: that made the
+// blocks of column 0 the critical path, 15 us of about 50), are summed in a
+// fixed order by route_dw_reduce_kernel.
 constexpr int RBM_COLS = 128;
 constexpr int RBM_SUB = 64;                   // tokens per sub-chunk
 constexpr int RBM_XS = RBM_COLS * 2 + 64;     // x row stride (bytes): the 4 rows of
@@ -570,7 +587,6 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
   char* zh = xs + RBM_SUB * RBM_XS;
   char* zl = zh + RBM_SUB * RBM_ZS;
   char* wl = zl + RBM_SUB * RBM_ZS;
-  __shared__ float bpart[4][64];
   const bf16_t* x = static_cast<const bf16_t*>(a.x);
   const bf16_t* w = static_cast<const bf16_t*>(a.w);
   bf16_t* dx = static_cast<bf16_t*>(a.dx);
@@ -641,21 +657,31 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
   };
 
   f32x16_t accw[2] = {f32x16_t{}, f32x16_t{}};
-  float bsum = 0.f;
   if (n_sub > 0) load_sub(chunk * RB_CHUNK);
+  // d_bias partial: column block b < n_bparts sums the exact fp32 dz of the
+  // sub-chunks s with s % n_bparts == b, from the registers that stage them:
+  // per thread its two rows, then across the 8 lanes of an expert group
+  // (xor shuffles), then (at the end) across the 4 waves in wave order
+  const bool do_bias = blockIdx.x < a.n_bparts;
+  float bacc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int sc = 0; sc < n_sub; ++sc) {
     const int t0 = chunk * RB_CHUNK + sc * RBM_SUB;
     __syncthreads();  // previous sub-chunk's LDS reads are done
     store_sub();
+    if (do_bias && sc % a.n_bparts == (int)blockIdx.x) {
+      static_assert(RBM_ZV == 2, "two dz rows per thread");
+      float b8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) b8[u] = zr[0][u] + zr[1][u];
+#pragma unroll
+      for (int m = 8; m < 64; m <<= 1)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) b8[u] += __shfl_xor(b8[u], m, 64);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) bacc[u] += b8[u];
+    }
     __syncthreads();
     if (sc + 1 < n_sub) load_sub(t0 + RBM_SUB);
-    if (blockIdx.x == 0 && lane < a.E) {
-      // d_bias: 16 tokens per wave, fixed order, exact fp32 dz
-      for (int i = 0; i < RBM_SUB / 4; ++i) {
-        const int t = t0 + wave * (RBM_SUB / 4) + i;
-        if (t < a.T) bsum += a.dz[(size_t)t * a.E + lane];
-      }
-    }
     // old dx of this thread's 16-byte chunks of the sub-chunk (requested
     // before the MFMAs; used by the coalesced update below)
     u32x4_t old[RBM_XV];
@@ -744,11 +770,15 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
       *reinterpret_cast<f32x4_t*>(p) = o;
     }
   }
-  if (blockIdx.x == 0) {
-    if (lane < 64) bpart[wave][lane] = bsum;
+  if (do_bias) {
+    // lanes 0..7 hold experts 8 lane .. 8 lane + 7 of this wave's rows
+    __shared__ float bpart[4][64];
+    if (lane < 8)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) bpart[wave][lane * 8 + u] = bacc[u];
     __syncthreads();
     if (tid < a.E)
-      a.part_b[(size_t)chunk * a.E + tid] =
+      a.part_b[((size_t)chunk * a.n_bparts + blockIdx.x) * a.E + tid] =
           ((bpart[0][tid] + bpart[1][tid]) + bpart[2][tid]) + bpart[3][tid];
   }
 }
@@ -773,9 +803,13 @@ hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int
   return hipGetLastError();
 }
 
+// d_bias partial sums per chunk: one per 64-token sub-chunk in the MFMA
+// kernel (at most one per column block), one in the VALU kernels
+int route_bwd_bparts(int d) { return std::max(1, std::min(d / RBM_COLS, RB_CHUNK / RBM_SUB)); }
+
 size_t route_bwd_ws_bytes(int T, int d, int E) {
   const size_t chunks = (size_t)(T + RB_CHUNK - 1) / RB_CHUNK;
-  return chunks * (size_t)E * ((size_t)d + 1) * sizeof(float) + 256;
+  return chunks * (size_t)E * ((size_t)d + route_bwd_bparts(d)) * sizeof(float) + 256;
 }
 
 hipError_t launch_route_bwd(const void* x, const void* w, int bf16, int T, int d, int E, int k,
@@ -786,10 +820,11 @@ hipError_t launch_route_bwd(const void* x, const void* w, int bf16, int T, int d
   const int n_chunks = (T + RB_CHUNK - 1) / RB_CHUNK;
   float* part_w = static_cast<float*>(ws);
   float* part_b = part_w + (size_t)n_chunks * E * d;
-  RouteBwdArgs a{x, w, idx, tw, logits, dtw, dz, dw_router, d_bias, dx, part_w, part_b,
-                 T, d, E, k, gate, accumulate_dx, n_chunks, inv_tau};
-  if (T > 0) MOE_TIMED("route_dz", s, route_dz_kernel<<<ceil_div(T, 4), 256, 0, s>>>(a));
   const bool mfma = bf16 && E <= 64 && d % RBM_COLS == 0;
+  RouteBwdArgs a{x, w, idx, tw, logits, dtw, dz, dw_router, d_bias, dx, part_w, part_b,
+                 T, d, E, k, gate, accumulate_dx, n_chunks,
+                 mfma ? std::min(d / RBM_COLS, RB_CHUNK / RBM_SUB) : 1, inv_tau};
+  if (T > 0) MOE_TIMED("route_dz", s, route_dz_kernel<<<ceil_div(T, 4), 256, 0, s>>>(a));
   if (n_chunks > 0) {
     if (mfma) {
       const dim3 g(d / RBM_COLS, n_chunks);
