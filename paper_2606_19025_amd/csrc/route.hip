@@ -183,75 +183,66 @@ DEVI uint32_t sel_key(float v) {
 
 constexpr int RT_KSEL = 8;
 
-// Insert (kv, e) into slots kept in descending key order.  A strictly larger
-// key is needed to pass a slot, so among equal logits the expert inserted
-// first (the lower id) ranks first.
-DEVI void sel_insert(uint32_t* key, int* id, uint32_t kv, int e) {
-#pragma unroll
-  for (int j = RT_KSEL - 1; j >= 1; --j) {
-    const bool up = kv > key[j - 1];
-    const bool here = kv > key[j];
-    key[j] = up ? key[j - 1] : (here ? kv : key[j]);
-    id[j] = up ? id[j - 1] : (here ? e : id[j]);
-  }
-  if (kv > key[0]) { key[0] = kv; id[0] = e; }
-}
-
-// Top-k, gate weights and local ids of the block's tokens, two lanes per
-// token (run by all 64 lanes of one wave): lane l scans the lower half of
-// token l % 32's experts if l < 32, else the upper half; the upper lane's
-// top RT_KSEL is then merged into the lower lane's (inserted after it, so
-// ties still go to the lower id).  The first k of the top RT_KSEL are the
-// top k.
-template <int LDZ>
-DEVI void select_pairs(const RouteFwdArgs& a, const float* zl, int t0, const int* lmap) {
+// Top-k (k <= RT_KSEL), gate weights and local ids of the block's tokens, 16
+// lanes per token (all RT_WAVES waves: wave w takes tokens 4w .. 4w+3): lane
+// s of a group holds experts s, s + 16, ... as 64-bit keys (order-preserving
+// logit key, then the inverted expert id, so that equal logits rank the lower
+// id first; 0 = taken or absent).  Round j takes the group's largest key by
+// xor shuffles and lane j keeps it, so the selections come out in rank order.
+template <int LDZ, int NE>
+DEVI void select_groups(const RouteFwdArgs& a, const float* zl, int t0, const int* lmap) {
   const int lane = threadIdx.x & 63;
-  const int i = lane & 31, half = lane >> 5;
-  const float* z = zl + i * LDZ;
-  const int e_mid = (a.E + 1) / 2;
-  const int eb = half ? e_mid : 0, ee = half ? a.E : e_mid;
-  uint32_t key[RT_KSEL];
-  int id[RT_KSEL];
-#pragma unroll
-  for (int j = 0; j < RT_KSEL; ++j) { key[j] = 0u; id[j] = 0; }
-  for (int e = eb; e < ee; ++e) sel_insert(key, id, sel_key(sel_value(z[e])), e);
-  uint32_t uk[RT_KSEL];
-  int ui[RT_KSEL];
-#pragma unroll
-  for (int j = 0; j < RT_KSEL; ++j) {
-    uk[j] = (uint32_t)__shfl((int)key[j], lane | 32, 64);
-    ui[j] = __shfl(id[j], lane | 32, 64);
-  }
+  const int wave = threadIdx.x >> 6;
+  const int s = lane & 15;
+  const int i = wave * 4 + (lane >> 4);
   const int t = t0 + i;
-  if (half || t >= a.T) return;
+  const float* z = zl + i * LDZ;
+  uint64_t cand[NE];
 #pragma unroll
-  for (int j = 0; j < RT_KSEL; ++j)
-    if (uk[j] != 0u) sel_insert(key, id, uk[j], ui[j]);
-  float zs[RT_KSEL];
-#pragma unroll
-  for (int j = 0; j < RT_KSEL; ++j) zs[j] = sel_value(z[id[j]]);
-  const float zmax = zs[0];
-  float denom = 1.f;
-  if (a.gate == 0) {  // softmax over the k selected logits
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < RT_KSEL; ++j)
-      if (j < a.k) s += expf(zs[j] - zmax);
-    denom = s;
-  } else if (a.gate == 1) {  // softmax over all E logits
-    float s = 0.f;
-    for (int e = 0; e < a.E; ++e) s += expf(sel_value(z[e]) - zmax);
-    denom = s;
+  for (int q = 0; q < NE; ++q) {
+    const int e = q * 16 + s;
+    cand[q] = e < a.E ? ((uint64_t)sel_key(sel_value(z[e])) << 32) | (uint32_t)~e : 0ull;
   }
+  int my_id = 0;
+  for (int j = 0; j < a.k; ++j) {
+    uint64_t m = 0ull;
 #pragma unroll
-  for (int j = 0; j < RT_KSEL; ++j) {
-    if (j < a.k) {
-      const float wj = (a.gate == 2) ? sigmoid_f(zs[j]) : expf(zs[j] - zmax) / denom;
-      const size_t o = (size_t)t * a.k + j;
-      a.idx[o] = id[j];
-      a.tw[o] = wj;
-      a.local[o] = lmap[id[j]];
+    for (int q = 0; q < NE; ++q) m = cand[q] > m ? cand[q] : m;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const uint64_t om = ((uint64_t)(uint32_t)__shfl_xor((int)(m >> 32), o, 64) << 32) |
+                          (uint32_t)__shfl_xor((int)(uint32_t)m, o, 64);
+      m = om > m ? om : m;
     }
+#pragma unroll
+    for (int q = 0; q < NE; ++q)
+      if (cand[q] == m) cand[q] = 0ull;
+    if (s == j) my_id = (int)~(uint32_t)m;
+  }
+  const float my_z = sel_value(z[my_id]);
+  const float zmax = __shfl(my_z, lane & 48, 64);  // the group's first selection
+  float denom = 1.f;
+  if (a.gate == 0 || a.gate == 1) {  // softmax over the k selected / all E logits
+    float acc = 0.f;
+    if (a.gate == 0) {
+      if (s < a.k) acc = expf(my_z - zmax);
+    } else {
+#pragma unroll
+      for (int q = 0; q < NE; ++q) {
+        const int e = q * 16 + s;
+        if (e < a.E) acc += expf(sel_value(z[e]) - zmax);
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) acc += __shfl_xor(acc, o, 64);
+    denom = acc;
+  }
+  if (s < a.k && t < a.T) {
+    const float wj = (a.gate == 2) ? sigmoid_f(my_z) : expf(my_z - zmax) / denom;
+    const size_t o = (size_t)t * a.k + s;
+    a.idx[o] = my_id;
+    a.tw[o] = wj;
+    a.local[o] = lmap[my_id];
   }
 }
 
@@ -280,9 +271,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   __syncthreads();
 
   if (a.k <= RT_KSEL) {
-    // two lanes per token: running top-RT_KSEL lists in registers
-    static_assert(RT_TOK == 32, "two lanes per token in one wave");
-    if (wave == 0) select_pairs<LDZ>(a, zl, t0, lmap);
+    static_assert(RT_TOK == 4 * RT_WAVES, "16 lanes per token in every wave");
+    select_groups<LDZ, 2 * NEB>(a, zl, t0, lmap);
     return;
   }
   for (int i = wave; i < RT_TOK; i += RT_WAVES) {

@@ -140,6 +140,57 @@ def test_topk_ties_go_to_lower_expert_id(gpu_lib):
     np.testing.assert_allclose(host(tw), 1.0 / 3.0, rtol=1e-6)
 
 
+# Router logits set exactly through the bias (x = 0, so every logit is its
+# expert's bias): ties, signed zeros, +inf and NaN at chosen places, for every
+# expert-count branch of the selection (E up to 32, 64, 128 and 256 experts),
+# k from 1 to E.  The oracle selects on the GPU's own logits.
+SELECT_CASES = {
+    "E8-k8-special": (8, 8, "softmax_topk",
+                      [0.5, np.nan, 0.5, -1.0, np.inf, 0.5, -0.0, 0.0]),
+    "E40-k5-ties": (40, 5, "softmax_topk", None),
+    "E40-k7-softmax-all": (40, 7, "softmax", None),
+    "E64-k1": (64, 1, "softmax_topk", None),
+    "E128-k8-sigmoid": (128, 8, "sigmoid", None),
+    "E200-k6-nan": (200, 6, "softmax_topk", "nan"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SELECT_CASES))
+def test_topk_selection_special_logits(gpu_lib, name):
+    E, k, gate, bias = SELECT_CASES[name]
+    T, d = 48, 64
+    g = np.random.default_rng([11, E, k])
+    if bias is None or bias == "nan":
+        b = np.round(g.standard_normal(E) * 2.0) / 2.0  # many exact ties
+        b[g.choice(E, E // 8, replace=False)] = -0.0
+        if bias == "nan":
+            b[g.choice(E, E // 10, replace=False)] = np.nan
+    else:
+        b = np.array(bias, np.float64)
+    say(f"[select] {name}")
+    x = torch.zeros(T, d, dtype=torch.bfloat16, device="cuda")
+    w = dev(g.standard_normal((E, d)).astype(np.float32), torch.bfloat16)
+    res = np.zeros(E, np.uint8)
+    res[g.choice(E, max(1, E // 3), replace=False)] = 1
+    logits = torch.empty(T, E, dtype=torch.float32, device="cuda")
+    idx = torch.empty(T, k, dtype=torch.int32, device="cuda")
+    loc = torch.empty_like(idx)
+    tw = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    B.moe_route_mask(x, w, torch.from_numpy(b.astype(np.float32)).cuda(), B.MOE_BF16, T, d, E, k,
+                     1.0, B.GATES[gate], torch.from_numpy(res).cuda(), logits, idx, tw, loc)
+    torch.cuda.synchronize()
+    z = host(logits)
+    assert np.array_equal(np.isnan(z), np.broadcast_to(np.isnan(b), z.shape))
+    assert np.array_equal(z[~np.isnan(z)], np.broadcast_to(b + 0.0, z.shape)[~np.isnan(z)])
+    ref = O.topk_select(z, k)
+    assert np.array_equal(host(idx), ref), "top-k differs from the stable sort on the logits"
+    rank = np.cumsum(res.astype(np.int64)) - 1
+    assert np.array_equal(host(loc), np.where(res[ref] == 1, rank[ref], -1))
+    wr = O.gate_weights(z, ref, gate=gate)
+    fin = np.isfinite(wr)
+    np.testing.assert_allclose(host(tw)[fin], wr[fin], rtol=2e-6, atol=1e-7)
+
+
 def test_layer_is_deterministic(gpu_lib):
     inp = synth_inputs(600, 128, 12, 3, 128, [0, 3, 5, 8], "bf16", seed=5, shared_hidden=64)
     L1, _ = run_gpu_layer(inp)
