@@ -46,6 +46,7 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 FLUSH_BYTES = 512 << 20     # twice the 256 MB Infinity Cache
+SWEEP_TRIALS = 3            # timed runs per configuration of --ghost-sweep
 
 
 def log(*a):
@@ -175,16 +176,22 @@ def ghost_sweep(args):
             for _ in range(args.warmup):
                 step()
             torch.cuda.synchronize()
-            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            ev0.record()
-            for _ in range(args.steps):
-                step()
-            ev1.record()
-            torch.cuda.synchronize()
-            ms = ev0.elapsed_time(ev1) / args.steps
+            # median of SWEEP_TRIALS timed runs: single runs of these short
+            # steps showed occasional 1.5x outliers on an otherwise idle GPU
+            trials = []
+            for _ in range(SWEEP_TRIALS):
+                ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ev0.record()
+                for _ in range(args.steps):
+                    step()
+                ev1.record()
+                torch.cuda.synchronize()
+                trials.append(ev0.elapsed_time(ev1) / args.steps)
+            ms = sorted(trials)[len(trials) // 2]
             n = int(L.offsets[-1].item())
             rows.append(dict(E_resident=Er, ghost_experts=E - Er, mode=mode, ms_per_step=round(ms, 4),
-                             tokens_per_s=round(T / (ms / 1e3), 1), executed_routes=n))
+                             tokens_per_s=round(T / (ms / 1e3), 1), executed_routes=n,
+                             trials_ms=[round(t, 4) for t in trials]))
             log(f"[sweep] E_r={Er:2d} {mode:11s} {ms:.3f} ms/step n={n}")
             del L
     full = {r["mode"]: r["tokens_per_s"] for r in rows if r["ghost_experts"] == 0}
