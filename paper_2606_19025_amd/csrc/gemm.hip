@@ -259,8 +259,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // see Cfg: two blocks per CU, 64 x 128 per wave = 2 x 4 MFMA tiles.)
 //
 // Operands stream through a ring of NS LDS stages of one k-step (GK) each,
-// filled with 16-byte global -> LDS DMA: full tiles NS = 2 stages of GK = 64
-// (64 KB each), half-height tiles NS = 3 stages of GK = 32 (24 KB each).  A
+// filled with 16-byte global -> LDS DMA: full M-ragged tiles NS = 2 stages of
+// GK = 64 (64 KB each), weight-gradient tiles NS = 4 stages of GK = 32 (32 KB
+// each), half-height tiles NS = 3 stages of GK = 32 (24 KB each).  A
 // k-step is GK / 16 k16-steps; per k-step and wave:
 //   k16-steps 0 .. GK/16 - 2: 16 MFMAs each (8 for half-height tiles),
 //   interleaved with the LDS reads of the next k16-step
@@ -313,16 +314,18 @@ constexpr int N_XCD = 8;
 // 256 x 256 tiles; DOWN_FWD and DX_BWD (light epilogues, longer K) were 7 %
 // and 3 % slower that way, so they and the K-ragged kinds keep 256 x 256
 // tiles with one block per CU.
-// Full tiles take k-steps of 64 in a ring of two 64 KB stages: every DMA load
-// then fetches whole 128-byte row pieces (half the L2 requests of 64-byte
-// pieces).  Measured against k-steps of 32 in four stages: DOWN_FWD 6 % and
-// DX_BWD 1-2 % faster, the weight-gradient kinds unchanged.  Half-height tiles
-// keep k-steps of 32 (two blocks of three 24 KB stages fill the LDS).
+// Full M-ragged tiles (DOWN_FWD, DX_BWD) take k-steps of 64 in a ring of two
+// 64 KB stages: every DMA load then fetches whole 128-byte row pieces (half
+// the L2 requests of 64-byte pieces); measured against k-steps of 32 in four
+// stages, DOWN_FWD 6-10 % and DX_BWD 1-2 % faster.  The weight-gradient kinds
+// keep k-steps of 32 in four stages (equal on the fine-grained workload, 2-6 %
+// faster on the mid-size one, and a ragged K pads at most 31 rows), and so do
+// half-height tiles (two blocks of three 24 KB stages fill the LDS).
 template <int KIND>
 struct Cfg {
   static constexpr bool HALF =
       KIND == GU_FWD || KIND == DHH_BWD || KIND == UP_FWD || KIND == DH_BWD;
-  static constexpr int GK = HALF ? 32 : 64;        // k-step
+  static constexpr int GK = HALF || !Kind<KIND>::MRAG ? 32 : 64;  // k-step
   static constexpr int KS = GK / 16;               // k16-steps per k-step
   static constexpr int BM = HALF ? 128 : 256;      // block tile rows
   static constexpr int WM = BM / 2;                // wave sub-tile rows
