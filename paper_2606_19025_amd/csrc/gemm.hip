@@ -276,11 +276,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // last one is loaded again into an unused stage) so vmcnt counting is uniform;
 // the ring is drained (vmcnt(0)) before a block moves to its next tile.
 //
-// Tile order (see tile_decode): bands of GROUP_M m-tiles (4 full or 8
-// half-height ones).  Workgroups are dealt to the 8 XCDs round-robin by id,
-// so block b works on tiles of the ranges assigned to XCD b % 8 (an eighth of
-// each set's tiles): the 32 (64 half-height) tiles an XCD runs at a time form
-// a GROUP_M x 8 rectangle whose operand panels its L2 serves.  Output tiles
+// Tile order (see tile_decode): bands of GROUP_M m-tiles (2 to 8, per kind,
+// see Cfg).  Workgroups are dealt to the 8 XCDs round-robin by id, so block b
+// works on tiles of the ranges assigned to XCD b % 8 (an eighth of each set's
+// tiles): the 32 (64 half-height) tiles an XCD runs at a time form a band
+// rectangle whose operand panels its L2 serves.  Output tiles
 // end in an epilogue: bf16 results are staged through the drained ring so
 // global accesses are whole 16-byte chunks; fp32 weight gradients are stored
 // (or added) straight from the accumulators.
@@ -340,7 +340,11 @@ struct Cfg {
   static constexpr int DMA_N = DMA_A + DMA_B;
   static constexpr int DMA_MAX = DMA_A > DMA_B ? DMA_A : DMA_B;
   static constexpr int EPI_WAVE = WM * 256;        // epilogue staging per wave
-  static constexpr int GROUP = HALF ? 8 : 4;       // m-tiles per band
+  // m-tiles per band of the tile order, measured per kind on the
+  // fine-grained workload (bands of 2, 4, 8 and 16 tried)
+  static constexpr int GROUP = (KIND == GU_FWD || KIND == UP_FWD || KIND == DOWN_FWD) ? 8
+                               : (KIND == DHH_BWD || KIND == DH_BWD || KIND == DX_BWD) ? 4
+                                                                                        : 2;
   static constexpr int OCC = HALF ? 2 : 1;         // blocks per CU
   static_assert(4 * EPI_WAVE <= LDS, "epilogue staging exceeds the ring");
 };
