@@ -69,22 +69,43 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   const int wave = threadIdx.x >> 6;
   const int row = lane & 31;
   const int half = lane >> 5;
-  const int t = t0 + row;
   f32x16_t acc[NEB];
 #pragma unroll
   for (int eb = 0; eb < NEB; ++eb) acc[eb] = f32x16_t{};
   const bf16x8_t zero8 = {};
+  const u32x4_t zero4 = {0u, 0u, 0u, 0u};
   const int n_slices = (a.d + 63) / 64;
+  // x slices go through a wave-private LDS buffer: loaded as whole 128-byte
+  // row pieces (8 lanes per token row; 32 rows per read in fragment order
+  // would touch 32 cache lines per instruction), stored with the 16-byte
+  // chunk c of row r at chunk position c ^ ((r >> 1) & 7) so that the
+  // fragment reads (16 consecutive rows, same chunk) are free of bank
+  // conflicts.  The W slices stay direct fragment loads (L2-resident).
+  constexpr int UNR = NEB <= 2 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) char xst[RT_WAVES][UNR][RT_TOK * 128];
+  auto xswz = [](int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); };
+  auto load_x = [&](int kb, u32x4_t* v) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tr = t0 + j * 8 + (lane >> 3);
+      const int c = kb * 64 + (lane & 7) * 8;
+      v[j] = (kb < n_slices && tr < a.T && c + 8 <= a.d)
+                 ? *reinterpret_cast<const u32x4_t*>(x + (size_t)tr * a.d + c)
+                 : zero4;
+    }
+  };
+  auto store_x = [&](int u, const u32x4_t* v) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<u32x4_t*>(&xst[wave][u][xswz(j * 8 + (lane >> 3), lane & 7)]) = v[j];
+  };
   // the lane's 32 consecutive elements of a slice feed the 4 k16 MFMA steps
   // in the same order for the token and the expert operand
-  auto load_slice = [&](int kb, bf16x8_t* av, bf16x8_t (*bv)[4]) {
+  auto load_slice = [&](int kb, bf16x8_t* av, bf16x8_t (*bv)[4], int u) {
     const int c0 = kb * 64 + half * 32;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int c = c0 + q * 8;
-      av[q] = (kb < n_slices && t < a.T && c + 8 <= a.d)
-                  ? *reinterpret_cast<const bf16x8_t*>(x + (size_t)t * a.d + c) : zero8;
-    }
+    for (int q = 0; q < 4; ++q)
+      av[q] = *reinterpret_cast<const bf16x8_t*>(&xst[wave][u][xswz(row, half * 4 + q)]);
 #pragma unroll
     for (int eb = 0; eb < NEB; ++eb) {
       const int e = eb * 32 + row;
@@ -97,11 +118,15 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
     }
   };
   // UNR slices per round (fewer for wide expert sets, to stay in registers)
-  constexpr int UNR = NEB <= 2 ? 2 : 1;
   for (int kb = wave; kb < n_slices; kb += UNR * RT_WAVES) {
     bf16x8_t av[UNR][4], bv[UNR][NEB][4];
+    u32x4_t xv[UNR][4];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) load_slice(kb + u * RT_WAVES, av[u], bv[u]);  // zeros past the end
+    for (int u = 0; u < UNR; ++u) load_x(kb + u * RT_WAVES, xv[u]);  // zeros past the end
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) store_x(u, xv[u]);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) load_slice(kb + u * RT_WAVES, av[u], bv[u], u);
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
 #pragma unroll
