@@ -233,10 +233,13 @@ DEVI void unpack16_f32(const u32x4_t& r, float* out, const bf16_t*) {
   }
 }
 
-// Routes whose rows are requested together, before any of them is summed.
-constexpr int RB = 4;
-// 16-byte chunks per lane and column pass of the weighted row sums.
-constexpr int WCPL = 2;
+// Routes whose rows are requested together, before any of them is summed,
+// and 16-byte chunks per lane and column pass of the weighted row sums: a
+// d = 2048 bf16 row in one pass, two routes at a time (measured against 2
+// chunks x 4 routes: combine_fwd 3 % faster warm, 6 % cold; 1 chunk or 4
+// routes were slower).
+constexpr int RB = 2;
+constexpr int WCPL = 4;
 
 // y[t] = sum over resident routes (in route order) of w * rows[slot] (+ add[t]);
 // combine forward (weights tw, add = shared output) and un-permute (tw NULL,
