@@ -364,7 +364,10 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 // wave-uniform).  Issued as inline asm so the compiler does not treat every
 // later LDS read as possibly aliasing the pending DMA (it would wait for all
 // outstanding global loads before each transposing read); the kernel waits for
-// the DMA explicitly (vmcnt) before the barrier that publishes a stage.
+// the DMA explicitly (vmcnt) before the barrier that publishes a stage.  The
+// asm sets m0 itself; the compiler keeps no value of its own in m0 across it
+// (m0 is reserved, and nothing else in these kernels uses it), which the
+// "m0" clobber records for the reader.
 DEVI void load_to_lds(const bf16_t* g, char* lds_base) {
   const unsigned m0 = (unsigned)(uintptr_t)(lds_void_t*)lds_base;
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0)
@@ -443,17 +446,8 @@ DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
   return __builtin_bit_cast(bf16x8_t, both);
 }
 
-DEVI void store4(bf16_t* p, const float* v) {
-  bf16x4_t o = {(bf16_t)v[0], (bf16_t)v[1], (bf16_t)v[2], (bf16_t)v[3]};
-  *reinterpret_cast<bf16x4_t*>(p) = o;
-}
-DEVI void load4(const bf16_t* p, float* v) {
-  const bf16x4_t x = *reinterpret_cast<const bf16x4_t*>(p);
-  v[0] = (float)x[0]; v[1] = (float)x[1]; v[2] = (float)x[2]; v[3] = (float)x[3];
-}
-
-// Epilogue staging.  A wave's 128x128 bf16 sub-tile occupies 128 rows of
-// 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
+// Epilogue staging.  A wave's bf16 sub-tile (128 columns; 128 rows, or 64 for
+// half-height tiles) occupies rows of 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
 // the key is a bijection on r mod 32, so the accumulator writes (32 rows at
 // one unit per half-wave) hit 32 distinct bank pairs, and rows 2m, 2m+1
 // differ in key bit 3, so the SwiGLU reads (8 chunks of two rows per 16
@@ -587,7 +581,7 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
   // when it finishes one (tiles of unequal K then balance across blocks).
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
-  if (L.zero && blockIdx.x == 0 && threadIdx.x < L.n_zero) L.zero[threadIdx.x] = 0;
+  if (L.zero && blockIdx.x == 0 && (int)threadIdx.x < L.n_zero) L.zero[threadIdx.x] = 0;
 
   const int nt0 = col_tiles<KIND>(L.s0);
   const int mt0 = m_tile_count<KIND>(L.s0);

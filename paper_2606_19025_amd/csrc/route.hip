@@ -470,7 +470,7 @@ __global__ __launch_bounds__(256) void route_dw_partial_kernel(RouteBwdArgs a) {
       if (c < a.d) a.part_w[((size_t)chunk * a.E + e) * a.d + c] = acc[u][v];
     }
   }
-  if (blockIdx.x == 0 && threadIdx.x < 64 && e0 + threadIdx.x < a.E)
+  if (blockIdx.x == 0 && threadIdx.x < 64 && e0 + (int)threadIdx.x < a.E)
     a.part_b[(size_t)chunk * a.n_bparts * a.E + e0 + threadIdx.x] = bacc;
 }
 
@@ -677,7 +677,7 @@ __global__ __launch_bounds__(256, 2) void route_bwd_mfma_kernel(RouteBwdArgs a) 
   // sub-chunks s with s % n_bparts == b, from the registers that stage them:
   // per thread its two rows, then across the 8 lanes of an expert group
   // (xor shuffles), then (at the end) across the 4 waves in wave order
-  const bool do_bias = blockIdx.x < a.n_bparts;
+  const bool do_bias = (int)blockIdx.x < a.n_bparts;
   float bacc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int sc = 0; sc < n_sub; ++sc) {
     const int t0 = chunk * RB_CHUNK + sc * RBM_SUB;
