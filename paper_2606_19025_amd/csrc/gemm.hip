@@ -18,9 +18,9 @@
 // device-side offsets; no host read-back), the last two ragged in K.
 //
 // bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulation in a persistent
-// kernel with 256 x 256 block tiles (128 x 256 for the kinds with a heavy
-// epilogue) fed from an LDS ring by global -> LDS DMA (details at
-// gemm_bf16_kernel and Cfg).  One launch per GEMM kind
+// kernel with 256 x 256 block tiles of 8 waves fed from an LDS ring by
+// global -> LDS DMA (details at gemm_bf16_kernel and Cfg).  One launch per
+// GEMM kind
 // covers up to two expert sets (routed and shared experts).
 // fp32: a plain 64x64 SIMT tile (4x4 outputs per thread) with the same
 // epilogues; used for fp32 layers.
@@ -252,26 +252,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 //
-// Persistent: one 256-thread block per CU loops over output tiles.  Block tile
-// 256 x 256; the 4 waves form a 2 x 2 grid and each owns a 128 x 128 sub-tile
-// = 4 x 4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane), so
-// LDS read traffic stays at 8 KB per 16 MFMAs.  (Half-height 128 x 256 tiles,
-// see Cfg: two blocks per CU, 64 x 128 per wave = 2 x 4 MFMA tiles.)
+// Persistent: one 512-thread block per CU loops over output tiles.  Block tile
+// 256 x 256; the 8 waves (two per SIMD) form a 4 x 2 grid and each owns a
+// 64 x 128 sub-tile = 2 x 4 v_mfma_f32_32x32x16_bf16 tiles (128 fp32
+// accumulators per lane), reading 6 fragments (6 KB per wave) per 8 MFMAs.
 //
 // Operands stream through a ring of NS LDS stages of one k-step (GK) each,
-// filled with 16-byte global -> LDS DMA: full M-ragged tiles NS = 2 stages of
-// GK = 64 (64 KB each), weight-gradient tiles NS = 4 stages of GK = 32 (32 KB
-// each), half-height tiles NS = 3 stages of GK = 32 (24 KB each).  A
-// k-step is GK / 16 k16-steps; per k-step and wave:
-//   k16-steps 0 .. GK/16 - 2: 16 MFMAs each (8 for half-height tiles),
-//   interleaved with the LDS reads of the next k16-step
+// filled with 16-byte global -> LDS DMA: M-ragged kinds NS = 2 stages of
+// GK = 64 (64 KB each), weight-gradient kinds NS = 4 stages of GK = 32
+// (32 KB each).  A k-step is GK / 16 k16-steps; per k-step and wave:
+//   k16-steps 0 .. GK/16 - 2: 8 MFMAs each, interleaved with the LDS reads of
+//   the next k16-step
 //   wait for own DMA of k-step kt+1 (vmcnt leaves the later k-steps' loads in
 //   flight) and for the LDS reads, barrier (stage kt+1 complete, stage kt
 //   free)
 //   last k16-step: its MFMAs, interleaved with the LDS reads of k-step kt+1's
 //   k16-step 0 and the DMA of k-step kt+NS into stage kt
-// So every load has NS - 1 k-steps less one k16-step (about 48 MFMAs per wave
-// for full tiles) to land.
+// So every load has NS - 1 k-steps less one k16-step to land.
 // Every k-step issues the same number of DMA loads (past the last k-step the
 // last one is loaded again into an unused stage) so vmcnt counting is uniform;
 // the ring is drained (vmcnt(0)) before a block moves to its next tile.
@@ -279,8 +276,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // Tile order (see tile_decode): bands of GROUP_M m-tiles (2 to 8, per kind,
 // see Cfg).  Workgroups are dealt to the 8 XCDs round-robin by id, so block b
 // works on tiles of the ranges assigned to XCD b % 8 (an eighth of each set's
-// tiles): the 32 (64 half-height) tiles an XCD runs at a time form a band
-// rectangle whose operand panels its L2 serves.  Output tiles
+// tiles): the 32 tiles an XCD runs at a time form a band rectangle whose
+// operand panels its L2 serves.  Output tiles
 // end in an epilogue: bf16 results are staged through the drained ring so
 // global accesses are whole 16-byte chunks; fp32 weight gradients are stored
 // (or added) straight from the accumulators.
@@ -305,38 +302,36 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 constexpr int GT = 256;                     // block tile width (N), and height (M) of full tiles
 constexpr int N_XCD = 8;
 
-// Tile configuration per kind.  The kinds with a heavy elementwise epilogue
-// (GU_FWD / UP_FWD write two outputs per element, DHH_BWD / DH_BWD read one or
-// two more) use 128 x 256 tiles, two blocks per CU, each wave 64 x 128 (128
-// accumulators): a ragged expert group then pads at most 127 rows instead of
-// 255 and the epilogue per tile is half as long.  Measured on the
-// fine-grained workload: GU_FWD 7 % and DHH_BWD 6 % faster than with
-// 256 x 256 tiles; DOWN_FWD and DX_BWD (light epilogues, longer K) were 7 %
-// and 3 % slower that way, so they and the K-ragged kinds keep 256 x 256
-// tiles with one block per CU.
-// Full M-ragged tiles (DOWN_FWD, DX_BWD) take k-steps of 64 in a ring of two
-// 64 KB stages: every DMA load then fetches whole 128-byte row pieces (half
-// the L2 requests of 64-byte pieces); measured against k-steps of 32 in four
-// stages, DOWN_FWD 6-10 % and DX_BWD 1-2 % faster.  The weight-gradient kinds
-// keep k-steps of 32 in four stages (equal on the fine-grained workload, 2-6 %
-// faster on the mid-size one, and a ragged K pads at most 31 rows), and so do
-// half-height tiles (two blocks of three 24 KB stages fill the LDS).
+// Tile configuration per kind.  Every kind runs 256 x 256 block tiles with 8
+// waves (two per SIMD), one block per CU; each wave owns 64 x 128 of the tile
+// (2 x 4 MFMA tiles, 128 accumulators).  Measured on the fine-grained
+// workload against 4 waves of 128 x 128 (one per SIMD): DOWN_FWD and DX_BWD
+// 9 % faster, the weight-gradient kinds level; and against 128 x 256 tiles at
+// two blocks per CU (which padded ragged groups less): GU_FWD 9 % and DHH_BWD
+// 3 % faster.  The second wave of a SIMD issues MFMAs while the first waits
+// on its operand loads; the 1.5x fragment reads per MFMA of the narrower wave
+// tile cost less than that gains.
+// M-ragged tiles take k-steps of 64 in a ring of two 64 KB stages: every DMA
+// load then fetches whole 128-byte row pieces (half the L2 requests of 64-byte
+// pieces; DOWN_FWD 6-10 % and DX_BWD 1-2 % faster than k-steps of 32).  The
+// weight-gradient kinds keep k-steps of 32 in four 32 KB stages (equal on the
+// fine-grained workload, 2-6 % faster on the mid-size one, and a ragged K
+// pads at most 31 rows).
 template <int KIND>
 struct Cfg {
-  static constexpr bool HALF =
-      KIND == GU_FWD || KIND == DHH_BWD || KIND == UP_FWD || KIND == DH_BWD;
-  static constexpr int GK = HALF || !Kind<KIND>::MRAG ? 32 : 64;  // k-step
+  static constexpr int NW = 8;                     // waves per block (two per SIMD)
+  static constexpr int GK = Kind<KIND>::MRAG ? 64 : 32;  // k-step
   static constexpr int KS = GK / 16;               // k16-steps per k-step
-  static constexpr int BM = HALF ? 128 : 256;      // block tile rows
-  static constexpr int WM = BM / 2;                // wave sub-tile rows
+  static constexpr int BM = GT;                    // block tile rows
+  static constexpr int WM = BM / (NW / 2);         // wave sub-tile rows (64)
   static constexpr int MI = WM / 32;               // 32-row MFMA tiles per wave
-  static constexpr int NS = HALF ? 3 : (GK == 64 ? 2 : 4);  // LDS ring stages
+  static constexpr int NS = GK == 64 ? 2 : 4;      // LDS ring stages
   static constexpr int A_BYTES = BM * GK * 2;      // A operand of one stage
   static constexpr int B_BYTES = GT * GK * 2;      // B operand of one stage
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int LDS = NS * STAGE;
-  static constexpr int DMA_A = A_BYTES / 4096;     // 16-byte DMA loads per wave and k-step
-  static constexpr int DMA_B = B_BYTES / 4096;
+  static constexpr int DMA_A = A_BYTES / (1024 * NW);  // 16-byte DMA loads per wave and k-step
+  static constexpr int DMA_B = B_BYTES / (1024 * NW);
   static constexpr int DMA_N = DMA_A + DMA_B;
   static constexpr int DMA_MAX = DMA_A > DMA_B ? DMA_A : DMA_B;
   static constexpr int EPI_WAVE = WM * 256;        // epilogue staging per wave
@@ -345,8 +340,7 @@ struct Cfg {
   static constexpr int GROUP = (KIND == GU_FWD || KIND == UP_FWD || KIND == DOWN_FWD) ? 8
                                : (KIND == DHH_BWD || KIND == DH_BWD || KIND == DX_BWD) ? 4
                                                                                         : 2;
-  static constexpr int OCC = HALF ? 2 : 1;         // blocks per CU
-  static_assert(4 * EPI_WAVE <= LDS, "epilogue staging exceeds the ring");
+  static_assert(NW * EPI_WAVE <= LDS, "epilogue staging exceeds the ring");
 };
 
 
@@ -391,28 +385,29 @@ struct DmaPtrs {
 template <int GK>
 DEVI int kc_swz(int r) { return GK == 32 ? (r >> 2) & 3 : (r >> 1) & 7; }
 
-template <int GK, int N, class RowPtr>
+template <int GK, int NW, int N, class RowPtr>
 DEVI void dma_kc_init(DmaPtrs<N>& d, const RowPtr& row_ptr, int w) {
   constexpr int CPR = GK / 8;  // chunks per row
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int row = (i * 4 + w) * (64 / CPR) + lane / CPR;
+    const int row = (i * NW + w) * (64 / CPR) + lane / CPR;
     d.p[i] = row_ptr(row) + ((lane % CPR) ^ kc_swz<GK>(row)) * 8;
   }
 }
 
-DEVI int mn_row(int i, int w) { return (i * 4 + w) * 2 + ((threadIdx.x & 63) >> 5); }
+template <int NW>
+DEVI int mn_row(int i, int w) { return (i * NW + w) * 2 + ((threadIdx.x & 63) >> 5); }
 DEVI int mn_col(int row) {
   const int ps = threadIdx.x & 31;
   return (((ps >> 1) ^ (2 * (row & 3))) * 16) + (ps & 1) * 8;
 }
 
-template <int N, class ElemPtr>
+template <int NW, int N, class ElemPtr>
 DEVI void dma_mn_init(DmaPtrs<N>& d, const ElemPtr& elem_ptr, int w, int k0) {
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    const int row = mn_row(i, w);
+    const int row = mn_row<NW>(i, w);
     d.p[i] = elem_ptr(k0 + row, mn_col(row));
   }
 }
@@ -446,8 +441,8 @@ DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
   return __builtin_bit_cast(bf16x8_t, both);
 }
 
-// Epilogue staging.  A wave's bf16 sub-tile (128 columns; 128 rows, or 64 for
-// half-height tiles) occupies rows of 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
+// Epilogue staging.  A wave's 64 x 128 bf16 sub-tile occupies 64 rows of
+// 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
 // the key is a bijection on r mod 32, so the accumulator writes (32 rows at
 // one unit per half-wave) hit 32 distinct bank pairs, and rows 2m, 2m+1
 // differ in key bit 3, so the SwiGLU reads (8 chunks of two rows per 16
@@ -565,7 +560,7 @@ struct GemmLaunch {
 };
 
 template <int KIND>
-__global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaunch L) {
+__global__ __launch_bounds__(64 * Cfg<KIND>::NW, Cfg<KIND>::NW / 4) void gemm_bf16_kernel(GemmLaunch L) {
   using K_ = Kind<KIND>;
   using C_ = Cfg<KIND>;
   constexpr int MI = C_::MI, WM = C_::WM, NS = C_::NS, GK = C_::GK, KS = C_::KS;
@@ -661,11 +656,11 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
     // tail k-step
     DmaPtrs<C_::DMA_A> da, ta;
     DmaPtrs<C_::DMA_B> db, tb;
-    if constexpr (K_::A_KC) dma_kc_init<GK>(da, a_row, wave); else dma_mn_init(da, a_elem, wave, 0);
-    if constexpr (K_::B_KC) dma_kc_init<GK>(db, b_row, wave); else dma_mn_init(db, b_elem, wave, 0);
+    if constexpr (K_::A_KC) dma_kc_init<GK, C_::NW>(da, a_row, wave); else dma_mn_init<C_::NW>(da, a_elem, wave, 0);
+    if constexpr (K_::B_KC) dma_kc_init<GK, C_::NW>(db, b_row, wave); else dma_mn_init<C_::NW>(db, b_elem, wave, 0);
     if constexpr (!K_::MRAG) {
-      dma_mn_init(ta, a_elem, wave, n_full * GK);
-      dma_mn_init(tb, b_elem, wave, n_full * GK);
+      dma_mn_init<C_::NW>(ta, a_elem, wave, n_full * GK);
+      dma_mn_init<C_::NW>(tb, b_elem, wave, n_full * GK);
     }
     const long a_step = K_::A_KC ? GK : (long)GK * a.lda;
     const long b_step = K_::B_KC ? GK : (long)GK * a.ldb;
@@ -679,13 +674,13 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
         const int ia = i < C_::DMA_A ? i : 0;
         const bf16_t* pa = da.p[ia] + ks * a_step;
         if constexpr (!K_::MRAG) pa = tail ? ta.p[ia] : pa;
-        load_to_lds(pa, la + (i * 4 + wave) * 1024);
+        load_to_lds(pa, la + (i * C_::NW + wave) * 1024);
       }
       if (i < C_::DMA_B) {
         const int ib = i < C_::DMA_B ? i : 0;
         const bf16_t* pb = db.p[ib] + ks * b_step;
         if constexpr (!K_::MRAG) pb = tail ? tb.p[ib] : pb;
-        load_to_lds(pb, la + C_::A_BYTES + (i * 4 + wave) * 1024);
+        load_to_lds(pb, la + C_::A_BYTES + (i * C_::NW + wave) * 1024);
       }
     };
 
@@ -768,7 +763,7 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
     WAIT_VMCNT(0);  // drain the ring before the next tile
 
     // epilogue: accumulator (i, j) register 4q + t holds
-    //   C[wm*128 + 32i + lane%32][wn*128 + 32j + 8q + 4(lane/32) + t]
+    //   C[wm*WM + 32i + lane%32][wn*128 + 32j + 8q + 4(lane/32) + t]
     if constexpr (KIND == DWD || KIND == DWGU) {
       // fp32 weight gradient of group g, 16 bytes per lane straight from the
       // accumulators
@@ -796,7 +791,7 @@ __global__ __launch_bounds__(256, Cfg<KIND>::OCC) void gemm_bf16_kernel(GemmLaun
       // bf16 outputs go through LDS so that every global access is a whole
       // 16-byte chunk and a wave instruction covers 256 contiguous bytes of a
       // row (4 rows) instead of 16 bytes of 32 rows.  Each wave transposes its
-      // 128x128 sub-tile in a private 32 KB region (the drained ring).  The
+      // 64 x 128 sub-tile in a private 16 KB region (the drained ring).  The
       // outputs (and the G/U that the dSwiGLU epilogue reads) are touched
       // once here, so they go past the caches (nontemporal: measured 2-4 %
       // faster for DHH_BWD, DX_BWD and DOWN_FWD; the fp32 weight gradients
@@ -980,7 +975,7 @@ template <int KIND>
 hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
                     int* counters = nullptr, int* zero = nullptr, int n_zero = 0) {
   if (bf16) {
-    // persistent: at most Cfg::OCC blocks per CU, a multiple of N_XCD blocks
+    // persistent: at most one block per CU, a multiple of N_XCD blocks
     GemmLaunch L{};
     L.s0 = sets[0];
     L.n_sets = n_sets;
@@ -1001,9 +996,9 @@ hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
       if (swap) std::swap(L.s0, L.s1);
     }
     if (tiles == 0 && n_zero == 0) return hipSuccess;
-    long blocks = std::min<long>((long)num_cus() * Cfg<KIND>::OCC, std::max<long>(tiles, 1));
+    long blocks = std::min<long>((long)num_cus(), std::max<long>(tiles, 1));
     blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
-    MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 256, 0, s>>>(L));
+    MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 64 * Cfg<KIND>::NW, 0, s>>>(L));
     return hipGetLastError();
   }
   for (int i = 0; i < n_sets; ++i) {
