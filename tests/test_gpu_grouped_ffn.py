@@ -3,8 +3,8 @@ oracle, with the group sizes chosen around the GEMM tile edges.
 
 The layer tests reach only the group sizes that routing happens to give.
 Here they are set directly: empty groups (also first and last), one row, and
-one below, at and above the 128-row (half-height) and 256-row (full) tile
-heights; hidden and model widths that leave a partial 256-wide column tile;
+one below, at and above 128 rows (a wave pair's share of a tile) and the
+256-row tile height; hidden and model widths that leave a partial 256-wide column tile;
 K extents (d, H, 2H) of one to several k-steps of 32 and 64 and ragged token
 counts for the weight-gradient kinds; the backward both without a workspace
 (static tile dealing, no split) and with one (dynamic dealing, split-K of a
