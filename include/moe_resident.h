@@ -150,7 +150,9 @@ int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
  * same input are one expert with their hidden units concatenated.
  * offsets is a device array of n_groups + 1 non-decreasing int32 values; each
  * group is clamped to [0, cap].
- * Limits (bf16): d % 64 == 0, H % 64 == 0.
+ * Limits (bf16): d % 64 == 0, H % 64 == 0, and each operand below 4 GiB
+ * (2 cap max(d, 2H) and 2 n_groups 2H d bytes below 2^32 - 16: the GEMMs
+ * address operands with 32-bit byte offsets); MOE_ERR_UNSUPPORTED otherwise.
  */
 int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_down, int dtype,
                         int cap, int d, int H, int n_groups, const int32_t* offsets,

@@ -279,6 +279,14 @@ int check_set(const moe_ffn_set& f, int dtype, int d, bool fwd) {
     REQUIRE(f.cap == 0 || (f.dyp && f.xp && f.gu && f.h && f.dgu && f.dxp),
             "dyp, xp, gu, h, dgu and dxp must not be NULL");
   }
+  if (dtype == MOE_BF16) {
+    // the bf16 GEMMs address each operand with 32-bit byte offsets
+    const long rows_bytes = 2L * f.cap * std::max<long>(d, 2L * f.H);
+    const long w_bytes = 2L * f.n_groups * 2L * f.H * d;
+    SUPPORT(std::max(rows_bytes, w_bytes) < 0xFFFFFFF0L,
+            "bf16 expert operands must each stay below 4 GiB (cap = %d, H = %d, groups = %d)",
+            f.cap, f.H, f.n_groups);
+  }
   for (const void* p : {f.xp, f.w_gate_up, f.w_down, (const void*)f.gu, (const void*)f.h,
                         (const void*)f.yp, f.dyp, (const void*)f.dgu, (const void*)f.dxp,
                         (const void*)f.dw_gate_up, (const void*)f.dw_down})

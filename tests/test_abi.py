@@ -93,6 +93,12 @@ def test_grouped_ffn_rejects_unsupported_shapes(lib):
     assert call_status(f, p, p, p, B.MOE_BF16, 64, 128, 128, 2, None, p, p, p) == ERR_ARG  # offsets
     g = lib.moe_grouped_ffn_bwd
     assert call_status(g, p, p, p, p, p, p, B.MOE_BF16, 64, 128, 128, -1, p, p, p, p, p, 0) == ERR_ARG
+    # bf16 operands of 4 GiB or more (32-bit DMA offsets): rows (cap x 2H)
+    # and weights (groups x 2H x d)
+    assert call_status(f, p, p, p, B.MOE_BF16, 1 << 20, 2048, 1024, 1, p, p, p, p) == ERR_UNSUPPORTED
+    assert call_status(f, p, p, p, B.MOE_BF16, 64, 4096, 4096, 64, p, p, p, p) == ERR_UNSUPPORTED
+    assert call_status(g, p, p, p, p, p, p, B.MOE_BF16, 1 << 20, 2048, 1024, 1, p, p, p, p, p,
+                       0) == ERR_UNSUPPORTED
 
 
 def test_combine_and_unpermute_reject_bad_arguments(lib):
