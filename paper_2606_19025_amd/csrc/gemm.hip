@@ -357,6 +357,21 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 #define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(waitcnt_imm((n), 15))
 #define WAIT_LGKMCNT(n) __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, (n)))
 
+// Wait until at most PER * min(n, MAXN) vector memory operations are
+// outstanding (n >= 0, wave-uniform; s_waitcnt takes only an immediate).
+template <int PER, int MAXN>
+DEVI void wait_vm_groups(int n) {
+  if constexpr (MAXN > 0) {
+    if (n >= MAXN) {
+      WAIT_VMCNT(PER * MAXN);
+      return;
+    }
+    wait_vm_groups<PER, MAXN - 1>(n);
+  } else {
+    WAIT_VMCNT(0);
+  }
+}
+
 // 16-byte global -> LDS DMA through a buffer resource: lane l reads the 16
 // bytes at byte offset off of the operand and writes them to lds_base + 16 l
 // (lds_base must be wave-uniform).  An offset at or past the resource's
@@ -757,13 +772,18 @@ __global__ __launch_bounds__(64 * Cfg<KIND>::NW, Cfg<KIND>::NW / 4) void gemm_bf
     };
 
     bf16x8_t af0[MI], bf0[4], af1[MI], bf1[4];
+    // Only k-steps below nk are loaded: every wait below lets the loads of
+    // the real k-steps issued after the one it needs stay in flight, DMA_N
+    // per k-step (vector memory loads complete in issue order).
     if (nk > 0) {
 #pragma unroll
       for (int p = 0; p < NS; ++p)
+        if (p < nk) {
 #pragma unroll
-        for (int i = 0; i < C_::DMA_MAX; ++i) dma(min(p, nk - 1), p, i);
-      // own DMA of k-step 0 done (NS - 1 k-steps' loads may stay in flight)
-      WAIT_VMCNT(C_::DMA_N * (NS - 1));
+          for (int i = 0; i < C_::DMA_MAX; ++i) dma(p, p, i);
+        }
+      // own DMA of k-step 0 done (k-steps 1 .. min(NS, nk) - 1 may stay in flight)
+      wait_vm_groups<C_::DMA_N, NS - 1>(nk - 1);
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < NF; ++q) read_frag(lds, 0, q, af0, bf0);
@@ -779,13 +799,16 @@ __global__ __launch_bounds__(64 * Cfg<KIND>::NW, Cfg<KIND>::NW / 4) void gemm_bf
         else kstep(af1, bf1, stage, s + 1, af0, bf0, -1, 0);
       }
       WAIT_LGKMCNT(0);
-      WAIT_VMCNT(C_::DMA_N * (NS - 2));
+      // k-step kt + 1 landed (kt + 2 .. min(kt + NS, nk) - 1 may stay in flight)
+      wait_vm_groups<C_::DMA_N, NS - 2>(nk - 2 - kt);
       __syncthreads();
       // the last one reads k16-step 0 of the next stage and refills this one
+      // (with k-step kt + NS if there is one)
+      const int refill = kt + NS < nk ? kt + NS : -1;
       if constexpr ((KS - 1) % 2 == 0)
-        kstep(af0, bf0, stage_next, 0, af1, bf1, min(kt + NS, nk - 1), st);
+        kstep(af0, bf0, stage_next, 0, af1, bf1, refill, st);
       else
-        kstep(af1, bf1, stage_next, 0, af0, bf0, min(kt + NS, nk - 1), st);
+        kstep(af1, bf1, stage_next, 0, af0, bf0, refill, st);
     }
     WAIT_VMCNT(0);  // drain the ring before the next tile
 
