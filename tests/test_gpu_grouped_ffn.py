@@ -38,6 +38,11 @@ CASES = {
     "one-large-group-splitk": ([4100], 256, 256, "swiglu", True, 0),
     "one-large-group-splitk-acc": ([4100], 256, 256, "swiglu", True, 1),
     "wide-d": ([200, 700, 1], 1024, 128, "swiglu", True, 0),
+    # one to four k-steps per tile for every kind (d = H = 64: one 64-deep
+    # k-step for the forward GEMMs; 1-4 k-steps of 32 rows for the weight
+    # gradients), so the load ring is never full
+    "short-k": ([33, 64, 65, 96, 97, 0, 1, 31, 32], 64, 64, "swiglu", True, 0),
+    "short-k-silu": ([33, 64, 65, 96, 97, 0, 1, 31, 32], 64, 64, "silu", False, 0),
 }
 
 
