@@ -84,6 +84,9 @@ def parse():
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="make one plain device-to-device copy of a known size before the "
                          "steps, the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
+    ap.add_argument("--copy-baseline", action="store_true",
+                    help="also time torch's device-to-device copy and a read-only sum of "
+                         "1 GiB (the HBM rates a plain streaming kernel reaches on the box)")
     return ap.parse_args()
 
 
@@ -502,6 +505,34 @@ def main():
                                       frac=round(ach / PEAK_HBM_GBS, 5), launches=launches,
                                       avg_us=round(1e3 * tot / max(launches, 1), 3))
 
+    hbm_copy = None
+    if args.copy_baseline:
+        # context for the HBM-bound kernels: a plain streaming copy (2 GiB
+        # moved) and a read-only sum of 1 GiB, event-timed, best of 5 after
+        # one untimed call
+        nb = 1 << 30
+        src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+
+        def best_ms(fn):
+            ts = []
+            for _ in range(6):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            return min(ts[1:])
+
+        t_copy = best_ms(lambda: dst.copy_(src))
+        t_read = best_ms(lambda: src.sum())
+        hbm_copy = {"bytes": nb, "copy_GBps": round(2 * nb / t_copy / 1e6, 1),
+                    "read_GBps": round(nb / t_read / 1e6, 1), "peak": PEAK_HBM_GBS}
+        del src, dst
+        log(f"[bench] copy baseline {hbm_copy}")
+
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import moe_oracle as O
@@ -552,6 +583,7 @@ def main():
         "cpu_baseline": cpu,
         "kernels": kernels,
         "kernels_cold": kernels_cold,
+        "hbm_copy": hbm_copy,
     }
     print(json.dumps(out), flush=True)
 
