@@ -358,7 +358,8 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 #define WAIT_LGKMCNT(n) __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, (n)))
 
 // Wait until at most PER * min(n, MAXN) vector memory operations are
-// outstanding (n >= 0, wave-uniform; s_waitcnt takes only an immediate).
+// outstanding; n <= 0 waits for all of them (n wave-uniform: s_waitcnt takes
+// only an immediate).
 template <int PER, int MAXN>
 DEVI void wait_vm_groups(int n) {
   if constexpr (MAXN > 0) {
