@@ -129,6 +129,26 @@ int moe_dispatch(const void* x, int dtype, int T, int d, int k, int E_r,
                  hipStream_t stream);
 
 /*
+ * moe_dispatch without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, outputs, limits and results as
+ * moe_dispatch; the workspace is a library-owned device array of
+ * MOE_DISPATCH_NOALLOC_MAX_WS bytes per device, reserved from the library's
+ * load until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); its first call on a device resolves
+ * that device's array address.  Returns MOE_ERR_UNSUPPORTED when
+ * moe_dispatch_workspace_size(T, k, E_r) exceeds MOE_DISPATCH_NOALLOC_MAX_WS
+ * (for example E_r = 256 with T above 130816), MOE_ERR_HIP when the array
+ * cannot be resolved.  All calls on one device share its array: calls that
+ * overlap in time on one device (different streams, or host threads) race
+ * and give undefined results; calls ordered on one stream are safe.
+ */
+#define MOE_DISPATCH_NOALLOC_MAX_WS ((size_t)1 << 20)
+int moe_dispatch_noalloc(const void* x, int dtype, int T, int d, int k, int E_r,
+                         const int32_t* topk_local, int32_t* counts, int32_t* offsets,
+                         int32_t* perm, int32_t* inv_perm, void* xp, hipStream_t stream);
+
+/*
  * Backward of the gather (un-permute):
  *   dx[t,:] (+)= sum_{j: inv_perm[t,j] >= 0} dxp[inv_perm[t,j], :]
  * A token whose routes are all ghosts gets exactly 0 (or keeps dx when

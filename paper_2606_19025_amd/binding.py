@@ -21,7 +21,7 @@ GATES = {"softmax_topk": MOE_GATE_SOFTMAX_TOPK, "softmax": MOE_GATE_SOFTMAX,
 
 EXPORTS = [
     "moe_last_error", "moe_abi_version", "moe_route_mask", "moe_route_bwd_workspace_size",
-    "moe_route_bwd", "moe_dispatch_workspace_size", "moe_dispatch", "moe_dispatch_bwd",
+    "moe_route_bwd", "moe_dispatch_workspace_size", "moe_dispatch", "moe_dispatch_noalloc", "moe_dispatch_bwd",
     "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_grouped_ffn_fwd_sets",
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
@@ -53,6 +53,7 @@ _SIGS = {
                            _I, _P, _Z, _P]),
     "moe_dispatch_workspace_size": (_Z, [_I, _I, _I]),
     "moe_dispatch": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+    "moe_dispatch_noalloc": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P]),
     "moe_dispatch_bwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _I, _P]),
     "moe_grouped_ffn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_grouped_ffn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P,
@@ -189,6 +190,13 @@ def moe_dispatch(x, dtype, T, d, k, E_r, topk_local, counts, offsets, perm, inv_
     return _check("moe_dispatch", lib().moe_dispatch(
         _ptr(x), dtype, T, d, k, E_r, _ptr(topk_local), _ptr(counts), _ptr(offsets), _ptr(perm),
         _ptr(inv_perm), _ptr(xp), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def moe_dispatch_noalloc(x, dtype, T, d, k, E_r, topk_local, counts, offsets, perm, inv_perm, xp,
+                         stream=None):
+    return _check("moe_dispatch_noalloc", lib().moe_dispatch_noalloc(
+        _ptr(x), dtype, T, d, k, E_r, _ptr(topk_local), _ptr(counts), _ptr(offsets), _ptr(perm),
+        _ptr(inv_perm), _ptr(xp), _stream(stream)))
 
 
 def moe_dispatch_bwd(dxp, dtype, T, d, k, cap, inv_perm, dx, accumulate, stream=None):

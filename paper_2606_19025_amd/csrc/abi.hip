@@ -239,6 +239,28 @@ int moe_dispatch(const void* x, int dtype, int T, int d, int k, int E_r,
                     "moe_dispatch");
 }
 
+int moe_dispatch_noalloc(const void* x, int dtype, int T, int d, int k, int E_r,
+                         const int32_t* topk_local, int32_t* counts, int32_t* offsets,
+                         int32_t* perm, int32_t* inv_perm, void* xp, hipStream_t stream) {
+  int r;
+  if ((r = check_dtype(dtype)) != MOE_OK) return r;
+  REQUIRE(T >= 0 && d >= 1 && k >= 1, "bad sizes T = %d, d = %d, k = %d", T, d, k);
+  REQUIRE(E_r >= 0 && E_r <= 256, "E_r = %d must be in [0, 256]", E_r);
+  REQUIRE(offsets && (E_r == 0 || counts), "counts and offsets must not be NULL");
+  REQUIRE(T == 0 || (x && topk_local && inv_perm && (E_r == 0 || (perm && xp))),
+          "x, topk_local, perm, inv_perm and xp must not be NULL");
+  const size_t need = moe::dispatch_ws_bytes(T, k, E_r);
+  SUPPORT(need <= MOE_DISPATCH_NOALLOC_MAX_WS,
+          "moe_dispatch_noalloc: T = %d, E_r = %d need a %zu-byte workspace, above the "
+          "library's %zu-byte array (use moe_dispatch with a workspace)",
+          T, E_r, need, (size_t)MOE_DISPATCH_NOALLOC_MAX_WS);
+  if ((r = check_rows16(d, "x", x)) != MOE_OK) return r;
+  if ((r = check_rows16(d, "xp", xp)) != MOE_OK) return r;
+  return hip_status(moe::launch_dispatch_noalloc(x, dtype == MOE_BF16, T, d, k, E_r, topk_local,
+                                                 counts, offsets, perm, inv_perm, xp, stream),
+                    "moe_dispatch_noalloc");
+}
+
 int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
                      const int32_t* inv_perm, void* dx, int accumulate, hipStream_t stream) {
   int r;

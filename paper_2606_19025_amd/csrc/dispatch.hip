@@ -14,9 +14,23 @@
 //      writes it to every slot of that token (16-byte vector accesses).
 // Combine, combine backward and un-permute are token-major too: one wave per
 // token, 16-byte loads of the routed rows, fp32 accumulation.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 #include "timing.h"
+
+// Workspace of the allocation-free dispatch (moe_dispatch_noalloc): a
+// file-scope device array, one copy per device, whose device address is
+// resolved once per device with that device current (dispatch_scratch).  In
+// host code the array's name is a host-side stand-in, so only the resolved
+// address is ever passed to a kernel.  The counting sort overwrites every word
+// it reads (per-block histograms, then bases), so the array needs no clearing
+// between calls; calls that overlap on one device share it and race.
+// External linkage on purpose: a static array is a LOCAL symbol of the device
+// code object, which the runtime's lookup by name (hipGetSymbolAddress) does
+// not find.
+__device__ __attribute__((aligned(256))) char moe_dispatch_scratch[MOE_DISPATCH_NOALLOC_MAX_WS];
 
 namespace moe {
 namespace {
@@ -463,6 +477,38 @@ hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r
           static_cast<const float*>(x), T, d, k, cap, inv_perm, static_cast<float*>(xp)));
   }
   return hipGetLastError();
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t dispatch_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(moe_dispatch_scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_dispatch_noalloc(const void* x, int bf16, int T, int d, int k, int E_r,
+                                   const int32_t* local, int32_t* counts, int32_t* offsets,
+                                   int32_t* perm, int32_t* inv_perm, void* xp, hipStream_t s) {
+  void* ws = nullptr;
+  const hipError_t e = dispatch_scratch(&ws);
+  if (e != hipSuccess) return e;
+  return launch_dispatch(x, bf16, T, d, k, E_r, local, counts, offsets, perm, inv_perm, xp, ws, s);
 }
 
 hipError_t launch_dispatch_bwd(const void* dxp, int bf16, int T, int d, int k, int cap,

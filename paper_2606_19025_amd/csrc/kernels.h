@@ -26,6 +26,13 @@ size_t dispatch_ws_bytes(int T, int k, int E_r);
 hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r,
                            const int32_t* local, int32_t* counts, int32_t* offsets,
                            int32_t* perm, int32_t* inv_perm, void* xp, void* ws, hipStream_t s);
+// The same counting sort with its workspace in a library-owned device array
+// of kDispatchScratchBytes (one per device); dispatch_ws_bytes() of the call
+// must not exceed it.
+constexpr size_t kDispatchScratchBytes = MOE_DISPATCH_NOALLOC_MAX_WS;
+hipError_t launch_dispatch_noalloc(const void* x, int bf16, int T, int d, int k, int E_r,
+                                   const int32_t* local, int32_t* counts, int32_t* offsets,
+                                   int32_t* perm, int32_t* inv_perm, void* xp, hipStream_t s);
 hipError_t launch_dispatch_bwd(const void* dxp, int bf16, int T, int d, int k, int cap,
                                const int32_t* inv_perm, void* dx, int accumulate, hipStream_t s);
 
