@@ -114,6 +114,13 @@ def algorithmic_work(cfg, n, t_act, s, expert="swiglu"):
         w["gemm_dx_bwd"] = ("flop", sum(2.0 * m * h * d for m, h in rows))
         w["gemm_dwgu"] = ("flop", sum(2.0 * m * h * d for m, h in rows))
         del w["gemm_gu_fwd"]
+    # bf16 layers run the backward GEMMs as two launches of two kinds each
+    # (dHh with dW_d, dX with dW_gu)
+    first = "gemm_dh_bwd" if expert == "silu" else "gemm_dhh_bwd"
+    w["gemm_dh_dwd" if expert == "silu" else "gemm_dhh_dwd"] = (
+        "flop", w[first][1] + w["gemm_dwd"][1])
+    w["gemm_dx_dwgu"] = ("flop", w["gemm_dx_bwd"][1] + w["gemm_dwgu"][1])
+    w["zero_counters"] = ("byte", 64)
     # routing / data movement: bytes (HBM-bound)
     w["route_fwd"] = ("byte", T * d * s + E * d * s + T * E * 4 + 3 * T * k * 4)
     w["dispatch_count"] = ("byte", T * k * 4)

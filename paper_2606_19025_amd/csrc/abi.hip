@@ -280,6 +280,7 @@ static int check_ffn(int dtype, int cap, int d, int H, int n_groups, const int32
   if ((r = check_dtype(dtype)) != MOE_OK) return r;
   REQUIRE(cap >= 0 && d >= 1 && H >= 1, "bad sizes cap = %d, d = %d, H = %d", cap, d, H);
   REQUIRE(n_groups >= 0, "n_groups = %d must be >= 0", n_groups);
+  SUPPORT(n_groups <= 256, "n_groups = %d: at most 256 groups per set", n_groups);
   REQUIRE(offsets, "offsets must not be NULL");
   SUPPORT(H % 64 == 0, "H = %d must be a multiple of 64", H);
   if (dtype == MOE_BF16) SUPPORT(d % 64 == 0, "d = %d must be a multiple of 64 for bf16", d);
@@ -305,7 +306,9 @@ int check_set(const moe_ffn_set& f, int dtype, int d, bool fwd) {
     // the bf16 GEMMs address each operand with 32-bit byte offsets
     const long rows_bytes = 2L * f.cap * std::max<long>(d, 2L * f.H);
     const long w_bytes = 2L * f.n_groups * 2L * f.H * d;
-    SUPPORT(std::max(rows_bytes, w_bytes) < 0xFFFFFFF0L,
+    // and each expert's fp32 weight gradient (stored with 32-bit offsets)
+    const long dw_bytes = 4L * 2L * f.H * d;
+    SUPPORT(std::max(std::max(rows_bytes, w_bytes), dw_bytes) < 0xFFFFFFF0L,
             "bf16 expert operands must each stay below 4 GiB (cap = %d, H = %d, groups = %d)",
             f.cap, f.H, f.n_groups);
   }

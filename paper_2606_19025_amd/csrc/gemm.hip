@@ -24,6 +24,8 @@
 // covers up to two expert sets (routed and shared experts).
 // fp32: a plain 64x64 SIMT tile (4x4 outputs per thread) with the same
 // epilogues; used for fp32 layers.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "timing.h"
@@ -322,10 +324,11 @@ template <int KIND>
 struct Cfg {
   static constexpr int NW = 8;                     // waves per block (two per SIMD)
   static constexpr int GK = Kind<KIND>::MRAG ? 64 : 32;  // k-step
-  static constexpr int KS = GK / 16;               // k16-steps per k-step
+  static constexpr int K32 = GK / 32;              // k32-steps per k-step
   static constexpr int BM = GT;                    // block tile rows
   static constexpr int WM = BM / (NW / 2);         // wave sub-tile rows (64)
-  static constexpr int MI = WM / 32;               // 32-row MFMA tiles per wave
+  static constexpr int MI = WM / 16;               // 16-row MFMA tiles per wave
+  static constexpr int NJ = 128 / 16;              // 16-column MFMA tiles per wave
   static constexpr int NS = GK == 64 ? 2 : 4;      // LDS ring stages
   static constexpr int A_BYTES = BM * GK * 2;      // A operand of one stage
   static constexpr int B_BYTES = GT * GK * 2;      // B operand of one stage
@@ -372,6 +375,14 @@ DEVI void wait_vm_groups(int n) {
     WAIT_VMCNT(0);
   }
 }
+// 16-byte (b128) or 8-byte store through a buffer resource; an offset at or
+// past the resource's record count is dropped, so every lane issues the
+// store and the count of outstanding vector memory operations is known at
+// compile time.  nt: past the caches (outputs touched once).
+template <bool NT>
+DEVI void store16(__amdgpu_buffer_rsrc_t r, unsigned off, u32x4_t v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, NT ? 2 : 0);
+}
 
 // 16-byte global -> LDS DMA through a buffer resource: lane l reads the 16
 // bytes at byte offset off of the operand and writes them to lds_base + 16 l
@@ -388,6 +399,10 @@ DEVI void wait_vm_groups(int n) {
 // "m0" clobber records for the reader.
 DEVI void load_to_lds(u32x4_t rsrc, unsigned off, char* lds_base) {
   const unsigned m0 = (unsigned)(uintptr_t)(lds_void_t*)lds_base;
+  // the resource is wave-uniform; readfirstlane keeps it in SGPRs after the
+  // tile context has passed through registers the compiler treats as per-lane
+#pragma unroll
+  for (int w = 0; w < 4; ++w) rsrc[w] = __builtin_amdgcn_readfirstlane(rsrc[w]);
   asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(off), "s"(rsrc), "s"(m0)
                : "m0", "memory");
 }
@@ -395,6 +410,10 @@ DEVI void load_to_lds(u32x4_t rsrc, unsigned off, char* lds_base) {
 // the gfx9 default data format.  Every operand stays below kOOB bytes (the
 // entry points reject larger ones).
 constexpr unsigned kOOB = 0xFFFFFFF0u;
+// The same resource for the epilogue's buffer stores.
+DEVI __amdgpu_buffer_rsrc_t store_rsrc(void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)kOOB, 0x00020000);
+}
 DEVI u32x4_t make_rsrc(const void* base) {
   const uint64_t b = (uint64_t)(uintptr_t)base;
   u32x4_t r;
@@ -434,11 +453,18 @@ DEVI void dma_kc_init(DmaPtrs<N>& d, const RowPtr& row_ptr, int w, const bf16_t*
   }
 }
 
+// m/n-contiguous layout: row k holds 256 m (512 B) in 32-byte chunks; chunk c
+// sits at position c ^ mn_swz(k), so that the 8 rows (k0..k0+3 and
+// k0+8..k0+11) a half-wave of transposing fragment reads touches fall on 8
+// distinct 32-byte bank groups.
+DEVI int mn_swz(int k) { return (2 * (k & 3)) ^ ((k >> 3) & 1); }
+
 template <int NW>
 DEVI int mn_row(int i, int w) { return (i * NW + w) * 2 + ((threadIdx.x & 63) >> 5); }
+// source column of the 16-byte LDS slot this lane writes in row `row`
 DEVI int mn_col(int row) {
   const int ps = threadIdx.x & 31;
-  return (((ps >> 1) ^ (2 * (row & 3))) * 16) + (ps & 1) * 8;
+  return (((ps >> 1) ^ mn_swz(row)) * 16) + (ps & 1) * 8;
 }
 
 template <int NW, int N, class ElemPtr>
@@ -454,26 +480,31 @@ DEVI void dma_mn_init(DmaPtrs<N>& d, const ElemPtr& elem_ptr, int w, int k0, con
   }
 }
 
-// fragment of rows/cols [mb, mb+32) at k16-step s, k-contiguous layout
+// MFMA 16x16x32 operand fragment of rows/cols [mb, mb+16) at k32-step s:
+// lane l holds index mb + l%16 and k = 32 s + 8 (l/16) + 0..7.
+// k-contiguous layout: one 16-byte read (16-byte chunk 4 s + l/16 of the row)
 template <int GK>
 DEVI bf16x8_t frag_kc(const char* lds_op, int mb, int s) {
   const int lane = threadIdx.x & 63;
-  const int row = mb + (lane & 31);
-  const int kc = s * 2 + (lane >> 5);
+  const int row = mb + (lane & 15);
+  const int kc = s * 4 + (lane >> 4);
   return *reinterpret_cast<const bf16x8_t*>(lds_op + row * (GK * 2) +
                                             ((kc ^ kc_swz<GK>(row)) << 4));
 }
 
-// same fragment from the m/n-contiguous layout with two transposing reads
+// the same fragment from the m/n-contiguous layout with two transposing
+// reads: in each 16-lane group g, lane i points at row k0 + i/4 (k0 = 32 s +
+// 8 g + 4 h) and columns mb + 4 (i%4) .. +3, and receives column mb + i of
+// rows k0 .. k0+3
 DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, i = lane & 15;
-  const int mn = mb + 16 * (g & 1) + 4 * (i & 3);
+  const int mn = mb + 4 * (i & 3);
   s16x4_t v[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int k = s * 16 + 8 * (g >> 1) + 4 * h + (i >> 2);
-    const int pc = (mn >> 4) ^ (2 * (k & 3));
+    const int k = s * 32 + 8 * g + 4 * h + (i >> 2);
+    const int pc = (mn >> 4) ^ mn_swz(k);
     const char* p = lds_op + k * 512 + pc * 32 + (mn & 15) * 2;
     v[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p));
   }
@@ -484,14 +515,14 @@ DEVI bf16x8_t frag_mn(const char* lds_op, int mb, int s) {
 }
 
 // Epilogue staging.  A wave's 64 x 128 bf16 sub-tile occupies 64 rows of
-// 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r):
-// the key is a bijection on r mod 32, so the accumulator writes (32 rows at
-// one unit per half-wave) hit 32 distinct bank pairs, and rows 2m, 2m+1
-// differ in key bit 3, so the SwiGLU reads (8 chunks of two rows per 16
-// lanes) fall on disjoint chunks.  A 16-byte chunk c is read back from chunk
-// c ^ (key >> 1), halves swapped when the key is odd.
-
-DEVI int epi_key(int r) { return ((r & 1) << 3) | ((r >> 1) & 7) | (r & 16); }
+// 256 B.  The 8-byte unit u (4 columns) of row r sits at unit u ^ epi_key(r),
+// epi_key(r) = 2 f(r mod 16) with f a bijection of 0..15 (bits b3 b2 b1 b0 of
+// r -> b3 b0 b2 b1).  The accumulator writes (16 rows x units 4j, 4j+1 per
+// half-wave) hit 32 distinct bank pairs because the keys are 16 distinct even
+// values; a 16-byte chunk c reads back whole from chunk c ^ (key >> 1); and
+// rows 2m, 2m+1 differ in key bit 3, so the SwiGLU reads (chunks 0-3 and 8-11
+// of two rows per 16 lanes) fall on disjoint chunks.
+DEVI int epi_key(int r) { return 2 * ((r & 8) | ((r & 1) << 2) | ((r >> 1) & 3)); }
 
 DEVI void epi_put(char* reg, int row, int u, float v0, float v1, float v2, float v3) {
   bf16x4_t o = {(bf16_t)v0, (bf16_t)v1, (bf16_t)v2, (bf16_t)v3};
@@ -500,9 +531,7 @@ DEVI void epi_put(char* reg, int row, int u, float v0, float v1, float v2, float
 
 DEVI bf16x8_t epi_get(const char* reg, int row, int c) {
   const int key = epi_key(row);
-  u32x4_t v = *reinterpret_cast<const u32x4_t*>(reg + row * 256 + ((c ^ (key >> 1)) << 4));
-  if (key & 1) v = __builtin_shufflevector(v, v, 2, 3, 0, 1);
-  return __builtin_bit_cast(bf16x8_t, v);
+  return *reinterpret_cast<const bf16x8_t*>(reg + row * 256 + ((c ^ (key >> 1)) << 4));
 }
 
 // Hardware exp2 / reciprocal (about 1 ulp of fp32); their results are rounded
@@ -519,27 +548,81 @@ DEVI float silu_fast(float g) { return g * sigmoid_fast(g); }
 // (32 / GROUP_M) rectangle and share GROUP_M A panels and 32 / GROUP_M B
 // panels in L2.
 
+// Group table of one set, staged in LDS once per block: the group offsets
+// clamped to [0, cap] (c), their running maximum (b: group g of an M-ragged
+// kind is rows [b[g], b[g+1])) and the number of m-tiles before group g (p).
+constexpr int kMaxGroups = 256;
+struct GroupTable {
+  int c[kMaxGroups + 1], b[kMaxGroups + 1], p[kMaxGroups + 1];
+};
+
+DEVI int wave_incl_max(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v = max(v, u);
+  }
+  return v;
+}
+DEVI int wave_incl_sum(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// Fill t from set a (one wave; n_groups <= kMaxGroups).
+DEVI void build_group_table(const GemmArgs& a, GroupTable& t) {
+  const int lane = threadIdx.x & 63;
+  const int ng = a.n_groups;
+  int run = 0;
+  for (int g0 = 0; g0 <= ng; g0 += 64) {
+    const int g = g0 + lane;
+    const int c = g <= ng ? clamp_row(a.offsets[g], a.cap) : 0;
+    int m = wave_incl_max(g <= ng ? c : 0);
+    if (g0 > 0) m = max(m, run);
+    if (g <= ng) {
+      t.c[g] = c;
+      t.b[g] = m;
+    }
+    run = __shfl(m, 63, 64);
+  }
+  WAIT_LGKMCNT(0);  // the wave's own table writes (lanes read their neighbours')
+  int acc = 0;
+  for (int g0 = 0; g0 <= ng; g0 += 64) {
+    const int g = g0 + lane;
+    const int tiles = g < ng ? (t.b[g + 1] - t.b[g] + GT - 1) / GT : 0;
+    const int inc = wave_incl_sum(tiles);
+    if (g <= ng) t.p[g] = acc + inc - tiles;
+    acc += __shfl(inc, 63, 64);
+  }
+}
+
+// Output tiles form an m_tiles x n_tiles grid (M-ragged kinds: m-tiles of all
+// groups in group order; K-ragged kinds: (group, split part, m-tile)
+// triples).
 template <int KIND>
-DEVI int m_tile_count(const GemmArgs& a) {
+DEVI int m_tile_count(const GemmArgs& a, const GroupTable& t) {
   constexpr int BM = Cfg<KIND>::BM;
   if constexpr (Kind<KIND>::MRAG) {
-    int tiles = 0;
-    int b = clamp_row(a.offsets[0], a.cap);
-    for (int g = 0; g < a.n_groups; ++g) {
-      int e = clamp_row(a.offsets[g + 1], a.cap);
-      if (e < b) e = b;
-      tiles += (e - b + BM - 1) / BM;
-      b = e;
-    }
-    return tiles;
+    return t.p[a.n_groups];
   } else {
     return a.n_groups * max(1, a.ksplit) * ((a.M + BM - 1) / BM);
   }
 }
 
+// Linear tile t walks bands of GROUP_M m-tiles: inside a band m varies
+// fastest, then n, so any 32 consecutive tiles cover a GROUP_M x
+// (32 / GROUP_M) rectangle and share GROUP_M A panels and 32 / GROUP_M B
+// panels in L2.  The m-tile's group is found by all lanes of the wave at once
+// (the number of groups whose m-tiles all lie before it).
 template <int KIND>
-DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& tl,
-                      int& tile_n) {
+DEVI void tile_decode(const GemmArgs& a, const GroupTable& gt, int t, int m_tiles, int n_tiles,
+                      Tile& tl, int& tile_n) {
   constexpr int BM = Cfg<KIND>::BM, GROUP_M = Cfg<KIND>::GROUP;
   const int band = t / (GROUP_M * n_tiles);
   const int first_m = band * GROUP_M;
@@ -549,24 +632,18 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
   tile_n = r / band_m;
   tl.n0 = tile_n * GT;
   if constexpr (Kind<KIND>::MRAG) {
-    int mt = q;
-    int b = clamp_row(a.offsets[0], a.cap);
-    for (int g = 0; g < a.n_groups; ++g) {
-      int e = clamp_row(a.offsets[g + 1], a.cap);
-      if (e < b) e = b;
-      const int tiles = (e - b + BM - 1) / BM;
-      if (mt < tiles) {
-        tl.g = g;
-        tl.row0 = b + mt * BM;
-        tl.rows = min(BM, e - tl.row0);
-        tl.m0 = 0;
-        tl.split = 0;
-        return;
-      }
-      mt -= tiles;
-      b = e;
+    const int lane = threadIdx.x & 63;
+    int g = 0;
+    for (int g0 = 0; g0 < a.n_groups; g0 += 64) {
+      const int gg = g0 + lane;
+      g += __builtin_popcountll(__ballot(gg < a.n_groups && gt.p[gg + 1] <= q));
     }
-    tl.g = 0; tl.row0 = 0; tl.rows = 0; tl.m0 = 0; tl.split = 0;  // not reached for t < count
+    g = __builtin_amdgcn_readfirstlane(g);
+    tl.g = g;
+    tl.row0 = gt.b[g] + (q - gt.p[g]) * BM;
+    tl.rows = min(BM, gt.b[g + 1] - tl.row0);
+    tl.m0 = 0;
+    tl.split = 0;
   } else {
     // (group, split part, m-tile); part p of a group of rows [b, e) is
     // [b + len p / S, b + len (p + 1) / S)
@@ -576,8 +653,8 @@ DEVI void tile_decode(const GemmArgs& a, int t, int m_tiles, int n_tiles, Tile& 
     tl.g = gs / S;
     tl.split = gs % S;
     tl.m0 = (q % mt_per_g) * BM;
-    const int b = clamp_row(a.offsets[tl.g], a.cap);
-    int e = clamp_row(a.offsets[tl.g + 1], a.cap);
+    const int b = gt.c[tl.g];
+    int e = gt.c[tl.g + 1];
     if (e < b) e = b;
     const long len = e - b;
     tl.row0 = b + (int)(len * tl.split / S);
@@ -590,46 +667,86 @@ DEVI int col_tiles(const GemmArgs& a) {
   return ((KIND == GU_FWD ? 2 * a.H : a.N) + GT - 1) / GT;
 }
 
-// Kernel argument of the bf16 kernel: one or two sets of groups of the same
-// GEMM kind (the routed experts and the merged shared experts) in one launch,
-// so that the tiles of both fill the CUs together.
+// Kernel argument of the bf16 kernel: up to kMaxSets sets of groups, each of
+// GEMM kind KA or KB (kind_b[s] != 0), whose tiles share one persistent
+// launch - the routed and the merged shared experts of one kind, and in the
+// backward two independent kinds (dHh with dW_d, dX with dW_gu), so that
+// tiles of different lengths fill the CUs together, keep the CUs out of step
+// (their epilogue stores do not all fall at once) and fill each other's last
+// round.
+constexpr int kMaxSets = 4;
 struct GemmLaunch {
-  GemmArgs s0, s1;
+  GemmArgs s[kMaxSets];
+  int kind_b[kMaxSets];
   int n_sets;
   int* counters;  // non-null: per-XCD tile counters (zero at launch) for dynamic dealing
-  int* zero;      // block 0 zeroes zero[0..n_zero) (the next launches' counters)
-  int n_zero;
 };
 
-template <int KIND>
-__global__ __launch_bounds__(64 * Cfg<KIND>::NW, Cfg<KIND>::NW / 4) void gemm_bf16_kernel(GemmLaunch L) {
-  using K_ = Kind<KIND>;
-  using C_ = Cfg<KIND>;
-  constexpr int MI = C_::MI, WM = C_::WM, NS = C_::NS, GK = C_::GK, KS = C_::KS;
-  __shared__ __attribute__((aligned(1024))) char lds[C_::LDS];
+template <int K>
+using KindTag = std::integral_constant<int, K>;
+
+// One output tile: its decode and the operands' DMA addressing (the first
+// DMA_A / DMA_B entries are used; the tail entries by the K-ragged kinds).
+struct TileCtx {
+  int set;
+  bool kb;  // of kind KB
+  Tile tl;
+  int tile_n, nk, n_full;
+  unsigned a_step, b_step;
+  u32x4_t rs_a, rs_b;
+  DmaPtrs<4> da, db;
+  DmaPtrs<2> ta, tb;
+};
+
+template <int KA, int KB>
+__global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
+  static_assert(Cfg<KA>::NW == 8 && Cfg<KB>::NW == 8, "8 waves per block");
+  static_assert(Cfg<KA>::LDS == Cfg<KB>::LDS, "one LDS ring size per launch");
+  constexpr int NW = 8, MI = Cfg<KA>::MI, NJ = Cfg<KA>::NJ, WM = Cfg<KA>::WM;
+  __shared__ __attribute__((aligned(1024))) char lds[Cfg<KA>::LDS];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const bf16_t* zero16 = reinterpret_cast<const bf16_t*>(&kZero16);
+
+  // runs f(KindTag<K>) for the kind of a set
+  auto for_kind = [&](bool kb, auto&& f) {
+    if constexpr (KA == KB) {
+      f(KindTag<KA>{});
+    } else {
+      if (kb) f(KindTag<KB>{});
+      else f(KindTag<KA>{});
+    }
+  };
+
   // XCD-aware assignment (the grid is a multiple of N_XCD blocks): XCD x takes
   // the x-th eighth of every set's tile range (so each XCD gets an equal share
-  // of each set's work), set 0 first.  Its blocks deal these tiles
+  // of each set's work), in set order.  Its blocks deal these tiles
   // round-robin, or - with counters - each block takes the XCD's next tile
   // when it finishes one (tiles of unequal K then balance across blocks).
   const int per_xcd = gridDim.x / N_XCD;
   const int xcd = blockIdx.x % N_XCD;
-  if (L.zero && blockIdx.x == 0 && (int)threadIdx.x < L.n_zero) L.zero[threadIdx.x] = 0;
-
-  const int nt0 = col_tiles<KIND>(L.s0);
-  const int mt0 = m_tile_count<KIND>(L.s0);
-  const int tot0 = mt0 * nt0;
-  const int nt1 = L.n_sets > 1 ? col_tiles<KIND>(L.s1) : 0;
-  const int mt1 = L.n_sets > 1 ? m_tile_count<KIND>(L.s1) : 0;
-  const int tot1 = mt1 * nt1;
-  const int lo0 = (int)((long)tot0 * xcd / N_XCD);
-  const int cnt0 = (int)((long)tot0 * (xcd + 1) / N_XCD) - lo0;
-  const int lo1 = (int)((long)tot1 * xcd / N_XCD);
-  const int cnt1 = (int)((long)tot1 * (xcd + 1) / N_XCD) - lo1;
+  __shared__ GroupTable gtab[kMaxSets];
+  if (wave < L.n_sets) build_group_table(L.s[wave], gtab[wave]);
+  __syncthreads();
+  int mt[kMaxSets], ntl[kMaxSets], lo[kMaxSets], pre[kMaxSets + 1];
+  pre[0] = 0;
+#pragma unroll
+  for (int q = 0; q < kMaxSets; ++q) {
+    int tot = 0;
+    mt[q] = ntl[q] = 0;
+    if (q < L.n_sets) {
+      for_kind(L.kind_b[q] != 0, [&](auto kc) {
+        constexpr int KIND = decltype(kc)::value;
+        ntl[q] = col_tiles<KIND>(L.s[q]);
+        mt[q] = m_tile_count<KIND>(L.s[q], gtab[q]);
+      });
+      tot = mt[q] * ntl[q];
+    }
+    lo[q] = (int)((long)tot * xcd / N_XCD);
+    pre[q + 1] = pre[q] + (int)((long)tot * (xcd + 1) / N_XCD) - lo[q];
+  }
+  const int total = pre[kMaxSets];
   const bool dyn = L.counters != nullptr;
   __shared__ int next_tile[2];  // double-buffered broadcast of the dealt tile
   int it_parity = 0;
@@ -641,355 +758,452 @@ __global__ __launch_bounds__(64 * Cfg<KIND>::NW, Cfg<KIND>::NW / 4) void gemm_bf
       nxt = atomicAdd(L.counters + xcd, 1);
     }
     __syncthreads();
-    i = next_tile[0];
+    // wave-uniform: every value derived from the tile index stays scalar
+    i = __builtin_amdgcn_readfirstlane(next_tile[0]);
   } else {
     i = (int)(blockIdx.x / N_XCD);
   }
 
-  while (i < cnt0 + cnt1) {
-    const bool second = i >= cnt0;
-    GemmArgs a;
-    if (second) a = L.s1; else a = L.s0;
-    const int t = second ? lo1 + (i - cnt0) : lo0 + i;
-    const int m_tiles = second ? mt1 : mt0;
-    const int n_tiles = second ? nt1 : nt0;
-    Tile tl;
-    int tile_n;
-    tile_decode<KIND>(a, t, m_tiles, n_tiles, tl, tile_n);
-    const bf16_t* A = static_cast<const bf16_t*>(a.A);
-    const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
-    const int Kd = K_::MRAG ? a.K : tl.rows;
-    const int nk = (Kd + GK - 1) / GK;
-    const int n_full = Kd / GK;  // k-steps without a ragged tail
-    const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
-
-    // operand pointers; out-of-range M/N indices are clamped to valid memory
-    // (outputs not stored), out-of-range k-rows read zeros
-    auto a_row = [&](int r) -> const bf16_t* {  // M-ragged A, k-contiguous
-      return A + (size_t)min(tl.row0 + r, last_row) * a.lda;
-    };
-    auto a_elem = [&](int k, int c) -> const bf16_t* {  // TN A(i = m0 + c, k)
-      if (k >= Kd) return zero16;
-      const int m = (tl.m0 + c + 8 <= a.M) ? tl.m0 + c : 0;
-      return A + (size_t)(tl.row0 + k) * a.lda + m;
-    };
-    auto b_row = [&](int r) -> const bf16_t* {  // NT B rows
-      if constexpr (KIND == GU_FWD) {
-        bool ok;
-        int br = gu_brow<GT>(tile_n, r, a.H, ok);
-        if (!ok) br = 0;
-        return B + (size_t)br * a.ldb;
-      } else {
-        return B + (size_t)min(tl.n0 + r, a.N - 1) * a.ldb;
-      }
-    };
-    auto b_elem = [&](int k, int c) -> const bf16_t* {  // NN / TN B(k, n = n0 + c)
-      const int n = (tl.n0 + c + 8 <= a.N) ? tl.n0 + c : 0;
-      if constexpr (K_::MRAG) {
-        return B + (size_t)k * a.ldb + n;
-      } else {
+  auto make_ctx = [&](int it, TileCtx& c) {
+    int q = 0;
+#pragma unroll
+    for (int r = 1; r < kMaxSets; ++r)
+      if (it >= pre[r]) q = r;
+    c.set = q;
+    c.kb = L.kind_b[q] != 0;
+    const int t = lo[q] + (it - pre[q]);
+    for_kind(c.kb, [&](auto kc) {
+      constexpr int KIND = decltype(kc)::value;
+      using K_ = Kind<KIND>;
+      constexpr int GK = Cfg<KIND>::GK;
+      const GemmArgs& a = L.s[q];
+      tile_decode<KIND>(a, gtab[q], t, mt[q], ntl[q], c.tl, c.tile_n);
+      const Tile tl = c.tl;
+      const int tile_n = c.tile_n;
+      const bf16_t* A = static_cast<const bf16_t*>(a.A);
+      const bf16_t* B = static_cast<const bf16_t*>(a.B) + (K_::MRAG ? (size_t)tl.g * a.b_gs : 0);
+      const int Kd = K_::MRAG ? a.K : tl.rows;
+      c.nk = (Kd + GK - 1) / GK;
+      c.n_full = Kd / GK;  // k-steps without a ragged tail
+      const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
+      // operand pointers; out-of-range M/N indices are clamped to valid
+      // memory (outputs not stored), out-of-range k-rows read zeros
+      auto a_row = [&](int r) -> const bf16_t* {  // M-ragged A, k-contiguous
+        return A + (size_t)min(tl.row0 + r, last_row) * a.lda;
+      };
+      auto a_elem = [&](int k, int col) -> const bf16_t* {  // TN A(i = m0 + col, k)
         if (k >= Kd) return zero16;
-        return B + (size_t)(tl.row0 + k) * a.ldb + n;
-      }
-    };
-
-    // DMA addresses at k-step 0 (k-contiguous operands advance by GK
-    // elements, m/n-contiguous ones by GK rows per k-step) and of the ragged
-    // tail k-step
-    DmaPtrs<C_::DMA_A> da, ta;
-    DmaPtrs<C_::DMA_B> db, tb;
-    if constexpr (K_::A_KC) dma_kc_init<GK, C_::NW>(da, a_row, wave, A); else dma_mn_init<C_::NW>(da, a_elem, wave, 0, A);
-    if constexpr (K_::B_KC) dma_kc_init<GK, C_::NW>(db, b_row, wave, B); else dma_mn_init<C_::NW>(db, b_elem, wave, 0, B);
-    if constexpr (!K_::MRAG) {
-      dma_mn_init<C_::NW>(ta, a_elem, wave, n_full * GK, A);
-      dma_mn_init<C_::NW>(tb, b_elem, wave, n_full * GK, B);
-    }
-    const u32x4_t rs_a = make_rsrc(A), rs_b = make_rsrc(B);
-    const unsigned a_step = 2u * (K_::A_KC ? GK : (unsigned)GK * a.lda);
-    const unsigned b_step = 2u * (K_::B_KC ? GK : (unsigned)GK * a.ldb);
-
-    // DMA load i of each operand (A: i < DMA_A, B: i < DMA_B) for k-step ks
-    // into stage st
-    auto dma = [&](int ks, int st, int i) {
-      char* la = lds + st * C_::STAGE;
-      const bool tail = !K_::MRAG && ks >= n_full;
-      if (i < C_::DMA_A) {
-        const int ia = i < C_::DMA_A ? i : 0;
-        unsigned pa = da.p[ia] + ks * a_step;
-        if constexpr (!K_::MRAG) pa = tail ? ta.p[ia] : pa;
-        load_to_lds(rs_a, pa, la + (i * C_::NW + wave) * 1024);
-      }
-      if (i < C_::DMA_B) {
-        const int ib = i < C_::DMA_B ? i : 0;
-        unsigned pb = db.p[ib] + ks * b_step;
-        if constexpr (!K_::MRAG) pb = tail ? tb.p[ib] : pb;
-        load_to_lds(rs_b, pb, la + C_::A_BYTES + (i * C_::NW + wave) * 1024);
-      }
-    };
-
-    auto read_frag = [&](const char* stage, int s, int idx, bf16x8_t* af, bf16x8_t* bfr) {
-      // in the order the next k16-step's MFMAs consume them: idx 0 = A
-      // fragment 0, 1..4 = B fragments 0..3, 5.. = A fragments 1..MI-1
-      if (idx == 0 || idx > 4) {
-        const int f = idx == 0 ? 0 : idx - 4;
-        af[f] = K_::A_KC ? frag_kc<GK>(stage, wm * WM + f * 32, s)
-                         : frag_mn(stage, wm * WM + f * 32, s);
-      } else {
-        const int f = idx - 1;
-        const char* lb = stage + C_::A_BYTES;
-        bfr[f] = K_::B_KC ? frag_kc<GK>(lb, wn * 128 + f * 32, s)
-                          : frag_mn(lb, wn * 128 + f * 32, s);
-      }
-    };
-
-    f32x16_t acc[MI][4];
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-
-    // One k16-step: 4 MI MFMAs on (A_c, B_c) in 2 MI chunks of two; chunk q
-    // also reads fragments [q NF / NQ, (q + 1) NF / NQ) of the next k16-step
-    // (NF = MI + 4 of them, from stage_n) into (A_n, B_n) and, for
-    // q < DMA_MAX when dma_ks >= 0, issues DMA load q of k-step dma_ks into
-    // stage dma_st.  sched_barrier(0) fences keep this order, so each fragment
-    // read has a whole k16-step to land and the compiler's waits fall at the
-    // first use in the next k16-step.
-    constexpr int NQ = 2 * MI, NF = MI + 4;
-    static_assert(C_::DMA_MAX <= NQ, "DMA loads per k-step exceed the chunks");
-    auto kstep = [&](const bf16x8_t* A_c, const bf16x8_t* B_c, const char* stage_n, int s_n,
-                     bf16x8_t* A_n, bf16x8_t* B_n, int dma_ks, int dma_st) {
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        if (dma_ks >= 0 && q < C_::DMA_MAX) dma(dma_ks, dma_st, q);
-#pragma unroll
-        for (int f = q * NF / NQ; f < (q + 1) * NF / NQ; ++f) read_frag(stage_n, s_n, f, A_n, B_n);
-        const int i = q >> 1, j0 = 2 * (q & 1);
-        acc[i][j0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_c[j0], A_c[i], acc[i][j0], 0, 0, 0);
-        acc[i][j0 + 1] =
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_c[j0 + 1], A_c[i], acc[i][j0 + 1], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-
-    bf16x8_t af0[MI], bf0[4], af1[MI], bf1[4];
-    // Only k-steps below nk are loaded: every wait below lets the loads of
-    // the real k-steps issued after the one it needs stay in flight, DMA_N
-    // per k-step (vector memory loads complete in issue order).
-    if (nk > 0) {
-#pragma unroll
-      for (int p = 0; p < NS; ++p)
-        if (p < nk) {
-#pragma unroll
-          for (int i = 0; i < C_::DMA_MAX; ++i) dma(p, p, i);
+        const int m = (tl.m0 + col + 8 <= a.M) ? tl.m0 + col : 0;
+        return A + (size_t)(tl.row0 + k) * a.lda + m;
+      };
+      auto b_row = [&](int r) -> const bf16_t* {  // NT B rows
+        if constexpr (KIND == GU_FWD) {
+          bool ok;
+          int br = gu_brow<GT>(tile_n, r, a.H, ok);
+          if (!ok) br = 0;
+          return B + (size_t)br * a.ldb;
+        } else {
+          return B + (size_t)min(tl.n0 + r, a.N - 1) * a.ldb;
         }
-      // own DMA of k-step 0 done (k-steps 1 .. min(NS, nk) - 1 may stay in flight)
-      wait_vm_groups<C_::DMA_N, NS - 1>(nk - 1);
-      __syncthreads();
+      };
+      auto b_elem = [&](int k, int col) -> const bf16_t* {  // NN / TN B(k, n = n0 + col)
+        const int n = (tl.n0 + col + 8 <= a.N) ? tl.n0 + col : 0;
+        if constexpr (K_::MRAG) {
+          return B + (size_t)k * a.ldb + n;
+        } else {
+          if (k >= Kd) return zero16;
+          return B + (size_t)(tl.row0 + k) * a.ldb + n;
+        }
+      };
+      // DMA addresses at k-step 0 (k-contiguous operands advance by GK
+      // elements, m/n-contiguous ones by GK rows per k-step) and of the
+      // ragged tail k-step
+      constexpr int DA = Cfg<KIND>::DMA_A, DB = Cfg<KIND>::DMA_B;
+      static_assert(DA <= 4 && DB <= 4 && (K_::MRAG || (DA <= 2 && DB <= 2)), "DMA slots");
+      DmaPtrs<DA> da, db;
+      if constexpr (K_::A_KC) dma_kc_init<GK, NW>(da, a_row, wave, A); else dma_mn_init<NW>(da, a_elem, wave, 0, A);
+      if constexpr (K_::B_KC) dma_kc_init<GK, NW>(db, b_row, wave, B); else dma_mn_init<NW>(db, b_elem, wave, 0, B);
 #pragma unroll
-      for (int q = 0; q < NF; ++q) read_frag(lds, 0, q, af0, bf0);
-    }
-    for (int kt = 0; kt < nk; ++kt) {
-      const int st = kt % NS;
-      const char* stage = lds + st * C_::STAGE;
-      const char* stage_next = lds + ((kt + 1) % NS) * C_::STAGE;
-      // k16-steps 0 .. KS-2 read the next fragments from this stage
+      for (int x = 0; x < DA; ++x) c.da.p[x] = da.p[x];
 #pragma unroll
-      for (int s = 0; s < KS - 1; ++s) {
-        if (s % 2 == 0) kstep(af0, bf0, stage, s + 1, af1, bf1, -1, 0);
-        else kstep(af1, bf1, stage, s + 1, af0, bf0, -1, 0);
+      for (int x = 0; x < DB; ++x) c.db.p[x] = db.p[x];
+      if constexpr (!K_::MRAG) {
+        DmaPtrs<DA> ta;
+        DmaPtrs<DB> tb;
+        dma_mn_init<NW>(ta, a_elem, wave, c.n_full * GK, A);
+        dma_mn_init<NW>(tb, b_elem, wave, c.n_full * GK, B);
+#pragma unroll
+        for (int x = 0; x < DA; ++x) c.ta.p[x] = ta.p[x];
+#pragma unroll
+        for (int x = 0; x < DB; ++x) c.tb.p[x] = tb.p[x];
       }
-      WAIT_LGKMCNT(0);
-      // k-step kt + 1 landed (kt + 2 .. min(kt + NS, nk) - 1 may stay in flight)
-      wait_vm_groups<C_::DMA_N, NS - 2>(nk - 2 - kt);
-      __syncthreads();
-      // the last one reads k16-step 0 of the next stage and refills this one
-      // (with k-step kt + NS if there is one)
-      const int refill = kt + NS < nk ? kt + NS : -1;
-      if constexpr ((KS - 1) % 2 == 0)
-        kstep(af0, bf0, stage_next, 0, af1, bf1, refill, st);
-      else
-        kstep(af1, bf1, stage_next, 0, af0, bf0, refill, st);
-    }
-    WAIT_VMCNT(0);  // drain the ring before the next tile
+      c.rs_a = make_rsrc(A);
+      c.rs_b = make_rsrc(B);
+      c.a_step = 2u * (K_::A_KC ? GK : (unsigned)GK * a.lda);
+      c.b_step = 2u * (K_::B_KC ? GK : (unsigned)GK * a.ldb);
+    });
+  };
 
-    // epilogue: accumulator (i, j) register 4q + t holds
-    //   C[wm*WM + 32i + lane%32][wn*128 + 32j + 8q + 4(lane/32) + t]
-    if constexpr (KIND == DWD || KIND == DWGU) {
-      // fp32 weight gradient of group g, 16 bytes per lane straight from the
-      // accumulators
-      const int r_in = lane & 31;
-      const int c_in = 4 * (lane >> 5);
+  // DMA load i of each operand (A: i < DMA_A, B: i < DMA_B) of tile c for
+  // k-step ks into stage st
+  auto dma = [&](auto kc, const TileCtx& c, int ks, int st, int i) {
+    constexpr int KIND = decltype(kc)::value;
+    using C_ = Cfg<KIND>;
+    constexpr bool MRAG = Kind<KIND>::MRAG;
+    char* la = lds + st * C_::STAGE;
+    const bool tail = !MRAG && ks >= c.n_full;
+    if (i < C_::DMA_A) {
+      unsigned pa = c.da.p[i] + ks * c.a_step;
+      if constexpr (!MRAG) pa = tail ? c.ta.p[i < 2 ? i : 0] : pa;
+      load_to_lds(c.rs_a, pa, la + (i * NW + wave) * 1024);
+    }
+    if (i < C_::DMA_B) {
+      unsigned pb = c.db.p[i] + ks * c.b_step;
+      if constexpr (!MRAG) pb = tail ? c.tb.p[i < 2 ? i : 0] : pb;
+      load_to_lds(c.rs_b, pb, la + C_::A_BYTES + (i * NW + wave) * 1024);
+    }
+  };
+  // the first NS k-steps of tile c into the ring (only k-steps below nk)
+  auto prologue = [&](const TileCtx& c) {
+    for_kind(c.kb, [&](auto kc) {
+      constexpr int KIND = decltype(kc)::value;
+      using C_ = Cfg<KIND>;
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int row = wm * WM + i * 32 + r_in;
-        if (tl.m0 + row >= a.M) continue;
+      for (int p = 0; p < C_::NS; ++p)
+        if (p < c.nk) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+          for (int q = 0; q < C_::DMA_MAX; ++q) dma(kc, c, p, p, q);
+        }
+    });
+  };
+
+  TileCtx cur;
+  if (i < total) {
+    make_ctx(i, cur);
+    prologue(cur);
+  }
+  while (i < total) {
+    // ---- main loop and epilogue of the current tile
+    for_kind(cur.kb, [&](auto kc) {
+      constexpr int KIND = decltype(kc)::value;
+      using K_ = Kind<KIND>;
+      using C_ = Cfg<KIND>;
+      constexpr int NS = C_::NS, GK = C_::GK, K32 = C_::K32;
+      const int nk = cur.nk;
+      f32x4_t acc[MI][NJ];
+      bf16x8_t out[16];   // staged bf16 results (epilogue part 1)
+      bool late = false;  // results left for part 2's stores
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int col = tl.n0 + wn * 128 + j * 32 + 8 * q + c_in;
-            if (col >= a.N) continue;
-            float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
-                       (size_t)tl.split * a.c_split + (size_t)(tl.m0 + row) * a.ldc + col;
-            f32x4_t o = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                         acc[i][j][4 * q + 3]};
-            if (a.accumulate) o += *reinterpret_cast<const f32x4_t*>(c);
-            *reinterpret_cast<f32x4_t*>(c) = o;
+      for (int a_ = 0; a_ < MI; ++a_)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[a_][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+      // fragment f of the wave's A rows (wm WM + 16 f ..) or B columns
+      // (wn 128 + 16 f ..) at k32-step s of a stage
+      auto frag_a = [&](const char* stage, int s, int f) -> bf16x8_t {
+        return K_::A_KC ? frag_kc<GK>(stage, wm * WM + f * 16, s)
+                        : frag_mn(stage, wm * WM + f * 16, s);
+      };
+      auto frag_b = [&](const char* stage, int s, int f) -> bf16x8_t {
+        const char* lb = stage + C_::A_BYTES;
+        return K_::B_KC ? frag_kc<GK>(lb, wn * 128 + f * 16, s)
+                        : frag_mn(lb, wn * 128 + f * 16, s);
+      };
+
+      // One k32-step s of `stage`: NJ chunks, chunk j issuing the MI MFMAs of
+      // B fragment j (acc[i][j] += A_i B_j).  B fragments pass through a ring
+      // of four register sets Bq, each read three chunks before its use
+      // (chunk j reads fragment j + 3, from the next k32-step - at s_n of
+      // stage_n - for j >= NJ - 3); the next k32-step's A fragments are read
+      // in chunks 4..7 into A_n.  On a k-step's last k32-step (`last`), chunk
+      // 4 first reads the stage's final fragment, then waits for the wave's
+      // LDS reads and for its DMA of k-step kt + 1, and takes the barrier
+      // after which every wave is done with this stage: the fragments of the
+      // next k32-step come from stage_n (k-step kt + 1), and the DMA loads of
+      // k-step dma_ks (if >= 0) refill this stage (dma_st) in chunks
+      // 4 .. 4 + DMA_MAX - 1.  sched_barrier(0) fences keep this order, so the
+      // compiler's LDS waits fall at each fragment's first use.
+      static_assert(C_::DMA_MAX <= NJ - 4, "DMA loads per k-step exceed the chunks");
+      static_assert(MI == 4, "A fragments are read in chunks 4..7");
+      auto k32step = [&](const char* stage, int s, const bf16x8_t* A_c, bf16x8_t* A_n,
+                         bf16x8_t* Bq, const char* stage_n, int s_n, bool last, int kt,
+                         int dma_ks, int dma_st) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          if (j + 3 < NJ) Bq[(j + 3) % 4] = frag_b(stage, s, j + 3);
+          if (last && j == 4) {
+            WAIT_LGKMCNT(0);
+            // k-step kt + 1 landed (kt + 2 .. min(kt + NS, nk) - 1 may stay in flight)
+            wait_vm_groups<C_::DMA_N, NS - 2>(nk - 2 - kt);
+            __syncthreads();
           }
+          if (j + 3 >= NJ) Bq[(j + 3) % 4] = frag_b(stage_n, s_n, j + 3 - NJ);
+          if (j >= 4) A_n[j - 4] = frag_a(stage_n, s_n, j - 4);
+          if (last && dma_ks >= 0 && j >= 4 && j - 4 < C_::DMA_MAX) dma(kc, cur, dma_ks, dma_st, j - 4);
+#pragma unroll
+          for (int ii = 0; ii < MI; ++ii)
+            acc[ii][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Bq[j % 4], A_c[ii], acc[ii][j], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      };
+
+      bf16x8_t af0[MI], af1[MI], bq[4];
+      if (nk > 0) {
+        // own DMA of k-step 0 done (k-steps 1 .. min(NS, nk) - 1 may stay in flight)
+        wait_vm_groups<C_::DMA_N, NS - 1>(nk - 1);
+        __syncthreads();
+#pragma unroll
+        for (int f = 0; f < MI; ++f) af0[f] = frag_a(lds, 0, f);
+#pragma unroll
+        for (int f = 0; f < 3; ++f) bq[f] = frag_b(lds, 0, f);
       }
-    } else {
-      // bf16 outputs go through LDS so that every global access is a whole
-      // 16-byte chunk and a wave instruction covers 256 contiguous bytes of a
-      // row (4 rows) instead of 16 bytes of 32 rows.  Each wave transposes its
-      // 64 x 128 sub-tile in a private 16 KB region (the drained ring).  The
-      // outputs (and the G/U that the dSwiGLU epilogue reads) are touched
-      // once here, so they go past the caches (nontemporal: measured 2-4 %
-      // faster for DHH_BWD, DX_BWD and DOWN_FWD; the fp32 weight gradients
-      // below are not, they were 1.4-1.7x slower that way).
-      __syncthreads();  // every wave is done with the ring
-      char* reg = lds + wave * C_::EPI_WAVE;
+      // k-step kt: K32 k32-steps, the last of which reads the next stage and
+      // refills this one (with k-step kt + NS if there is one).  A fragments
+      // alternate between af0 and af1 every k32-step.
+      auto kstep = [&](int kt, bf16x8_t* A_even, bf16x8_t* A_odd) {
+        const int st = kt % NS;
+        const char* stage = lds + st * C_::STAGE;
+        const char* stage_next = lds + ((kt + 1) % NS) * C_::STAGE;
+        const int refill = kt + NS < nk ? kt + NS : -1;
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int row = i * 32 + (lane & 31);
-            const int u = 8 * j + 2 * q + (lane >> 5);
-            epi_put(reg, row, u, acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                    acc[i][j][4 * q + 3]);
-          }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region is wave-private
+        for (int s = 0; s < K32; ++s) {
+          const bool last = s == K32 - 1;
+          bf16x8_t* A_c = s % 2 == 0 ? A_even : A_odd;
+          bf16x8_t* A_n = s % 2 == 0 ? A_odd : A_even;
+          k32step(stage, s, A_c, A_n, bq, last ? stage_next : stage, last ? 0 : s + 1, last, kt,
+                  last ? refill : -1, st);
+        }
+      };
+      if constexpr (K32 % 2 == 0) {
+        for (int kt = 0; kt < nk; ++kt) kstep(kt, af0, af1);
+      } else {
+        for (int kt = 0; kt < nk; kt += 2) {
+          kstep(kt, af0, af1);
+          if (kt + 1 < nk) kstep(kt + 1, af1, af0);
+        }
+      }
+      // (the last k-step's wait took every DMA load of this tile)
+
+      // ---- epilogue, part 1: results into registers (or, for the kinds
+      // that read memory and the accumulating weight gradients, the whole
+      // epilogue).  Accumulator (i, j) register t
+      // holds C[wm*WM + 16i + lane%16][wn*128 + 16j + 4(lane/16) + t]
+      const GemmArgs& a = L.s[cur.set];
+      const Tile tl = cur.tl;
       const int row_lim = tl.rows - wm * WM;  // rows of this wave's sub-tile to store
-      if constexpr (KIND == GU_FWD) {
-        // region row: [G h0..31 | U h0..31 | G h32..63 | U h32..63] of the
-        // wave's 64 hidden units; lane -> (row, 8 hidden units)
-        const int h = tile_n * (GT / 2) + wn * 64 + 32 * ((lane & 7) >> 2) + 8 * (lane & 3);
-        const int cg = 8 * ((lane & 7) >> 2) + (lane & 3);
-        bf16_t* gu = static_cast<bf16_t*>(a.C);
-        bf16_t* hh = static_cast<bf16_t*>(a.out2);
-        if (h < a.H) {
-#pragma unroll 4
+      char* reg = lds + wave * C_::EPI_WAVE;
+      if constexpr (KIND == DWD || KIND == DWGU) {
+        late = !a.accumulate;
+        if (a.accumulate) {
+          // fp32 weight gradient added to the caller's values, 16 bytes per
+          // lane straight from the accumulators, before the next tile's loads
+          const int r_in = lane & 15;
+          const int c_in = 4 * (lane >> 4);
+#pragma unroll
+          for (int ii = 0; ii < MI; ++ii) {
+            const int row = wm * WM + ii * 16 + r_in;
+            if (tl.m0 + row >= a.M) continue;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+              const int col = tl.n0 + wn * 128 + j * 16 + c_in;
+              if (col >= a.N) continue;
+              float* c = static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs +
+                         (size_t)tl.split * a.c_split + (size_t)(tl.m0 + row) * a.ldc + col;
+              *reinterpret_cast<f32x4_t*>(c) = acc[ii][j] + *reinterpret_cast<const f32x4_t*>(c);
+            }
+          }
+        }
+      } else {
+        // bf16 outputs go through LDS so that every global access is a whole
+        // 16-byte chunk and a wave instruction covers 256 contiguous bytes of
+        // a row (4 rows) instead of 32 bytes of 16 rows.  Each wave transposes
+        // its 64 x 128 sub-tile in a private 16 KB region of the ring (every
+        // wave passed the last k-step's barrier, after which no wave reads the
+        // ring's data).  The outputs (and the G/U that the dSwiGLU epilogue
+        // reads) are touched once here, so they go past the caches
+        // (nontemporal: measured 2-4 % faster for DHH_BWD, DX_BWD and
+        // DOWN_FWD; the fp32 weight gradients are not, they were 1.4-1.7x
+        // slower that way).
+#pragma unroll
+        for (int ii = 0; ii < MI; ++ii)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int row = ii * 16 + (lane & 15);
+            const int u = 4 * j + (lane >> 4);
+            epi_put(reg, row, u, acc[ii][j][0], acc[ii][j][1], acc[ii][j][2], acc[ii][j][3]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region is wave-private
+        if constexpr (KIND == GU_FWD) {
+          // region row: [G h0..31 | U h0..31 | G h32..63 | U h32..63] of the
+          // wave's 64 hidden units; lane -> (row, 8 hidden units)
+          const int cg = 8 * ((lane & 7) >> 2) + (lane & 3);
+#pragma unroll
           for (int it = 0; it < WM / 8; ++it) {
             const int row = it * 8 + (lane >> 3);
-            if (row >= row_lim) break;
-            const bf16x8_t G = epi_get(reg, row, cg);
-            const bf16x8_t U = epi_get(reg, row, cg + 4);
-            bf16x8_t Hv;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)(silu_fast((float)G[e]) * (float)U[e]);
-            const size_t m = (size_t)(tl.row0 + wm * WM + row);
-            __builtin_nontemporal_store(G, reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + h));
-            __builtin_nontemporal_store(U, reinterpret_cast<bf16x8_t*>(gu + m * 2 * a.H + a.H + h));
-            __builtin_nontemporal_store(Hv, reinterpret_cast<bf16x8_t*>(hh + m * a.H + h));
+            out[it] = epi_get(reg, row, cg);
+            out[8 + it] = epi_get(reg, row, cg + 4);
           }
-        }
-      } else {
-        const int c = lane & 15;
-        const int col = tl.n0 + wn * 128 + 8 * c;
-        if (col < a.N) {
-          if constexpr (KIND == DHH_BWD) {
-            // dG = dHh * U * silu'(G), dU = dHh * silu(G); G and U of a batch of
-            // rows are loaded before any store of it
-            const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
-            bf16_t* dgu = static_cast<bf16_t*>(a.C);
-            for (int it0 = 0; it0 < WM / 4; it0 += 8) {
-              if (it0 * 4 >= row_lim) break;
-              bf16x8_t G[8], U[8];
+          late = true;
+        } else if constexpr (KIND == DOWN_FWD || KIND == DX_BWD || KIND == UP_FWD) {
+          const int c = lane & 15;
 #pragma unroll
-              for (int b = 0; b < 8; ++b) {
-                const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
-                const size_t m = (size_t)(tl.row0 + wm * WM + row);
-                G[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col));
-                U[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col));
-              }
+          for (int it = 0; it < WM / 4; ++it) out[it] = epi_get(reg, it * 4 + (lane >> 4), c);
+          late = true;
+        } else {
+          const int c = lane & 15;
+          const int col = tl.n0 + wn * 128 + 8 * c;
+          if (col < a.N) {
+            if constexpr (KIND == DHH_BWD) {
+              // dG = dHh * U * silu'(G), dU = dHh * silu(G); G and U of a batch
+              // of rows are loaded before any store of it (all rows at once
+              // measured slower: the 128 registers of G and U spill)
+              const bf16_t* gu = static_cast<const bf16_t*>(a.aux);
+              bf16_t* dgu = static_cast<bf16_t*>(a.C);
+              for (int it0 = 0; it0 < WM / 4; it0 += 8) {
+                if (it0 * 4 >= row_lim) break;
+                bf16x8_t G[8], U[8];
 #pragma unroll
-              for (int b = 0; b < 8; ++b) {
-                const int row = (it0 + b) * 4 + (lane >> 4);
-                const bf16x8_t v = epi_get(reg, row, c);
-                bf16x8_t dG, dU;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const float g = (float)G[b][e], dh = (float)v[e];
-                  const float s = sigmoid_fast(g);
-                  dG[e] = (bf16_t)(dh * (float)U[b][e] * (s * (1.0f + g * (1.0f - s))));
-                  dU[e] = (bf16_t)(dh * g * s);
-                }
-                if (row < row_lim) {
+                for (int b = 0; b < 8; ++b) {
+                  const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
                   const size_t m = (size_t)(tl.row0 + wm * WM + row);
-                  __builtin_nontemporal_store(dG, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + col));
-                  __builtin_nontemporal_store(dU, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + a.H + col));
+                  G[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col));
+                  U[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col));
+                }
+#pragma unroll
+                for (int b = 0; b < 8; ++b) {
+                  const int row = (it0 + b) * 4 + (lane >> 4);
+                  const bf16x8_t v = epi_get(reg, row, c);
+                  bf16x8_t dG, dU;
+#pragma unroll
+                  for (int e = 0; e < 8; ++e) {
+                    const float g = (float)G[b][e], dh = (float)v[e];
+                    const float sg = sigmoid_fast(g);
+                    dG[e] = (bf16_t)(dh * (float)U[b][e] * (sg * (1.0f + g * (1.0f - sg))));
+                    dU[e] = (bf16_t)(dh * g * sg);
+                  }
+                  if (row < row_lim) {
+                    const size_t m = (size_t)(tl.row0 + wm * WM + row);
+                    __builtin_nontemporal_store(dG, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + col));
+                    __builtin_nontemporal_store(dU, reinterpret_cast<bf16x8_t*>(dgu + m * 2 * a.H + a.H + col));
+                  }
                 }
               }
-            }
-          } else if constexpr (KIND == DH_BWD) {
-            // dA = dHh * silu'(A); A of a batch of rows is loaded before any
-            // store of it
-            const bf16_t* Ab = static_cast<const bf16_t*>(a.aux);
-            bf16_t* C = static_cast<bf16_t*>(a.C);
-            for (int it0 = 0; it0 < WM / 4; it0 += 8) {
-              if (it0 * 4 >= row_lim) break;
-              bf16x8_t Av[8];
+            } else if constexpr (KIND == DH_BWD) {
+              // dA = dHh * silu'(A); A of a batch of rows is loaded before any
+              // store of it
+              const bf16_t* Ab = static_cast<const bf16_t*>(a.aux);
+              bf16_t* C = static_cast<bf16_t*>(a.C);
+              for (int it0 = 0; it0 < WM / 4; it0 += 8) {
+                if (it0 * 4 >= row_lim) break;
+                bf16x8_t Av[8];
 #pragma unroll
-              for (int b = 0; b < 8; ++b) {
-                const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
-                Av[b] = *reinterpret_cast<const bf16x8_t*>(
-                    Ab + (size_t)(tl.row0 + wm * WM + row) * a.H + col);
-              }
-#pragma unroll
-              for (int b = 0; b < 8; ++b) {
-                const int row = (it0 + b) * 4 + (lane >> 4);
-                const bf16x8_t v = epi_get(reg, row, c);
-                bf16x8_t dA;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const float g = (float)Av[b][e];
-                  const float sg = sigmoid_fast(g);
-                  dA[e] = (bf16_t)((float)v[e] * (sg * (1.0f + g * (1.0f - sg))));
+                for (int b = 0; b < 8; ++b) {
+                  const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
+                  Av[b] = *reinterpret_cast<const bf16x8_t*>(
+                      Ab + (size_t)(tl.row0 + wm * WM + row) * a.H + col);
                 }
-                if (row < row_lim)
-                  __builtin_nontemporal_store(dA, reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * WM + row) * a.ldc + col));
-              }
-            }
-          } else if constexpr (KIND == UP_FWD) {
-            // A and h = silu(A) (of the bf16-rounded A)
-            bf16_t* C = static_cast<bf16_t*>(a.C);
-            bf16_t* hh = static_cast<bf16_t*>(a.out2);
-#pragma unroll 8
-            for (int it = 0; it < WM / 4; ++it) {
-              const int row = it * 4 + (lane >> 4);
-              if (row >= row_lim) break;
-              const bf16x8_t A = epi_get(reg, row, c);
-              bf16x8_t Hv;
 #pragma unroll
-              for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)silu_fast((float)A[e]);
-              const size_t m = (size_t)(tl.row0 + wm * WM + row);
-              __builtin_nontemporal_store(A, reinterpret_cast<bf16x8_t*>(C + m * a.ldc + col));
-              __builtin_nontemporal_store(Hv, reinterpret_cast<bf16x8_t*>(hh + m * a.H + col));
-            }
-          } else {  // DOWN_FWD / DX_BWD
-            bf16_t* C = static_cast<bf16_t*>(a.C);
-#pragma unroll 8
-            for (int it = 0; it < WM / 4; ++it) {
-              const int row = it * 4 + (lane >> 4);
-              if (row >= row_lim) break;
-              __builtin_nontemporal_store(epi_get(reg, row, c), reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * WM + row) * a.ldc + col));
+                for (int b = 0; b < 8; ++b) {
+                  const int row = (it0 + b) * 4 + (lane >> 4);
+                  const bf16x8_t v = epi_get(reg, row, c);
+                  bf16x8_t dA;
+#pragma unroll
+                  for (int e = 0; e < 8; ++e) {
+                    const float g = (float)Av[b][e];
+                    const float sg = sigmoid_fast(g);
+                    dA[e] = (bf16_t)((float)v[e] * (sg * (1.0f + g * (1.0f - sg))));
+                  }
+                  if (row < row_lim)
+                    __builtin_nontemporal_store(dA, reinterpret_cast<bf16x8_t*>(C + (size_t)(tl.row0 + wm * WM + row) * a.ldc + col));
+                }
+              }
             }
           }
         }
       }
-    }
-    // next tile: the prefetched counter value (dynamic) or the next stride
+
+      // ---- epilogue, part 2: the stores
+      if (late) {
+      if constexpr (KIND == DWD || KIND == DWGU) {
+        // fp32 weight gradient of group g, 16 bytes per lane straight from
+        // the accumulators (64 contiguous bytes of 16 rows per instruction)
+        const __amdgpu_buffer_rsrc_t rc = store_rsrc(
+            static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs + (size_t)tl.split * a.c_split);
+        const int r_in = lane & 15;
+        const int c_in = 4 * (lane >> 4);
+#pragma unroll
+        for (int ii = 0; ii < MI; ++ii) {
+          const int row = wm * WM + ii * 16 + r_in;
+          const bool rok = tl.m0 + row < a.M;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int col = tl.n0 + wn * 128 + j * 16 + c_in;
+            const unsigned off = rok && col < a.N
+                                     ? 4u * ((unsigned)(tl.m0 + row) * (unsigned)a.ldc + (unsigned)col)
+                                     : kOOB;
+            store16<false>(rc, off, __builtin_bit_cast(u32x4_t, acc[ii][j]));
+          }
+        }
+      } else if constexpr (KIND == GU_FWD) {
+        const int h = cur.tile_n * (GT / 2) + wn * 64 + 32 * ((lane & 7) >> 2) + 8 * (lane & 3);
+        const __amdgpu_buffer_rsrc_t rg = store_rsrc(a.C), rh = store_rsrc(a.out2);
+        const unsigned H = (unsigned)a.H;
+#pragma unroll
+        for (int it = 0; it < WM / 8; ++it) {
+          const int row = it * 8 + (lane >> 3);
+          const bool ok = row < row_lim && h < a.H;
+          const unsigned m = (unsigned)(tl.row0 + wm * WM + row);
+          const bf16x8_t G = out[it], U = out[8 + it];
+          bf16x8_t Hv;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)(silu_fast((float)G[e]) * (float)U[e]);
+          store16<true>(rg, ok ? 2u * (m * 2u * H + h) : kOOB, __builtin_bit_cast(u32x4_t, G));
+          store16<true>(rg, ok ? 2u * (m * 2u * H + H + h) : kOOB, __builtin_bit_cast(u32x4_t, U));
+          store16<true>(rh, ok ? 2u * (m * H + h) : kOOB, __builtin_bit_cast(u32x4_t, Hv));
+        }
+      } else if constexpr (KIND == DOWN_FWD || KIND == DX_BWD || KIND == UP_FWD) {
+        const int c = lane & 15;
+        const int col = tl.n0 + wn * 128 + 8 * c;
+        const __amdgpu_buffer_rsrc_t rc = store_rsrc(a.C);
+#pragma unroll
+        for (int it = 0; it < WM / 4; ++it) {
+          const int row = it * 4 + (lane >> 4);
+          const bool ok = row < row_lim && col < a.N;
+          const unsigned m = (unsigned)(tl.row0 + wm * WM + row);
+          store16<true>(rc, ok ? 2u * (m * (unsigned)a.ldc + col) : kOOB,
+                        __builtin_bit_cast(u32x4_t, out[it]));
+          if constexpr (KIND == UP_FWD) {
+            // h = silu(A) of the bf16-rounded A
+            bf16x8_t Hv;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) Hv[e] = (bf16_t)silu_fast((float)out[it][e]);
+            store16<true>(store_rsrc(a.out2), ok ? 2u * (m * (unsigned)a.H + col) : kOOB,
+                          __builtin_bit_cast(u32x4_t, Hv));
+          }
+        }
+      }
+      }
+    });
+
+    // ---- next tile: the dealt tile is broadcast through LDS; the barrier
+    // also frees the ring (every wave has read back its staged results)
     if (dyn) {
       it_parity ^= 1;
       if (threadIdx.x == 0) {
         next_tile[it_parity] = nxt;
-        if (nxt < cnt0 + cnt1) nxt = atomicAdd(L.counters + xcd, 1);
+        if (nxt < total) nxt = atomicAdd(L.counters + xcd, 1);
       }
     }
-    __syncthreads();  // LDS is reused by the next tile
-    i = dyn ? next_tile[it_parity] : i + per_xcd;
+    __syncthreads();
+    const int i_next = __builtin_amdgcn_readfirstlane(dyn ? next_tile[it_parity] : i + per_xcd);
+    TileCtx nx;
+    if (i_next < total) {
+      make_ctx(i_next, nx);
+      prologue(nx);
+    }
+
+    cur = nx;
+    i = i_next;
   }
 }
 
@@ -1014,44 +1228,60 @@ long max_tiles(const GemmArgs& a) {
                           : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, BM) * n_tiles;
 }
 
+// reduction length of one tile of a set (rows per group for the K-ragged kinds)
+template <int KIND>
+long k_per_tile(const GemmArgs& a) {
+  return Kind<KIND>::MRAG ? a.K : a.cap / std::max(1, a.n_groups) / std::max(1, a.ksplit);
+}
+
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
                                       "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu",
                                       "gemm_up_fwd", "gemm_dh_bwd"};
 
-// One launch over the sets sets[0..n_sets) (at most 2) of one GEMM kind.
-// counters (bf16 only): zeroed per-XCD tile counters for dynamic dealing;
-// zero[0..n_zero): words the launch's block 0 clears for later launches (the
-// launch then runs even without tiles).
+template <int KA, int KB>
+const char* gemm_name() {
+  if constexpr (KA == KB) return kGemmNames[KA];
+  else if constexpr (KA == DHH_BWD && KB == DWD) return "gemm_dhh_dwd";
+  else if constexpr (KA == DH_BWD && KB == DWD) return "gemm_dh_dwd";
+  else if constexpr (KA == DX_BWD && KB == DWGU) return "gemm_dx_dwgu";
+  else return "gemm_merged";
+}
+
+// One bf16 launch over up to kMaxSets sets: sets_a[0..na) of kind KA and
+// sets_b[0..nb) of kind KB.  counters: zeroed per-XCD tile counters for
+// dynamic dealing (then the sets are dealt longest reduction first, so that
+// long tiles do not start last), or NULL for round-robin dealing.
+template <int KA, int KB>
+hipError_t run_gemm_bf16(const GemmArgs* sets_a, int na, const GemmArgs* sets_b, int nb,
+                         hipStream_t s, int* counters) {
+  GemmLaunch L{};
+  struct Entry { GemmArgs a; int kb; long k; long tiles; };
+  Entry e[kMaxSets];
+  int n = 0;
+  for (int q = 0; q < na; ++q) e[n++] = Entry{sets_a[q], 0, k_per_tile<KA>(sets_a[q]), max_tiles<KA>(sets_a[q])};
+  for (int q = 0; q < nb; ++q) e[n++] = Entry{sets_b[q], 1, k_per_tile<KB>(sets_b[q]), max_tiles<KB>(sets_b[q])};
+  if (counters) std::stable_sort(e, e + n, [](const Entry& x, const Entry& y) { return x.k > y.k; });
+  long tiles = 0;
+  for (int q = 0; q < n; ++q) {
+    L.s[q] = e[q].a;
+    L.kind_b[q] = e[q].kb;
+    tiles += e[q].tiles;
+  }
+  L.n_sets = n;
+  L.counters = counters;
+  if (tiles == 0) return hipSuccess;
+  // persistent: at most one block per CU, a multiple of N_XCD blocks
+  long blocks = std::min<long>((long)num_cus(), tiles);
+  blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
+  MOE_TIMED((gemm_name<KA, KB>()), s, gemm_bf16_kernel<KA, KB><<<(int)blocks, 512, 0, s>>>(L));
+  return hipGetLastError();
+}
+
+// One launch per set group of one GEMM kind (fp32: one SIMT launch per set).
 template <int KIND>
 hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
-                    int* counters = nullptr, int* zero = nullptr, int n_zero = 0) {
-  if (bf16) {
-    // persistent: at most one block per CU, a multiple of N_XCD blocks
-    GemmLaunch L{};
-    L.s0 = sets[0];
-    L.n_sets = n_sets;
-    // dynamic dealing: the set with the longer reduction per tile goes first,
-    // so that its tiles do not start last
-    auto k_per_tile = [](const GemmArgs& a) -> long {
-      return Kind<KIND>::MRAG ? a.K
-                              : a.cap / std::max(1, a.n_groups) / std::max(1, a.ksplit);
-    };
-    const bool swap = counters && n_sets > 1 && k_per_tile(sets[1]) > k_per_tile(sets[0]);
-    L.counters = counters;
-    L.zero = zero;
-    L.n_zero = n_zero;
-    long tiles = max_tiles<KIND>(sets[0]);
-    if (n_sets > 1) {
-      L.s1 = sets[1];
-      tiles += max_tiles<KIND>(sets[1]);
-      if (swap) std::swap(L.s0, L.s1);
-    }
-    if (tiles == 0 && n_zero == 0) return hipSuccess;
-    long blocks = std::min<long>((long)num_cus(), std::max<long>(tiles, 1));
-    blocks = std::max<long>(N_XCD, (blocks + N_XCD - 1) / N_XCD * N_XCD);
-    MOE_TIMED(kGemmNames[KIND], s, gemm_bf16_kernel<KIND><<<(int)blocks, 64 * Cfg<KIND>::NW, 0, s>>>(L));
-    return hipGetLastError();
-  }
+                    int* counters = nullptr) {
+  if (bf16) return run_gemm_bf16<KIND, KIND>(sets, n_sets, nullptr, 0, s, counters);
   for (int i = 0; i < n_sets; ++i) {
     const GemmArgs& a = sets[i];
     dim3 grid;
@@ -1069,6 +1299,11 @@ hipError_t run_gemm(const GemmArgs* sets, int n_sets, int bf16, hipStream_t s,
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+// counters[0..n) = 0 (the per-XCD tile counters of the next launches)
+__global__ __launch_bounds__(64) void zero_counters_kernel(int* counters, int n) {
+  if ((int)threadIdx.x < n) counters[threadIdx.x] = 0;
 }
 
 // dst[i] = (accumulate ? dst[i] : 0) + p_0[i] + p_1[i] + ... (fixed order),
@@ -1103,7 +1338,7 @@ int ksplit_factor(int bf16, long M, long N, const moe_ffn_set& f) {
 }
 
 constexpr size_t kWsAlign = 256;
-constexpr int kCounterWords = 2 * N_XCD;  // DWD then DWGU per-XCD counters
+constexpr int kCounterWords = 2 * N_XCD;  // per-XCD counters of the two backward launches
 size_t align_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
 }  // namespace
@@ -1207,16 +1442,26 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     }
   }
   hipError_t e;
-  // the first launch clears the counters of the two weight-gradient launches
-  e = silu ? run_gemm<DH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
-                              ws ? kCounterWords : 0)
-           : run_gemm<DHH_BWD>(hh, n_sets, bf16, s, nullptr, ws ? counters : nullptr,
-                               ws ? kCounterWords : 0);
-  if (e != hipSuccess) return e;
-  if ((e = run_gemm<DX_BWD>(dx, n_sets, bf16, s)) != hipSuccess) return e;
-  if ((e = run_gemm<DWD>(wd, n_sets, bf16, s, ws ? counters : nullptr)) != hipSuccess) return e;
-  if ((e = run_gemm<DWGU>(wgu, n_sets, bf16, s, ws ? counters + N_XCD : nullptr)) != hipSuccess)
-    return e;
+  if (!bf16) {
+    e = silu ? run_gemm<DH_BWD>(hh, n_sets, bf16, s) : run_gemm<DHH_BWD>(hh, n_sets, bf16, s);
+    if (e != hipSuccess) return e;
+    if ((e = run_gemm<DX_BWD>(dx, n_sets, bf16, s)) != hipSuccess) return e;
+    if ((e = run_gemm<DWD>(wd, n_sets, bf16, s)) != hipSuccess) return e;
+    if ((e = run_gemm<DWGU>(wgu, n_sets, bf16, s)) != hipSuccess) return e;
+  } else {
+    // two launches of two independent kinds each: dHh with dW_d (both read
+    // dY), then dX with dW_gu (both read dG/dU); with a workspace their tiles
+    // are dealt dynamically from per-XCD counters, cleared here first
+    if (ws) {
+      MOE_TIMED("zero_counters", s, zero_counters_kernel<<<1, 64, 0, s>>>(counters, kCounterWords));
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    e = silu ? run_gemm_bf16<DH_BWD, DWD>(hh, n_sets, wd, n_sets, s, ws ? counters : nullptr)
+             : run_gemm_bf16<DHH_BWD, DWD>(hh, n_sets, wd, n_sets, s, ws ? counters : nullptr);
+    if (e != hipSuccess) return e;
+    e = run_gemm_bf16<DX_BWD, DWGU>(dx, n_sets, wgu, n_sets, s, ws ? counters + N_XCD : nullptr);
+    if (e != hipSuccess) return e;
+  }
   for (int r = 0; r < n_red; ++r) {
     const int blocks = (int)std::min<size_t>(8192, (red[r].n / 4 + 255) / 256);
     MOE_TIMED("splitk_reduce", s,

@@ -34,8 +34,17 @@ CALIBRATION_BYTES = 1 << 30  # the plain copy bench.py makes for the counter sca
 GEMM_KINDS = ["gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd", "gemm_dx_bwd", "gemm_dwd",
               "gemm_dwgu", "gemm_up_fwd", "gemm_dh_bwd"]
 
+# launches of two GEMM kinds (the backward's dHh with dW_d, dX with dW_gu)
+_MERGED = {(2, 4): "gemm_dhh_dwd", (7, 4): "gemm_dh_dwd", (3, 5): "gemm_dx_dwgu"}
+
+
+def _gemm_launch_name(ka: int, kb: int) -> str:
+    return GEMM_KINDS[ka] if ka == kb else _MERGED.get((ka, kb), "gemm_merged")
+
+
 # kernel symbol (demangled, as rocprofv3 prints it) -> timing name
 _SYMBOLS = [
+    (r"gemm_bf16_kernel(?:<|ILi)(\d)(?:, |ELi)(\d)", lambda m: _gemm_launch_name(int(m.group(1)), int(m.group(2)))),
     (r"gemm_bf16_kernel(?:<|ILi)(\d)", lambda m: GEMM_KINDS[int(m.group(1))]),
     (r"gemm_f32_kernel(?:<|ILi)(\d)", lambda m: GEMM_KINDS[int(m.group(1))]),
     (r"route_fwd_kernel", lambda m: "route_fwd"),
@@ -53,6 +62,7 @@ _SYMBOLS = [
     (r"unpermute_kernel", lambda m: "unpermute"),
     (r"expert_delta_kernel", lambda m: "expert_delta"),
     (r"splitk_reduce_kernel", lambda m: "splitk_reduce"),
+    (r"zero_counters_kernel", lambda m: "zero_counters"),
     (r"adamw_kernel", lambda m: "adamw_step"),
     (r"outer_nesterov_kernel", lambda m: "outer_nesterov"),
     (r"replica_mean_kernel", lambda m: "replica_mean"),
@@ -60,7 +70,7 @@ _SYMBOLS = [
 ]
 
 # timing name prefix -> source file that holds the kernel
-_SOURCES = [("gemm_", "gemm.hip"), ("splitk_", "gemm.hip"), ("route_", "route.hip"), ("dispatch_", "dispatch.hip"),
+_SOURCES = [("gemm_", "gemm.hip"), ("splitk_", "gemm.hip"), ("zero_counters", "gemm.hip"), ("route_", "route.hip"), ("dispatch_", "dispatch.hip"),
             ("combine_", "dispatch.hip"), ("unpermute", "dispatch.hip"),
             ("expert_delta", "dispatch.hip"), ("adamw", "optim.hip"), ("outer_", "optim.hip"),
             ("replica_", "optim.hip"),

@@ -9,6 +9,12 @@ def test_symbols_map_to_timing_names():
                          "moe::(anonymous namespace)::GemmArgs)") == "gemm_dwgu"
     assert P.timing_name("_ZN3moe12_GLOBAL__N_116gemm_bf16_kernelILi2EEEvNS0_8GemmArgsE") \
         == "gemm_dhh_bwd"
+    assert P.timing_name("void moe::(anonymous namespace)::gemm_bf16_kernel<1, 1>("
+                         "moe::(anonymous namespace)::GemmLaunch)") == "gemm_down_fwd"
+    assert P.timing_name("_ZN3moe12_GLOBAL__N_116gemm_bf16_kernelILi3ELi5EEEvNS0_10GemmLaunchE") \
+        == "gemm_dx_dwgu"
+    assert P.timing_name("void moe::(anonymous namespace)::gemm_bf16_kernel<2, 4>(x)") \
+        == "gemm_dhh_dwd"
     assert P.timing_name("_ZN3moe12_GLOBAL__N_118combine_fwd_kernelIDF16bEEvPKT_") == "combine_fwd"
     assert P.timing_name("moe::(anonymous namespace)::route_bwd_mfma_kernel(x)") == "route_bwd_mfma"
     assert P.timing_name("__amd_rocclr_copyBuffer") is None
