@@ -729,22 +729,56 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
   __shared__ GroupTable gtab[kMaxSets];
   if (wave < L.n_sets) build_group_table(L.s[wave], gtab[wave]);
   __syncthreads();
-  int mt[kMaxSets], ntl[kMaxSets], lo[kMaxSets], pre[kMaxSets + 1];
-  pre[0] = 0;
+  // per set: m-tiles, n-tiles, this XCD's first tile and its reduction
+  // length per tile (rows per group for the K-ragged kinds, from the table)
+  int mt[kMaxSets], ntl[kMaxSets], lo[kMaxSets], cnt[kMaxSets], kpt[kMaxSets];
 #pragma unroll
   for (int q = 0; q < kMaxSets; ++q) {
     int tot = 0;
-    mt[q] = ntl[q] = 0;
+    mt[q] = ntl[q] = kpt[q] = 0;
     if (q < L.n_sets) {
       for_kind(L.kind_b[q] != 0, [&](auto kc) {
         constexpr int KIND = decltype(kc)::value;
-        ntl[q] = col_tiles<KIND>(L.s[q]);
-        mt[q] = m_tile_count<KIND>(L.s[q], gtab[q]);
+        const GemmArgs& a = L.s[q];
+        ntl[q] = col_tiles<KIND>(a);
+        mt[q] = __builtin_amdgcn_readfirstlane(m_tile_count<KIND>(a, gtab[q]));
+        if constexpr (KA != KB)
+          kpt[q] = Kind<KIND>::MRAG
+                       ? a.K
+                       : __builtin_amdgcn_readfirstlane(gtab[q].b[a.n_groups] - gtab[q].b[0]) /
+                             max(1, a.n_groups) / max(1, a.ksplit);
       });
       tot = mt[q] * ntl[q];
     }
     lo[q] = (int)((long)tot * xcd / N_XCD);
-    pre[q + 1] = pre[q] + (int)((long)tot * (xcd + 1) / N_XCD) - lo[q];
+    cnt[q] = (int)((long)tot * (xcd + 1) / N_XCD) - lo[q];
+  }
+  // dealing order of the sets: with dynamic dealing the longest reduction per
+  // tile first (so that long tiles do not start last and short ones fill the
+  // last round), otherwise as given.  rank[q] = position of set q (stable);
+  // pre[p] = first tile of position p.  (Indices stay compile-time constants:
+  // runtime indexing of these arrays would move them to scratch memory.)
+  int rank[kMaxSets], pre[kMaxSets + 1];
+#pragma unroll
+  for (int q = 0; q < kMaxSets; ++q) {
+    rank[q] = q;
+    if constexpr (KA != KB) {  // the single-kind launches keep the given order
+      if (L.counters) {
+        rank[q] = 0;
+#pragma unroll
+        for (int r = 0; r < kMaxSets; ++r)
+          if (r != q && (kpt[r] > kpt[q] || (kpt[r] == kpt[q] && r < q))) ++rank[q];
+      }
+    }
+  }
+  pre[0] = 0;
+#pragma unroll
+  for (int p = 0; p < kMaxSets; ++p) {
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < kMaxSets; ++q)
+      if (rank[q] == p) c = cnt[q];
+    pre[p + 1] = pre[p] + c;
   }
   const int total = pre[kMaxSets];
   const bool dyn = L.counters != nullptr;
@@ -765,19 +799,30 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
   }
 
   auto make_ctx = [&](int it, TileCtx& c) {
-    int q = 0;
+    int pos = 0, first = 0;
 #pragma unroll
     for (int r = 1; r < kMaxSets; ++r)
-      if (it >= pre[r]) q = r;
+      if (it >= pre[r]) {
+        pos = r;
+        first = pre[r];
+      }
+    int q = 0, t = 0, m_t = 0, n_t = 0;
+#pragma unroll
+    for (int x = 0; x < kMaxSets; ++x)
+      if (rank[x] == pos) {
+        q = x;
+        t = lo[x] + (it - first);
+        m_t = mt[x];
+        n_t = ntl[x];
+      }
     c.set = q;
     c.kb = L.kind_b[q] != 0;
-    const int t = lo[q] + (it - pre[q]);
     for_kind(c.kb, [&](auto kc) {
       constexpr int KIND = decltype(kc)::value;
       using K_ = Kind<KIND>;
       constexpr int GK = Cfg<KIND>::GK;
       const GemmArgs& a = L.s[q];
-      tile_decode<KIND>(a, gtab[q], t, mt[q], ntl[q], c.tl, c.tile_n);
+      tile_decode<KIND>(a, gtab[q], t, m_t, n_t, c.tl, c.tile_n);
       const Tile tl = c.tl;
       const int tile_n = c.tile_n;
       const bf16_t* A = static_cast<const bf16_t*>(a.A);
@@ -1228,12 +1273,6 @@ long max_tiles(const GemmArgs& a) {
                           : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, BM) * n_tiles;
 }
 
-// reduction length of one tile of a set (rows per group for the K-ragged kinds)
-template <int KIND>
-long k_per_tile(const GemmArgs& a) {
-  return Kind<KIND>::MRAG ? a.K : a.cap / std::max(1, a.n_groups) / std::max(1, a.ksplit);
-}
-
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
                                       "gemm_dx_bwd", "gemm_dwd", "gemm_dwgu",
                                       "gemm_up_fwd", "gemm_dh_bwd"};
@@ -1249,18 +1288,18 @@ const char* gemm_name() {
 
 // One bf16 launch over up to kMaxSets sets: sets_a[0..na) of kind KA and
 // sets_b[0..nb) of kind KB.  counters: zeroed per-XCD tile counters for
-// dynamic dealing (then the sets are dealt longest reduction first, so that
-// long tiles do not start last), or NULL for round-robin dealing.
+// dynamic dealing (the kernel then deals the sets longest reduction per tile
+// first, measured from the device-side group offsets), or NULL for
+// round-robin dealing in the given set order.
 template <int KA, int KB>
 hipError_t run_gemm_bf16(const GemmArgs* sets_a, int na, const GemmArgs* sets_b, int nb,
                          hipStream_t s, int* counters) {
   GemmLaunch L{};
-  struct Entry { GemmArgs a; int kb; long k; long tiles; };
+  struct Entry { GemmArgs a; int kb; long tiles; };
   Entry e[kMaxSets];
   int n = 0;
-  for (int q = 0; q < na; ++q) e[n++] = Entry{sets_a[q], 0, k_per_tile<KA>(sets_a[q]), max_tiles<KA>(sets_a[q])};
-  for (int q = 0; q < nb; ++q) e[n++] = Entry{sets_b[q], 1, k_per_tile<KB>(sets_b[q]), max_tiles<KB>(sets_b[q])};
-  if (counters) std::stable_sort(e, e + n, [](const Entry& x, const Entry& y) { return x.k > y.k; });
+  for (int q = 0; q < na; ++q) e[n++] = Entry{sets_a[q], 0, max_tiles<KA>(sets_a[q])};
+  for (int q = 0; q < nb; ++q) e[n++] = Entry{sets_b[q], 1, max_tiles<KB>(sets_b[q])};
   long tiles = 0;
   for (int q = 0; q < n; ++q) {
     L.s[q] = e[q].a;
