@@ -127,6 +127,9 @@ def algorithmic_work(cfg, n, t_act, s, expert="swiglu"):
     w["dispatch_scan"] = ("byte", 0)
     w["dispatch_scatter"] = ("byte", T * k * 4 + n * 4 + T * k * 4)
     w["dispatch_gather"] = ("byte", t_act * d * s + n * d * s + T * k * 4)
+    # fused scan + slots + gather: every x row read, n rows written, the
+    # local ids read and perm / inv_perm written
+    w["dispatch_place"] = ("byte", T * d * s + n * d * s + T * k * 4 + n * 4 + T * k * 4)
     w["combine_fwd"] = ("byte", n * d * s + (T * d * s if Hs else 0) + T * d * s + T * k * 8)
     w["combine_bwd"] = ("byte", t_act * d * s + 2 * n * d * s + T * k * 12)
     w["unpermute"] = ("byte", n * d * s + (T * d * s if Hs else 0) + T * d * s + T * k * 4)

@@ -234,6 +234,140 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* x, int T_, in
   }
 }
 
+// Scan, slot assignment and gather in one kernel (k <= PK): block = PB
+// tokens.  Its slots follow from the per-DB-token-block histograms: for local
+// expert r, base = offsets[r] (exclusive scan of the totals) + the routes to r
+// of the DB-blocks before its own + those of the tokens before it in its own
+// DB-block (counted here) + the rank among the block's tokens (bitmap
+// popcount).  The x rows are requested before any of that, so their latency
+// overlaps the scan; each wave then writes its tokens' rows to their slots.
+// Block 0 writes counts and offsets.
+constexpr int PB = 32;  // tokens per block (one bitmap word per expert)
+constexpr int PK = 8;   // routes per token handled here
+template <class T>
+__global__ __launch_bounds__(256) void dispatch_place_kernel(const T* x, const int32_t* local, int Tn,
+                                                             int d, int k, int E_r, int cap,
+                                                             int nblk, const int32_t* blk_counts,
+                                                             int32_t* counts, int32_t* offsets,
+                                                             int32_t* perm, int32_t* inv_perm,
+                                                             T* xp) {
+  constexpr int V = Vec16<T>::N;
+  __shared__ int base[256];
+  __shared__ int wsum[4];
+  __shared__ uint32_t bits[256];
+  __shared__ int slot[PB][PK];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * PB;
+  const int B = t0 / DB;  // counting block of these tokens
+  // this wave's tokens' rows (4 tokens per wave, CPL chunks of 16 bytes per
+  // lane per pass; rows longer than one pass are handled by the loop below)
+  constexpr int TPW = PB / 4;  // tokens per wave
+  static_assert(TPW * 4 == PB, "tokens per wave");
+  const int pass = CPL * 64 * V;  // elements per pass
+  u32x4_t row[TPW][CPL];
+  auto load_rows = [&](int c0) {
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int t = t0 + wave * TPW + i;
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (t < Tn && c < d) row[i][cc] = *reinterpret_cast<const u32x4_t*>(x + (size_t)t * d + c);
+      }
+    }
+  };
+  if (E_r > 0) load_rows(0);
+  // per-expert totals and the routes of the DB-blocks before B
+  int tot = 0, pre = 0;
+  if (tid < E_r) {
+    int b = 0;
+    for (; b + 8 <= nblk; b += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = blk_counts[(size_t)(b + u) * E_r + tid];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        tot += v[u];
+        if (b + u < B) pre += v[u];
+      }
+    }
+    for (; b < nblk; ++b) {
+      const int v = blk_counts[(size_t)b * E_r + tid];
+      tot += v;
+      if (b < B) pre += v;
+    }
+    bits[tid] = 0u;
+  }
+  // exclusive scan of the totals over the experts (4 waves of 64)
+  int inc = tot;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += u;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  int carry = 0;
+  for (int w = 0; w < wave; ++w) carry += wsum[w];
+  const int off = carry + inc - tot;
+  if (tid < E_r) {
+    base[tid] = off + pre;
+    if (blockIdx.x == 0) {
+      counts[tid] = tot;
+      offsets[tid] = off;
+    }
+  }
+  if (blockIdx.x == 0 && tid == 0) offsets[E_r] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  __syncthreads();
+  // routes of the tokens of B before this block
+  for (int q = B * DB * k + tid; q < t0 * k; q += 256) {
+    const int r = local[q];
+    if (r >= 0 && r < E_r) atomicAdd(&base[r], 1);
+  }
+  // bitmaps of this block's tokens
+  const int i = tid >> 3, jl = tid & 7;  // token, route
+  const int t = t0 + i;
+  int r = -1;
+  if (t < Tn && jl < k) {
+    r = local[(size_t)t * k + jl];
+    if (r >= 0 && r < E_r) atomicOr(&bits[r], 1u << i);
+  }
+  __syncthreads();
+  if (t < Tn && jl < k) {
+    const size_t o = (size_t)t * k + jl;
+    int p = -1;
+    if (r >= 0 && r < E_r) {
+      p = base[r] + __popc(bits[r] & ((1u << i) - 1u));
+      // p < cap whenever a token's routes name distinct experts; anything
+      // else is malformed input and its extra routes are dropped
+      if (p < cap) perm[p] = (int32_t)o; else p = -1;
+    }
+    inv_perm[o] = p;
+    slot[i][jl] = p;
+  }
+  __syncthreads();
+  if (E_r == 0) return;
+  // each wave writes its tokens' rows to their slots
+  for (int c0 = 0; c0 < d; c0 += pass) {
+    if (c0 > 0) load_rows(c0);
+#pragma unroll
+    for (int ii = 0; ii < TPW; ++ii) {
+      const int ti = wave * TPW + ii;
+      if (t0 + ti >= Tn) break;
+      for (int j = 0; j < k; ++j) {
+        const int pj = slot[ti][j];
+        if (pj < 0) continue;
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int c = c0 + (cc * 64 + lane) * V;
+          if (c < d) *reinterpret_cast<u32x4_t*>(xp + (size_t)pj * d + c) = row[ii][cc];
+        }
+      }
+    }
+  }
+}
+
 // 16 bytes of T held as raw words, widened to fp32 (exact).
 DEVI void unpack16_f32(const u32x4_t& r, float* out, const float*) {
 #pragma unroll
@@ -462,6 +596,19 @@ hipError_t launch_dispatch(const void* x, int bf16, int T, int d, int k, int E_r
   int32_t* blk_base = blk_counts + (size_t)nblk * std::max(E_r, 1);
   if (nblk > 0 && E_r > 0)
     MOE_TIMED("dispatch_count", s, dispatch_count_kernel<<<nblk, DB, 0, s>>>(local, T, k, E_r, blk_counts));
+  if (nblk > 0 && k <= PK && E_r <= 256) {
+    // scan, slots and gather in one launch
+    const int pblk = ceil_div(T, PB);
+    if (bf16)
+      MOE_TIMED("dispatch_place", s, dispatch_place_kernel<bf16_t><<<pblk, 256, 0, s>>>(
+          static_cast<const bf16_t*>(x), local, T, d, k, E_r, cap, E_r > 0 ? nblk : 0, blk_counts,
+          counts, offsets, perm, inv_perm, static_cast<bf16_t*>(xp)));
+    else
+      MOE_TIMED("dispatch_place", s, dispatch_place_kernel<float><<<pblk, 256, 0, s>>>(
+          static_cast<const float*>(x), local, T, d, k, E_r, cap, E_r > 0 ? nblk : 0, blk_counts,
+          counts, offsets, perm, inv_perm, static_cast<float*>(xp)));
+    return hipGetLastError();
+  }
   MOE_TIMED("dispatch_scan", s,
             dispatch_scan_kernel<<<1, 64 * SCAN_WAVES, 0, s>>>(blk_counts, E_r > 0 ? nblk : 0, E_r,
                                                                blk_base, counts, offsets));

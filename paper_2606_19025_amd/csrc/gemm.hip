@@ -1365,12 +1365,29 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const fl
   }
 }
 
-// Split-K factor of a K-ragged (weight-gradient) GEMM of one set: a single
-// large group whose M x N tiles cannot fill the CUs (the merged shared
-// experts: one group over all T tokens) is cut into parts of its rows, each
-// part writing its own fp32 partial, summed afterwards in a fixed order.
-int ksplit_factor(int bf16, long M, long N, const moe_ffn_set& f) {
-  if (!bf16 || f.n_groups != 1 || f.cap < 4096) return 1;
+// Split-K factor of the weight-gradient GEMM of one set.  A single large
+// group (the merged shared experts: one group over all T tokens) is cut into
+// parts of its rows, each part writing its own fp32 partial, summed
+// afterwards in a fixed order - but only when the whole backward launch that
+// holds it (dHh with dW_d, or dX with dW_gu, over every set) has fewer tiles
+// than the GPU has CUs; otherwise the other kind's tiles fill the CUs and the
+// long tiles simply start first.
+long bwd_launch_tiles(const moe_ffn_set* sets, int n_sets, int d, bool second) {
+  long t = 0;
+  for (int i = 0; i < n_sets; ++i) {
+    const moe_ffn_set& f = sets[i];
+    const long R1 = f.activation == MOE_ACT_SILU ? 1 : 2;
+    const long m_tiles = ceil_div(f.cap, GT) + (long)f.n_groups;  // M-ragged bound
+    if (!second)  // dHh (N = H) and dW_d (d x H per group)
+      t += m_tiles * ceil_div(f.H, GT) + (long)f.n_groups * ceil_div(d, GT) * ceil_div(f.H, GT);
+    else          // dX (N = d) and dW_gu (R1 H x d per group)
+      t += m_tiles * ceil_div(d, GT) + (long)f.n_groups * ceil_div((int)(R1 * f.H), GT) * ceil_div(d, GT);
+  }
+  return t;
+}
+
+int ksplit_factor(int bf16, long M, long N, const moe_ffn_set& f, long launch_tiles) {
+  if (!bf16 || f.n_groups != 1 || f.cap < 4096 || launch_tiles >= num_cus()) return 1;
   const long tiles = ceil_div((int)M, GT) * (long)ceil_div((int)N, GT);
   const long sp = num_cus() / std::max<long>(tiles, 1);
   return (int)std::max<long>(1, std::min<long>(4, sp));
@@ -1391,8 +1408,8 @@ size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
     const long H = f.H, R1 = first_rows(f);
-    const int s_wd = ksplit_factor(bf16, d, H, f);
-    const int s_wgu = ksplit_factor(bf16, R1 * H, d, f);
+    const int s_wd = ksplit_factor(bf16, d, H, f, bwd_launch_tiles(sets, n_sets, d, false));
+    const int s_wgu = ksplit_factor(bf16, R1 * H, d, f, bwd_launch_tiles(sets, n_sets, d, true));
     if (s_wd > 1) bytes += align_up((size_t)s_wd * d * H * sizeof(float));
     if (s_wgu > 1) bytes += align_up((size_t)s_wgu * R1 * H * d * sizeof(float));
   }
@@ -1468,7 +1485,8 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     w.M = (int)(R1 * f.H); w.N = d;
     if (ws) {
       for (GemmArgs* g : {&c, &w}) {
-        const int S = ksplit_factor(bf16, g->M, g->N, f);
+        const int S = ksplit_factor(bf16, g->M, g->N, f,
+                                    bwd_launch_tiles(sets, n_sets, d, g == &w));
         if (S <= 1) continue;
         const size_t n = (size_t)g->M * g->N;
         red[n_red++] = Reduce{static_cast<float*>(g->C), reinterpret_cast<const float*>(part), S, n};

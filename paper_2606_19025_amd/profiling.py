@@ -57,6 +57,7 @@ _SYMBOLS = [
     (r"dispatch_scan_kernel", lambda m: "dispatch_scan"),
     (r"dispatch_scatter_kernel", lambda m: "dispatch_scatter"),
     (r"gather_rows_kernel", lambda m: "dispatch_gather"),
+    (r"dispatch_place_kernel", lambda m: "dispatch_place"),
     (r"combine_fwd_kernel", lambda m: "combine_fwd"),
     (r"combine_bwd_kernel", lambda m: "combine_bwd"),
     (r"unpermute_kernel", lambda m: "unpermute"),
