@@ -84,9 +84,10 @@ def parse():
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="make one plain device-to-device copy of a known size before the "
                          "steps, the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
-    ap.add_argument("--copy-baseline", action="store_true",
-                    help="also time torch's device-to-device copy and a read-only sum of "
-                         "1 GiB (the HBM rates a plain streaming kernel reaches on the box)")
+    ap.add_argument("--no-copy-baseline", dest="copy_baseline", action="store_false",
+                    help="skip timing torch's device-to-device copy and read-only sum of 1 GiB "
+                         "(the HBM rates a plain streaming kernel reaches on the box; on by "
+                         "default)")
     return ap.parse_args()
 
 
@@ -142,6 +143,21 @@ def algorithmic_work(cfg, n, t_act, s, expert="swiglu"):
     w["route_bwd_mfma"] = ("byte", T * E * 4 + 3 * T * d * s + E * d * s
                            + -(-T // 256) * E * d * 4)
     return w
+
+
+def survey_bytes(cfg, n, s):
+    """Bytes per step of the routing, dispatch and combine kernels under the
+    scope table's formulas (each kernel's compulsory row traffic as the method
+    defines it; they count neither the shared experts' output that the combine
+    adds, nor the dx that the un-permute accumulates into, nor the tokens
+    without resident routes, which the kernels here skip or add)."""
+    T, d, E, k = cfg["T"], cfg["d"], cfg["E"], cfg["k"]
+    return {"route_fwd": T * d * s + E * d * s + 4 * T * E + 9 * T * k,
+            "dispatch_place": 2 * n * d * s,
+            "dispatch_gather": 2 * n * d * s,
+            "combine_fwd": n * d * s + T * d * s,
+            "combine_bwd": T * d * s + 2 * n * d * s + 8 * T * k,
+            "unpermute": n * d * s + T * d * s}
 
 
 def optimizer_work(n_step_params, n_round_params, n_peers):
@@ -459,7 +475,8 @@ def main():
                 ent = dict(unit="GB/s", achieved=rate / 1e9, peak=PEAK_HBM_GBS)
             ent["frac"] = ent["achieved"] / ent["peak"]
             ent.update(launches=launches, avg_us=1e3 * tot / max(launches, 1),
-                       ms_per_step=tot / args.steps)
+                       ms_per_step=tot / args.steps,
+                       per_launch=amount / max(launches, 1))
             kernels[name] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in ent.items()}
         dom = max((nm for nm in kernels if nm not in per_round + ("copy_expert_rows",)),
                   key=lambda nm: kernels[nm]["ms_per_step"])
@@ -514,6 +531,12 @@ def main():
             kernels_cold[name] = dict(unit="GB/s", achieved=round(ach, 3), peak=PEAK_HBM_GBS,
                                       frac=round(ach / PEAK_HBM_GBS, 5), launches=launches,
                                       avg_us=round(1e3 * tot / max(launches, 1), 3))
+            sb = survey_bytes(cfg, n, s_bytes).get(name)
+            if sb is not None and tot > 0:
+                # the same duration under the scope table's byte formula
+                ach_s = sb * args.cold_steps / (tot / 1e3) / 1e9
+                kernels_cold[name].update(achieved_survey=round(ach_s, 3),
+                                          frac_survey=round(ach_s / PEAK_HBM_GBS, 5))
 
     hbm_copy = None
     if args.copy_baseline:

@@ -1,11 +1,14 @@
 """Summaries of rocprofv3 output for the kernels of the resident-expert layer.
 
-Two summaries, written as short text files:
+Three summaries, written as short text files:
 
 * ``kernel-stats``: the ``--kernel-trace --stats`` table (``*_kernel_stats.csv``)
   with every kernel symbol mapped to the name the library's own HIP-event
   timing uses (``moe_timing_collect``), so the two can be compared launch for
   launch.
+* ``mfma``: the bf16 MFMA flops each GEMM launch executed and its MFMA busy
+  share, from a ``--pmc MfmaFlopsBF16 MfmaUtil`` run, beside the algorithmic
+  flops a bench.py run counts for the same launch.
 * ``traffic``: HBM bytes per launch from two ``--pmc`` runs of the same
   command (``FETCH_SIZE``, then ``WRITE_SIZE``; both in KiB per dispatch).
   Each counter is scaled by the factor that makes it read exactly the known
@@ -16,6 +19,7 @@ Two summaries, written as short text files:
 
     python -m paper_2606_19025_amd.profiling kernel-stats STATS_CSV OUT --command "..."
     python -m paper_2606_19025_amd.profiling traffic FETCH_CSV WRITE_CSV OUT --command "..."
+    python -m paper_2606_19025_amd.profiling mfma COUNTERS_CSV BENCH_JSON OUT --command "..."
 """
 from __future__ import annotations
 
@@ -184,7 +188,9 @@ def traffic(fetch_csv: str, write_csv: str, out: str, command: str) -> None:
         f.write(f"# write command: {command.replace('{COUNTER}', 'WRITE_SIZE')}\n")
         f.write(f"# calibration: a plain {CALIBRATION_BYTES} B device-to-device copy read "
                 f"FETCH_SIZE {c_fetch:.0f} KiB and WRITE_SIZE {c_write:.0f} KiB\n")
-        f.write(f"# scale: fetch x {f_fetch:.5f}, write x {f_write:.5f}\n")
+        f.write(f"# scale: fetch x {f_fetch:.5f}, write x {f_write:.5f} (one factor per counter for "
+                "every kernel: it assumes each kernel's requests are sized like the copy's; "
+                "partial-line or scattered reads may be overstated)\n")
         f.write("# columns: name launches fetch_kib write_kib bytes_per_launch source_digest\n")
         for nm in sorted(set(fn) | set(wn)):
             fv, wv = fn.get(nm, []), wn.get(nm, [])
@@ -193,6 +199,44 @@ def traffic(fetch_csv: str, write_csv: str, out: str, command: str) -> None:
             b = fa * kib * f_fetch + wa * kib * f_write
             f.write(f"{nm} {max(len(fv), len(wv))} {fa:.1f} {wa:.1f} {b:.0f} "
                     f"{source_digest(nm)}\n")
+
+
+def mfma(counters_csv: str, bench_json: str, out: str, command: str) -> None:
+    """Per GEMM launch: the bf16 MFMA flops the hardware executed (rocprofv3's
+    MfmaFlopsBF16 = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the algorithmic
+    flops bench.py counts for the same launch (executed rows only), and the
+    MFMA busy share (MfmaUtil = MFMA busy cycles over all SIMDs / (GPU active
+    cycles x SIMDs))."""
+    import json
+    per = collections.defaultdict(lambda: collections.defaultdict(lambda: collections.defaultdict(float)))
+    for r in csv.DictReader(open(counters_csv)):
+        nm = timing_name(r["Kernel_Name"])
+        if nm is None or not nm.startswith("gemm_"):
+            continue
+        per[nm][r["Counter_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+    bench = {}
+    for line in open(bench_json):
+        line = line.strip()
+        if line.startswith("{"):
+            bench = json.loads(line)
+    kern = bench.get("kernels", {})
+    with open(out, "w") as f:
+        f.write("# bf16 MFMA work and busy share per GEMM launch (rocprofv3 --pmc, derived counters)\n")
+        f.write(f"# command: {command}\n")
+        f.write("# algorithmic flops per launch: bench.py 'kernels' per_launch of the run\n")
+        f.write(f"#   {bench_json.split('/')[-1]} (executed routes only; config {bench.get('config', {}).get('workload')})\n")
+        f.write("# executed/algorithmic above 1 is tile padding: rows of partial m-tiles and\n")
+        f.write("# columns past N in the last n-tile still run MFMAs\n")
+        f.write("# columns: name launches executed_gflop algorithmic_gflop executed/algorithmic mfma_util_pct\n")
+        for nm in sorted(per):
+            fl = per[nm].get("MfmaFlopsBF16", {})
+            ut = per[nm].get("MfmaUtil", {})
+            n = max(len(fl), len(ut))
+            ex = sum(fl.values()) / len(fl) if fl else float("nan")
+            u = sum(ut.values()) / len(ut) if ut else float("nan")
+            alg = kern.get(nm, {}).get("per_launch")
+            ratio = ex / alg if alg else float("nan")
+            f.write(f"{nm} {n} {ex / 1e9:.1f} {(alg or float('nan')) / 1e9:.1f} {ratio:.3f} {u:.1f}\n")
 
 
 def load_traffic(path: str) -> dict:
@@ -220,9 +264,16 @@ def main() -> None:
     t.add_argument("write_csv")
     t.add_argument("out")
     t.add_argument("--command", required=True, help="the pmc command with {COUNTER}")
+    m = sub.add_parser("mfma")
+    m.add_argument("counters_csv")
+    m.add_argument("bench_json", help="a bench.py JSON line of the same workload (kernel timing on)")
+    m.add_argument("out")
+    m.add_argument("--command", required=True)
     a = ap.parse_args()
     if a.cmd == "kernel-stats":
         kernel_stats(a.stats_csv, a.out, a.command)
+    elif a.cmd == "mfma":
+        mfma(a.counters_csv, a.bench_json, a.out, a.command)
     else:
         traffic(a.fetch_csv, a.write_csv, a.out, a.command)
 
