@@ -544,6 +544,99 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(const T* dy, const T* 
   }
 }
 
+// combine_bwd for k <= 8: per token (one wave) the dy row is loaded once and
+// the Yp rows of up to CB_RB resident routes are requested together with it,
+// before any is used; routes beyond the batch (k > CB_RB) reuse the loaded
+// dy.  dtw of route j (0 for ghost routes) is written by lane j.
+constexpr int CB_RB = 4;
+template <class T>
+__global__ __launch_bounds__(256) void combine_bwd_rows_kernel(const T* dy, const T* yp, int T_,
+                                                               int d, int k, int cap,
+                                                               const float* tw,
+                                                               const int32_t* inv_perm, T* dyp,
+                                                               float* dtw) {
+  constexpr int V = Vec16<T>::N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;
+  const size_t o = (size_t)t * k;
+  const int my_p = lane < k ? slot_of(inv_perm, o, lane, cap) : -1;
+  const float my_w = lane < k ? tw[o + lane] : 0.f;
+  const uint64_t m = __ballot(my_p >= 0);
+  const int nr = __popcll(m);
+  // resident routes in route order: slot, weight
+  int p[8];
+  float w[8];
+  {
+    uint64_t mm = m;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int src = mm ? __builtin_ctzll(mm) : 0;
+      p[s] = __shfl(my_p, src, 64);
+      w[s] = __shfl(my_w, src, 64);
+      mm &= mm - 1;
+    }
+  }
+  float dot[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (nr > 0) {
+    for (int c0 = 0; c0 < d; c0 += WCPL * 64 * V) {
+      u32x4_t g_raw[WCPL];
+#pragma unroll
+      for (int cc = 0; cc < WCPL; ++cc) {
+        const int c = c0 + (cc * 64 + lane) * V;
+        if (c < d) g_raw[cc] = *reinterpret_cast<const u32x4_t*>(dy + (size_t)t * d + c);
+      }
+#pragma unroll
+      for (int s0 = 0; s0 < 8; s0 += CB_RB) {
+        if (s0 >= nr) break;
+        u32x4_t v_raw[CB_RB][WCPL];
+#pragma unroll
+        for (int b = 0; b < CB_RB; ++b) {
+          if (s0 + b >= nr) continue;
+#pragma unroll
+          for (int cc = 0; cc < WCPL; ++cc) {
+            const int c = c0 + (cc * 64 + lane) * V;
+            if (c < d) v_raw[b][cc] = *reinterpret_cast<const u32x4_t*>(yp + (size_t)p[s0 + b] * d + c);
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < CB_RB; ++b) {
+          if (s0 + b >= nr) continue;
+#pragma unroll
+          for (int cc = 0; cc < WCPL; ++cc) {
+            const int c = c0 + (cc * 64 + lane) * V;
+            if (c >= d) continue;
+            float g[V], v[V], out[V];
+            unpack16_f32(g_raw[cc], g, dy);
+            unpack16_f32(v_raw[b][cc], v, yp);
+#pragma unroll
+            for (int u = 0; u < V; ++u) {
+              dot[s0 + b] = fmaf(g[u], v[u], dot[s0 + b]);
+              out[u] = w[s0 + b] * g[u];
+            }
+            store16_f32(dyp + (size_t)p[s0 + b] * d + c, out);
+          }
+        }
+      }
+    }
+  }
+  // the routes' dot products, reduced together (fixed xor order)
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+    for (int s = 0; s < 8; ++s) dot[s] += __shfl_xor(dot[s], off, 64);
+  if (lane < k) {
+    float r = 0.f;
+    if (my_p >= 0) {
+      const int pos = __popcll(m & ((1ull << lane) - 1ull));
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        if (s == pos) r = dot[s];
+    }
+    dtw[o + lane] = r;
+  }
+}
+
 struct DeltaArgs {
   const float* start;
   const float* now;
@@ -689,6 +782,17 @@ hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, i
                               int cap, const float* tw, const int32_t* inv_perm, void* dyp,
                               float* dtw, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  if (k <= 8) {
+    if (bf16)
+      MOE_TIMED("combine_bwd", s, combine_bwd_rows_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
+          static_cast<const bf16_t*>(dy), static_cast<const bf16_t*>(yp), T, d, k, cap, tw, inv_perm,
+          static_cast<bf16_t*>(dyp), dtw));
+    else
+      MOE_TIMED("combine_bwd", s, combine_bwd_rows_kernel<float><<<ceil_div(T, 4), 256, 0, s>>>(
+          static_cast<const float*>(dy), static_cast<const float*>(yp), T, d, k, cap, tw, inv_perm,
+          static_cast<float*>(dyp), dtw));
+    return hipGetLastError();
+  }
   if (bf16)
     MOE_TIMED("combine_bwd", s, combine_bwd_kernel<bf16_t><<<ceil_div(T, 4), 256, 0, s>>>(
         static_cast<const bf16_t*>(dy), static_cast<const bf16_t*>(yp), T, d, k, cap, tw, inv_perm,
