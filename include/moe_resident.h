@@ -95,7 +95,8 @@ int moe_route_mask(const void* x, const void* w_router, const float* router_bias
  * writes it).  logits is required for MOE_GATE_SOFTMAX and may be NULL
  * otherwise.  accumulate_dx != 0 adds into dx, else overwrites it.
  * ws: device workspace (16-byte aligned) of at least
- * moe_route_bwd_workspace_size(T, d, E) bytes.  In bf16 with E <= 64 and
+ * moe_route_bwd_workspace_size(T, d, E) bytes; its contents on entry are
+ * ignored.  In bf16 with E <= 64 and
  * d % 128 == 0 the fp32 dz enters the MFMA products as a bf16 pair hi + lo
  * (relative error <= 2^-17 per element); otherwise the sums run in fp32 FMA.
  * Every sum is taken in a fixed order, so results are run-to-run identical.
@@ -120,7 +121,7 @@ int moe_route_bwd(const void* x, const void* w_router, int dtype, int T, int d, 
  *
  * cap = T * min(k, E_r) bounds n; perm and xp have cap rows, of which rows
  * n..cap-1 are left untouched.  ws: at least moe_dispatch_workspace_size()
- * bytes.  Limits: E_r <= 256.
+ * bytes; its contents on entry are ignored.  Limits: E_r <= 256.
  */
 size_t moe_dispatch_workspace_size(int T, int k, int E_r);
 int moe_dispatch(const void* x, int dtype, int T, int d, int k, int E_r,
@@ -159,8 +160,12 @@ int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
                      const int32_t* inv_perm, void* dx, int accumulate, hipStream_t stream);
 
 /*
- * Grouped SwiGLU expert FFN, forward.  Group g is rows [offsets[g],
- * offsets[g+1]) of xp and uses expert g's weights:
+ * Grouped SwiGLU expert FFN, forward: the expert outputs E_i(x) of the
+ * combine (App. A), evaluated only for the experts this worker hosts and only
+ * on the rows routed to them (Sec. 3.3.3 "Ghost Experts and Skip-Token";
+ * Alg. 2's local step).  The SwiGLU form is the one the layer workloads use;
+ * MOE_ACT_SILU below selects the paper's own expert (App. B.3.1).  Group g is
+ * rows [offsets[g], offsets[g+1]) of xp and uses expert g's weights:
  *   G = X Wg^T, U = X Wu^T, Hh = silu(G) * U, Y = Hh Wd^T   (no biases)
  * w_gate_up [n_groups, 2H, d]: rows 0..H-1 are Wg, rows H..2H-1 are Wu.
  * w_down    [n_groups, d, H].
@@ -170,16 +175,21 @@ int moe_dispatch_bwd(const void* dxp, int dtype, int T, int d, int k, int cap,
  * same input are one expert with their hidden units concatenated.
  * offsets is a device array of n_groups + 1 non-decreasing int32 values; each
  * group is clamped to [0, cap].
- * Limits (bf16): d % 64 == 0, H % 64 == 0, and each operand below 4 GiB
- * (2 cap max(d, 2H) and 2 n_groups 2H d bytes below 2^32 - 16: the GEMMs
- * address operands with 32-bit byte offsets); MOE_ERR_UNSUPPORTED otherwise.
+ * Limits: n_groups <= 256 (the GEMM kernels hold the group table in LDS),
+ * H % 64 == 0; fp32: d % 8 == 0; bf16: d % 64 == 0 and each operand below
+ * 4 GiB (2 cap max(d, 2H) and 2 n_groups 2H d bytes below 2^32 - 16: the
+ * GEMMs address operands with 32-bit byte offsets); MOE_ERR_UNSUPPORTED
+ * otherwise.
  */
 int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_down, int dtype,
                         int cap, int d, int H, int n_groups, const int32_t* offsets,
                         void* gu, void* h, void* yp, hipStream_t stream);
 
 /*
- * Grouped SwiGLU expert FFN, backward (chain rule of the forward, per group):
+ * Grouped SwiGLU expert FFN, backward: the gradients of the resident
+ * experts' parameters and of their input rows that the local step of Alg. 2
+ * needs (the chain rule of the forward, per group; the SiLU form as stated
+ * with MOE_ACT_SILU below):
  *   dHh = dY Wd;  dG = dHh * U * silu'(G);  dU = dHh * silu(G)
  *   dX  = dG Wg + dU Wu
  *   dWd = dY^T Hh;  dWg = dG^T X;  dWu = dU^T X           (fp32, per expert)
@@ -187,6 +197,8 @@ int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_dow
  * Outputs: dgu [cap,2H] = [dG | dU] (dtype), dxp [cap,d] (dtype),
  * dw_gate_up [n_groups,2H,d] fp32, dw_down [n_groups,d,H] fp32 - written for
  * every group (zero for an empty group), or added to when accumulate_dw != 0.
+ * Limits as for the forward, and 4 * 2H * d bytes of one expert's dw_gate_up
+ * below 4 GiB.
  */
 int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,
                         const void* w_gate_up, const void* w_down, int dtype, int cap, int d,

@@ -25,7 +25,10 @@ from . import binding as B
 class ResidentMoELayer:
     def __init__(self, T, d, E, k, H, resident, dtype=torch.bfloat16, n_shared_hidden=0,
                  gate="softmax_topk", inv_tau=1.0, device="cuda", partitioned=False,
-                 expert="swiglu"):
+                 expert="swiglu", canary=False):
+        """canary: fill every output and workspace buffer with NaN (integers:
+        -7, workspaces: 0xFF bytes) instead of leaving it uninitialised, so
+        that tests see any element the kernels fail to write."""
         self.T, self.d, self.E, self.k, self.H = int(T), int(d), int(E), int(k), int(H)
         res = torch.as_tensor(resident, dtype=torch.uint8).reshape(-1)
         assert res.numel() == self.E
@@ -53,7 +56,12 @@ class ResidentMoELayer:
         dev = torch.device(device)
         T, d, E, k, H, cap = self.T, self.d, self.E, self.k, self.H, self.cap
         f32, i32, act = torch.float32, torch.int32, dtype
-        e = lambda *s, dt=act: torch.empty(*s, dtype=dt, device=dev)
+        def e(*s, dt=act):
+            if not canary:
+                return torch.empty(*s, dtype=dt, device=dev)
+            fill = 0xFF if dt == torch.uint8 else -7 if dt == torch.int32 else float("nan")
+            return torch.full(s, fill, dtype=dt, device=dev)
+        self._alloc = e
         self.resident = res.to(dev)
         # routing
         self.logits = e(T, E, dt=f32)
@@ -108,12 +116,43 @@ class ResidentMoELayer:
         if not self.partitioned:
             self.resident.copy_(res.to(self.resident.device))
 
+    # ------------------------------------------------------------ validation
+    def _check(self, name, t, shape, dtype=None):
+        """Raise ValueError unless t is a contiguous tensor on this layer's
+        device with the given shape and dtype (the layer's own by default)."""
+        dtype = self.dtype if dtype is None else dtype
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name} must be a tensor, got {type(t).__name__}")
+        if t.device != self.resident.device:
+            raise ValueError(f"{name} is on {t.device}, the layer on {self.resident.device}")
+        if t.dtype != dtype:
+            raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+    def _check_weights(self, x, w_router, w_gate_up, w_down, shared_gate_up, shared_down):
+        r1 = 2 if self.act == B.MOE_ACT_SWIGLU else 1
+        self._check("x", x, (self.T, self.d))
+        self._check("w_router", w_router, (self.E, self.d))
+        self._check("w_gate_up", w_gate_up, (self.E_r, r1 * self.H, self.d))
+        self._check("w_down", w_down, (self.E_r, self.d, self.H))
+        if self.Hs:
+            self._check("shared_gate_up", shared_gate_up, (1, r1 * self.Hs, self.d))
+            self._check("shared_down", shared_down, (1, self.d, self.Hs))
+        elif shared_gate_up is not None or shared_down is not None:
+            raise ValueError("shared expert weights given to a layer built without them")
+
     # ------------------------------------------------------------------ forward
     def forward(self, x, w_router, w_gate_up, w_down, router_bias=None, shared_gate_up=None,
                 shared_down=None, stream=None, hook=None):
         """hook: called before each library call (e.g. a cache flush between
         kernels for cold per-kernel timing); None in normal use."""
         T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        self._check_weights(x, w_router, w_gate_up, w_down, shared_gate_up, shared_down)
+        if router_bias is not None:
+            self._check("router_bias", router_bias, (E,), torch.float32)
         hook = hook or (lambda: None)
         hook()
         B.moe_route_mask(x, w_router, router_bias, dt, T, d, E, k, self.inv_tau, self.gate,
@@ -142,6 +181,8 @@ class ResidentMoELayer:
     def backward(self, dy, x, w_router, w_gate_up, w_down, shared_gate_up=None, shared_down=None,
                  accumulate_dw=0, stream=None, hook=None):
         T, d, E, k, H, cap, dt = self.T, self.d, self.E, self.k, self.H, self.cap, self.dt
+        self._check_weights(x, w_router, w_gate_up, w_down, shared_gate_up, shared_down)
+        self._check("dy", dy, (T, d))
         hook = hook or (lambda: None)
         hook()
         B.moe_combine_bwd(dy, self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, self.dyp,
@@ -157,7 +198,7 @@ class ResidentMoELayer:
                                   activation=self.act))
         if self.ws_ffn is None:
             self.ws_ffn_bytes = B.moe_grouped_ffn_bwd_workspace_size(sets, dt, d)
-            self.ws_ffn = torch.empty(self.ws_ffn_bytes, dtype=torch.uint8, device=self.device)
+            self.ws_ffn = self._alloc(self.ws_ffn_bytes, dt=torch.uint8)
         hook()
         B.moe_grouped_ffn_bwd_sets(sets, dt, d, accumulate_dw, self.ws_ffn, self.ws_ffn_bytes,
                                    stream)

@@ -25,7 +25,8 @@ from oracle import moe_oracle as O
 from paper_2606_19025_amd import inputs as I
 from paper_2606_19025_amd.layer import expert_delta
 
-from .parity_helpers import TOL, assert_close, host, make_layer, run_gpu_layer, say
+from .parity_helpers import (TOL, assert_close, host, make_layer, record_errors, run_gpu_layer,
+                             say)
 
 pytestmark = pytest.mark.gpu
 
@@ -93,7 +94,7 @@ def test_full_size_layer(gpu_lib, wl):
     dz = host(L.dz)
     errs["dz"] = assert_close("dz", dz[tok], bwd["dz"], tol)
     errs["dtopk_w"] = assert_close("d_topk_w", host(L.dtopk_w)[tok], bwd["dw"], tol)
-    say(f"[full] workload {wl}: {N_SAMPLE} sampled tokens {errs}")
+    record_errors(f"full_size_layer[{wl}] {N_SAMPLE} sampled tokens", errs)
 
     # weight gradients of two sampled resident experts
     res_ids = np.flatnonzero(inp["resident"])
@@ -107,7 +108,8 @@ def test_full_size_layer(gpu_lib, wl):
         be = O.layer_bwd(se, fe, se["dy"])
         e1 = assert_close(f"dW_gate_up[{r}]", L.dw_gate_up[r].cpu().numpy(), be["dW_gate_up"][0], tol)
         e2 = assert_close(f"dW_down[{r}]", L.dw_down[r].cpu().numpy(), be["dW_down"][0], tol)
-        say(f"[full] workload {wl}: expert {g} (local {r}, {len(t_e)} tokens) dW errs {e1:.2e} {e2:.2e}")
+        record_errors(f"full_size_layer[{wl}] expert {g} ({len(t_e)} tokens)",
+                      {"dW_gate_up": e1, "dW_down": e2})
 
     # shared expert: all tokens, weight 1
     if L.Hs:
@@ -117,7 +119,7 @@ def test_full_size_layer(gpu_lib, wl):
                           inp["shared_down"][0])
         e1 = assert_close("shared dW_gate_up", L.s_dw_gate_up[0].cpu().numpy(), sb["dW_gate_up"], tol)
         e2 = assert_close("shared dW_down", L.s_dw_down[0].cpu().numpy(), sb["dW_down"], tol)
-        say(f"[full] workload {wl}: shared expert dW errs {e1:.2e} {e2:.2e}")
+        record_errors(f"full_size_layer[{wl}] shared expert", {"dW_gate_up": e1, "dW_down": e2})
 
     # router weight gradient over all tokens from the layer's own dz
     dzx = dz.T @ inp["x"].astype(np.float64)
@@ -138,18 +140,28 @@ def test_full_size_layer(gpu_lib, wl):
     say(f"[full] workload {wl}: {len(skipped)} fully skipped tokens exact")
 
 
-def test_full_size_expert_delta(gpu_lib):
-    # the fine-grained workload's resident experts: 16 x (2H d + d H) fp32 masters
-    cfg = I.workload(2, 42)
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("wl", [2, 4])
+def test_full_size_expert_delta(gpu_lib, wl):
+    """Round-boundary delta over every resident-expert fp32 master parameter
+    of the workload (16 x 3Hd = 138,412,032 for the fine-grained layer,
+    32 x 3Hd = 805,306,368 for the large one), averaged with the site copies
+    (S = 4 copies: this one and 3 peers, Alg. 2 round end), bit-exact."""
+    cfg = I.workload(wl, 42)
     n = cfg["E_r"] * 3 * cfg["H"] * cfg["d"]
-    say(f"[full] expert delta over {n} parameters")
-    dpar = I.make_delta_inputs(2, n)
+    say(f"[full] expert delta over {n} parameters, {cfg['n_peers']} peers: inputs")
+    dpar = I.make_delta_inputs(wl, n)
+    say("[full] expert delta: oracle")
     dl_ref, avg_ref = O.expert_delta(dpar["theta_start"], dpar["theta_now"], list(dpar["peers"]))
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     ts, tn = dev(dpar["theta_start"]), dev(dpar["theta_now"])
     peers = [dev(p) for p in dpar["peers"]]
-    dl = torch.empty_like(ts)
+    del dpar
+    dl = torch.full_like(ts, float("nan"))
+    say("[full] expert delta: kernel")
     avg = expert_delta(ts, tn, peers, delta_local=dl)
     torch.cuda.synchronize()
-    assert np.array_equal(dl.cpu().numpy(), dl_ref)
-    assert np.array_equal(avg.cpu().numpy(), avg_ref)
+    del ts, tn, peers
+    assert torch.equal(dl.cpu().view(torch.int32), torch.from_numpy(dl_ref).view(torch.int32))
+    assert torch.equal(avg.cpu().view(torch.int32), torch.from_numpy(avg_ref).view(torch.int32))
+    say(f"[full] expert delta over {n} parameters bit-exact")

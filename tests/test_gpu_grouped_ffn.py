@@ -23,7 +23,7 @@ from oracle import moe_oracle as O
 from paper_2606_19025_amd import binding as B
 from paper_2606_19025_amd import inputs as I
 
-from .parity_helpers import TOL, assert_close, host, say
+from .parity_helpers import TOL, assert_close, canary, host, record_errors, say
 
 pytestmark = pytest.mark.gpu
 
@@ -76,15 +76,15 @@ def test_grouped_ffn_tile_edges(gpu_lib, name):
     act = B.MOE_ACT_SWIGLU if expert == "swiglu" else B.MOE_ACT_SILU
     t_xp, t_dyp, t_wgu, t_wd = _dev(xp), _dev(dyp), _dev(w_gu), _dev(w_d)
     t_off = torch.from_numpy(offsets).cuda()
-    gu = torch.empty(cap, r1 * H, dtype=torch.bfloat16, device="cuda")
-    h = torch.empty(cap, H, dtype=torch.bfloat16, device="cuda")
-    yp = torch.empty(cap, d, dtype=torch.bfloat16, device="cuda")
-    dgu = torch.empty_like(gu)
-    dxp = torch.empty_like(yp)
-    t_dwgu = (torch.from_numpy(dw_gu0).cuda() if acc else
-              torch.empty(G, r1 * H, d, dtype=torch.float32, device="cuda"))
-    t_dwd = (torch.from_numpy(dw_d0).cuda() if acc else
-             torch.empty(G, d, H, dtype=torch.float32, device="cuda"))
+    # outputs start as NaN so that a row or gradient the kernels leave
+    # unwritten fails the comparison
+    gu = canary(cap, r1 * H)
+    h = canary(cap, H)
+    yp = canary(cap, d)
+    dgu = canary(cap, r1 * H)
+    dxp = canary(cap, d)
+    t_dwgu = (torch.from_numpy(dw_gu0).cuda() if acc else canary(G, r1 * H, d, dtype=torch.float32))
+    t_dwd = (torch.from_numpy(dw_d0).cuda() if acc else canary(G, d, H, dtype=torch.float32))
     fset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, gu, h, yp=yp, activation=act)
     B.moe_grouped_ffn_fwd_sets([fset], B.MOE_BF16, d)
     bset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, gu, h, dyp=t_dyp, dgu=dgu, dxp=dxp,
@@ -92,7 +92,7 @@ def test_grouped_ffn_tile_edges(gpu_lib, name):
     ws, ws_bytes = None, 0
     if use_ws:
         ws_bytes = B.moe_grouped_ffn_bwd_workspace_size([bset], B.MOE_BF16, d)
-        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        ws = torch.full((ws_bytes,), 0xFF, dtype=torch.uint8, device="cuda")
     B.moe_grouped_ffn_bwd_sets([bset], B.MOE_BF16, d, acc, ws, ws_bytes)
     torch.cuda.synchronize()
 
@@ -123,4 +123,80 @@ def test_grouped_ffn_tile_edges(gpu_lib, name):
         else:
             errs[f"dWgu{r}"] = assert_close(f"dW_gate_up[{r}]", got_gu[r], want_gu[r], tol)
             errs[f"dWd{r}"] = assert_close(f"dW_down[{r}]", got_d[r], want_d[r], tol)
-    say(f"[grouped-ffn] {name} n={n} max err {max(errs.values()):.2e}")
+    record_errors(f"grouped_ffn[{name}]", errs)
+
+
+@pytest.mark.parametrize("acc", [0, 1])
+def test_grouped_ffn_single_set_entry_points(gpu_lib, acc):
+    """moe_grouped_ffn_fwd / moe_grouped_ffn_bwd (one expert set, no
+    workspace) against the oracle, and bit-exact against the same set passed
+    through the _sets entry points without a workspace."""
+    sizes, d, H = [0, 5, 128, 300, 0, 257, 64], 192, 128
+    say(f"[grouped-ffn] single-set entry points accumulate={acc}")
+    g = np.random.default_rng([23, acc])
+    G = len(sizes)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    n = int(offsets[-1])
+    cap = n + 40
+    xp, dyp = _bf16(g, (cap, d), 1.0), _bf16(g, (cap, d), 1.0)
+    w_gu, w_d = _bf16(g, (G, 2 * H, d), d ** -0.5), _bf16(g, (G, d, H), H ** -0.5)
+    dw_gu0 = (g.standard_normal((G, 2 * H, d)) * 0.01).astype(np.float32)
+    dw_d0 = (g.standard_normal((G, d, H)) * 0.01).astype(np.float32)
+    t_xp, t_dyp, t_wgu, t_wd = _dev(xp), _dev(dyp), _dev(w_gu), _dev(w_d)
+    t_off = torch.from_numpy(offsets).cuda()
+
+    def outputs():
+        o = dict(gu=canary(cap, 2 * H), h=canary(cap, H), yp=canary(cap, d),
+                 dgu=canary(cap, 2 * H), dxp=canary(cap, d))
+        if acc:
+            o["dwgu"], o["dwd"] = torch.from_numpy(dw_gu0).cuda(), torch.from_numpy(dw_d0).cuda()
+        else:
+            o["dwgu"] = canary(G, 2 * H, d, dtype=torch.float32)
+            o["dwd"] = canary(G, d, H, dtype=torch.float32)
+        return o
+
+    one = outputs()
+    B.moe_grouped_ffn_fwd(t_xp, t_wgu, t_wd, B.MOE_BF16, cap, d, H, G, t_off, one["gu"],
+                          one["h"], one["yp"])
+    B.moe_grouped_ffn_bwd(t_dyp, t_xp, one["gu"], one["h"], t_wgu, t_wd, B.MOE_BF16, cap, d, H,
+                          G, t_off, one["dgu"], one["dxp"], one["dwgu"], one["dwd"], acc)
+    sets = outputs()
+    fset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, sets["gu"], sets["h"], yp=sets["yp"])
+    B.moe_grouped_ffn_fwd_sets([fset], B.MOE_BF16, d)
+    bset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, sets["gu"], sets["h"], dyp=t_dyp,
+                     dgu=sets["dgu"], dxp=sets["dxp"], dw_gate_up=sets["dwgu"],
+                     dw_down=sets["dwd"])
+    B.moe_grouped_ffn_bwd_sets([bset], B.MOE_BF16, d, acc)
+    torch.cuda.synchronize()
+
+    rows = {"gu": n, "h": n, "yp": n, "dgu": n, "dxp": n, "dwgu": G, "dwd": G}
+    for key, r in rows.items():
+        a, b = one[key][:r].cpu(), sets[key][:r].cpu()
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32)), \
+            f"{key}: single-set and _sets entry points differ"
+
+    tol = TOL["bf16"]
+    f = O.grouped_ffn_fwd(xp[:n], offsets, w_gu, w_d, "swiglu")
+    b = O.grouped_ffn_bwd(dyp[:n], xp[:n], f["G"], f["U"], f["Hh"], offsets, w_gu, w_d, "swiglu")
+    errs = {}
+    g_gu = host(one["gu"][:n])
+    errs["G"] = assert_close("G", g_gu[:, :H], f["G"], tol)
+    errs["U"] = assert_close("U", g_gu[:, H:], f["U"], tol)
+    errs["h"] = assert_close("h", host(one["h"][:n]), f["Hh"], tol)
+    errs["yp"] = assert_close("yp", host(one["yp"][:n]), f["Y"], tol)
+    g_dgu = host(one["dgu"][:n])
+    errs["dG"] = assert_close("dG", g_dgu[:, :H], b["dG"], tol)
+    errs["dU"] = assert_close("dU", g_dgu[:, H:], b["dU"], tol)
+    errs["dxp"] = assert_close("dxp", host(one["dxp"][:n]), b["dXp"], tol)
+    want_gu = b["dW_gate_up"] + (dw_gu0 if acc else 0.0)
+    want_d = b["dW_down"] + (dw_d0 if acc else 0.0)
+    got_gu, got_d = host(one["dwgu"]), host(one["dwd"])
+    for r, sz in enumerate(sizes):
+        if sz == 0:
+            assert np.array_equal(got_gu[r], want_gu[r]), f"dW_gate_up of empty group {r}"
+            assert np.array_equal(got_d[r], want_d[r]), f"dW_down of empty group {r}"
+        else:
+            errs[f"dWgu{r}"] = assert_close(f"dW_gate_up[{r}]", got_gu[r], want_gu[r], tol)
+            errs[f"dWd{r}"] = assert_close(f"dW_down[{r}]", got_d[r], want_d[r], tol)
+    record_errors(f"grouped_ffn_single_set[acc={acc}]", errs)

@@ -30,7 +30,7 @@ def test_adamw_bit_exact(gpu_lib, n, wd):
     g = np.random.default_rng(n)
     theta = (g.standard_normal(n) * 0.02).astype(np.float32)
     th_d, m_d, v_d = dev(theta), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
-    lp = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    lp = torch.full((n,), float("nan"), dtype=torch.bfloat16, device="cuda")
     th, m, v = theta, np.zeros(n, np.float32), np.zeros(n, np.float32)
     for t in range(1, 4):
         grad = (g.standard_normal(n) * 0.1).astype(np.float32)
@@ -49,7 +49,7 @@ def test_outer_nesterov_bit_exact(gpu_lib, n):
     start = (g.standard_normal(n) * 0.02).astype(np.float32)
     s_d, now_d = dev(start), dev(start + 1.0)
     b_d = torch.zeros(n, device="cuda")
-    lp = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    lp = torch.full((n,), float("nan"), dtype=torch.bfloat16, device="cuda")
     th, b = start, np.zeros(n, np.float32)
     for _ in range(3):
         delta = (g.standard_normal(n) * 1e-3).astype(np.float32)
@@ -69,7 +69,7 @@ def test_replica_mean_bit_exact(gpu_lib, n, n_peers):
     peers = [g.standard_normal(n).astype(np.float32) for _ in range(n_peers)]
     ref = O.replica_mean(x, peers)
     x_d = dev(x)
-    out = torch.empty_like(x_d)
+    out = torch.full_like(x_d, float("nan"))
     B.moe_replica_mean(x_d, [dev(p) for p in peers], n_peers, n, out)
     torch.cuda.synchronize()
     assert np.array_equal(out.cpu().numpy(), ref)
@@ -131,7 +131,7 @@ def test_adamw_rows_with_own_steps_and_rates(gpu_lib):
     lr = np.array([1e-3, 1e-3, 1e-3 * O.warmup_scale(1, 4), 1e-3 * O.warmup_scale(1, 4), 1e-3,
                    1e-3 * O.warmup_scale(3, 4)], np.float32)
     th_d, m_d, v_d = dev(theta), dev(m0), dev(v0)
-    lp = torch.empty(n_rows, row_len, dtype=torch.bfloat16, device="cuda")
+    lp = torch.full((n_rows, row_len), float("nan"), dtype=torch.bfloat16, device="cuda")
     B.moe_adamw_step_rows(th_d, dev(grad), m_d, v_d, n_rows, row_len, steps, lr, theta_bf16=lp)
     torch.cuda.synchronize()
     for r in range(n_rows):

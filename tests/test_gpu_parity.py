@@ -14,7 +14,7 @@ from paper_2606_19025_amd import inputs as I
 from paper_2606_19025_amd.layer import expert_delta
 
 from .parity_helpers import (TOL, assert_close, check_layer_against_oracle, dev, gpu_outputs,
-                             host, run_gpu_layer, say)
+                             host, record_errors, run_gpu_layer, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -47,7 +47,7 @@ def test_layer_parity_workload(gpu_lib, wl):
     L, _ = run_gpu_layer(inp)
     g = gpu_outputs(L)
     errs = check_layer_against_oracle(inp, g)
-    say(f"[parity] workload {wl} n={g['n']} errs={ {k: (round(v, 8) if isinstance(v, float) else v) for k, v in errs.items()} }")
+    record_errors(f"layer_parity_workload[{wl}] n={g['n']}", errs)
 
 
 CASES = {
@@ -83,7 +83,8 @@ def test_layer_parity_edge_cases(gpu_lib, name):
         inp["w_down"] = np.zeros((0, d, H), np.float32)
     L, _ = run_gpu_layer(inp, gate=gate, inv_tau=tau)
     g = gpu_outputs(L)
-    check_layer_against_oracle(inp, g, gate=gate, inv_tau=tau)
+    errs = check_layer_against_oracle(inp, g, gate=gate, inv_tau=tau)
+    record_errors(f"layer_parity_edge[{name}] n={g['n']}", errs)
     if not res:
         assert g["n"] == 0
         assert np.all(g["dz"] == 0) and np.all(g["dw"] == 0)
@@ -117,7 +118,7 @@ def test_partitioned_router_parity(gpu_lib, name):
     errs = check_layer_against_oracle(part, g)
     assert np.all(g["local"] >= 0), "a partitioned router has no ghost routes"
     assert g["n"] == inp["x"].shape[0] * part["cfg"]["k"]
-    say(f"[partitioned] {name} n={g['n']} errs={ {k: (round(v, 8) if isinstance(v, float) else v) for k, v in errs.items()} }")
+    record_errors(f"partitioned_router[{name}] n={g['n']}", errs)
 
 
 def test_topk_ties_go_to_lower_expert_id(gpu_lib):
@@ -129,9 +130,9 @@ def test_topk_ties_go_to_lower_expert_id(gpu_lib):
     w[[1, 3, 6], :] = 0.5   # three-way tie at the top
     w[[2, 7], :] = 0.25     # two-way tie below
     res = np.zeros(E, np.uint8); res[[3, 7]] = 1
-    idx = torch.empty(T, k, dtype=torch.int32, device="cuda")
-    loc = torch.empty_like(idx)
-    tw = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    idx = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    loc = torch.full_like(idx, -7)
+    tw = torch.full((T, k), float("nan"), dtype=torch.float32, device="cuda")
     B.moe_route_mask(dev(x, torch.bfloat16), dev(w, torch.bfloat16), None, B.MOE_BF16, T, d, E, k,
                      1.0, 0, torch.from_numpy(res).cuda(), None, idx, tw, loc)
     torch.cuda.synchronize()
@@ -172,10 +173,10 @@ def test_topk_selection_special_logits(gpu_lib, name):
     w = dev(g.standard_normal((E, d)).astype(np.float32), torch.bfloat16)
     res = np.zeros(E, np.uint8)
     res[g.choice(E, max(1, E // 3), replace=False)] = 1
-    logits = torch.empty(T, E, dtype=torch.float32, device="cuda")
-    idx = torch.empty(T, k, dtype=torch.int32, device="cuda")
-    loc = torch.empty_like(idx)
-    tw = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    logits = torch.full((T, E), float("nan"), dtype=torch.float32, device="cuda")
+    idx = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    loc = torch.full_like(idx, -7)
+    tw = torch.full((T, k), float("nan"), dtype=torch.float32, device="cuda")
     B.moe_route_mask(x, w, torch.from_numpy(b.astype(np.float32)).cuda(), B.MOE_BF16, T, d, E, k,
                      1.0, B.GATES[gate], torch.from_numpy(res).cuda(), logits, idx, tw, loc)
     torch.cuda.synchronize()
@@ -220,7 +221,7 @@ def test_expert_delta_bit_exact(gpu_lib, n, n_peers):
     dl_ref, avg_ref = O.expert_delta(d["theta_start"], d["theta_now"], peers)
     ts, tn = dev(d["theta_start"], torch.float32), dev(d["theta_now"], torch.float32)
     pd = [dev(p, torch.float32) for p in peers]
-    dl = torch.empty_like(ts)
+    dl = torch.full_like(ts, float("nan"))
     avg = expert_delta(ts, tn, pd, delta_local=dl)
     torch.cuda.synchronize()
     assert np.array_equal(dl.cpu().numpy(), dl_ref)

@@ -46,14 +46,14 @@ def test_random_placement_round_boundary(gpu_lib):
     say(f"[placement] prev {prev.tolist()} new {new.tolist()} map {mig.tolist()}")
 
     # migration on the GPU: weights from the store (+ bf16 copy), state by the map
-    theta_gu = torch.empty(N_le, gu_len, device="cuda")
-    theta_dn = torch.empty(N_le, dn_len, device="cuda")
-    w_gu = torch.empty(N_le, 2 * H, D, dtype=torch.bfloat16, device="cuda")
-    w_dn = torch.empty(N_le, D, H, dtype=torch.bfloat16, device="cuda")
+    theta_gu = torch.full((N_le, gu_len), float("nan"), device="cuda")
+    theta_dn = torch.full((N_le, dn_len), float("nan"), device="cuda")
+    w_gu = torch.full((N_le, 2 * H, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    w_dn = torch.full((N_le, D, H), float("nan"), dtype=torch.bfloat16, device="cuda")
     B.moe_copy_expert_rows(f32(store_gu), new, theta_gu, N_le, gu_len, dst_bf16=w_gu)
     B.moe_copy_expert_rows(f32(store_dn), new, theta_dn, N_le, dn_len, dst_bf16=w_dn)
-    m_new = torch.empty(N_le, gu_len, device="cuda")
-    v_new = torch.empty(N_le, gu_len, device="cuda")
+    m_new = torch.full((N_le, gu_len), float("nan"), device="cuda")
+    v_new = torch.full((N_le, gu_len), float("nan"), device="cuda")
     B.moe_copy_expert_rows(f32(m_old), mig, m_new, N_le, gu_len)
     B.moe_copy_expert_rows(f32(v_old), mig, v_new, N_le, gu_len)
     steps = np.where(mig >= 0, steps_old[np.maximum(mig, 0)], 0)
