@@ -248,17 +248,30 @@ typedef struct moe_ffn_set {
   int activation;          /* MOE_ACT_SWIGLU (0) or MOE_ACT_SILU; the same in every set */
 } moe_ffn_set;
 
-int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
-                             hipStream_t stream);
+/*
+ * ws: device workspace of at least moe_grouped_ffn_fwd_workspace_size(sets,
+ * n_sets, dtype, d) bytes (which may be 0), 256-byte aligned, or NULL with
+ * ws_bytes = 0.  Its contents on entry are ignored.  With a workspace (bf16)
+ * the down projection may cut its reduction (the hidden units) into up to 8
+ * parts when its output tiles are too few to fill the GPU (small groups,
+ * e.g. few resident experts): each part writes fp32 partial rows, summed in
+ * a fixed part order into yp afterwards.  The kernel chooses the parts from
+ * the device-side group sizes; partials of at most 256 MiB per set are
+ * reserved (none when two do not fit).  Results are run-to-run identical.
+ */
+size_t moe_grouped_ffn_fwd_workspace_size(const moe_ffn_set* sets, int n_sets, int dtype, int d);
+int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
 /*
  * ws: device workspace of at least moe_grouped_ffn_bwd_workspace_size(sets,
  * n_sets, dtype, d) bytes, 256-byte aligned, or NULL with ws_bytes = 0.  Its
  * contents on entry are ignored.  With a workspace the weight-gradient GEMMs
  * hand out tiles dynamically (per-XCD counters) and a set with one large
  * group (the shared experts) may have its rows split into parts whose fp32
- * partial gradients are summed in a fixed order afterwards; the size depends
- * on the sets and on the device's compute-unit count.  Results are
- * run-to-run identical either way.
+ * partial gradients are summed in a fixed order afterwards; dX may cut its
+ * reduction (the 2H columns of [dG | dU]) into parts as the forward's down
+ * projection does.  The size depends on the sets and on the device's
+ * compute-unit count.  Results are run-to-run identical either way.
  */
 size_t moe_grouped_ffn_bwd_workspace_size(const moe_ffn_set* sets, int n_sets, int dtype, int d);
 int moe_grouped_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,

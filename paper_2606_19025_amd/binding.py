@@ -22,7 +22,8 @@ GATES = {"softmax_topk": MOE_GATE_SOFTMAX_TOPK, "softmax": MOE_GATE_SOFTMAX,
 EXPORTS = [
     "moe_last_error", "moe_abi_version", "moe_route_mask", "moe_route_bwd_workspace_size",
     "moe_route_bwd", "moe_dispatch_workspace_size", "moe_dispatch", "moe_dispatch_noalloc", "moe_dispatch_bwd",
-    "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_grouped_ffn_fwd_sets",
+    "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_grouped_ffn_fwd_workspace_size",
+    "moe_grouped_ffn_fwd_sets",
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
     "moe_expert_delta", "moe_adamw_step", "moe_outer_nesterov", "moe_replica_mean",
@@ -58,7 +59,8 @@ _SIGS = {
     "moe_grouped_ffn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_grouped_ffn_bwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P,
                                  _I, _P]),
-    "moe_grouped_ffn_fwd_sets": (_I, [_P, _I, _I, _I, _P]),
+    "moe_grouped_ffn_fwd_workspace_size": (_Z, [_P, _I, _I, _I]),
+    "moe_grouped_ffn_fwd_sets": (_I, [_P, _I, _I, _I, _P, _Z, _P]),
     "moe_grouped_ffn_bwd_workspace_size": (_Z, [_P, _I, _I, _I]),
     "moe_grouped_ffn_bwd_sets": (_I, [_P, _I, _I, _I, _I, _P, _Z, _P]),
     "moe_combine_fwd": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
@@ -219,10 +221,15 @@ def moe_grouped_ffn_bwd(dyp, xp, gu, h, w_gate_up, w_down, dtype, cap, d, H, n_g
         accumulate_dw, _stream(stream)))
 
 
-def moe_grouped_ffn_fwd_sets(sets, dtype, d, stream=None):
+def moe_grouped_ffn_fwd_workspace_size(sets, dtype, d):
+    arr = (moe_ffn_set * len(sets))(*sets)
+    return lib().moe_grouped_ffn_fwd_workspace_size(C.cast(arr, C.c_void_p), len(sets), dtype, d)
+
+
+def moe_grouped_ffn_fwd_sets(sets, dtype, d, ws=None, ws_bytes=0, stream=None):
     arr = (moe_ffn_set * len(sets))(*sets)
     return _check("moe_grouped_ffn_fwd_sets", lib().moe_grouped_ffn_fwd_sets(
-        C.cast(arr, C.c_void_p), len(sets), dtype, d, _stream(stream)))
+        C.cast(arr, C.c_void_p), len(sets), dtype, d, _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def moe_grouped_ffn_bwd_workspace_size(sets, dtype, d):

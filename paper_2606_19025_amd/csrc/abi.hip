@@ -156,7 +156,7 @@ int moe_timing_collect(moe_kernel_time* out, int max_out, int* n_out) {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
 
-int moe_abi_version(void) { return 2; }
+int moe_abi_version(void) { return 3; }
 
 int moe_route_mask(const void* x, const void* w_router, const float* router_bias, int dtype,
                    int T, int d, int E, int k, float inv_tau, int gate,
@@ -335,11 +335,22 @@ int check_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d, bool fwd) 
 
 }  // namespace
 
-int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d,
-                             hipStream_t stream) {
+size_t moe_grouped_ffn_fwd_workspace_size(const moe_ffn_set* sets, int n_sets, int dtype, int d) {
+  if (!sets || n_sets < 1 || n_sets > 2 || d < 1) return 0;
+  return moe::ffn_fwd_ws_bytes(sets, n_sets, dtype == MOE_BF16, d);
+}
+
+int moe_grouped_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int dtype, int d, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
   int r;
   if ((r = check_sets(sets, n_sets, dtype, d, true)) != MOE_OK) return r;
-  return hip_status(moe::launch_ffn_fwd_sets(sets, n_sets, dtype == MOE_BF16, d, stream),
+  if (ws) {
+    const size_t need = moe::ffn_fwd_ws_bytes(sets, n_sets, dtype == MOE_BF16, d);
+    REQUIRE(ws_bytes >= need, "workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+    SUPPORT((reinterpret_cast<uintptr_t>(ws) & 255u) == 0, "the workspace must be 256-byte aligned");
+    if (need == 0) ws = nullptr;
+  }
+  return hip_status(moe::launch_ffn_fwd_sets(sets, n_sets, dtype == MOE_BF16, d, ws, stream),
                     "moe_grouped_ffn_fwd_sets");
 }
 
@@ -369,7 +380,7 @@ int moe_grouped_ffn_fwd(const void* xp, const void* w_gate_up, const void* w_dow
   f.xp = xp; f.w_gate_up = w_gate_up; f.w_down = w_down; f.offsets = offsets;
   f.cap = cap; f.H = H; f.n_groups = n_groups;
   f.gu = gu; f.h = h; f.yp = yp;
-  return moe_grouped_ffn_fwd_sets(&f, 1, dtype, d, stream);
+  return moe_grouped_ffn_fwd_sets(&f, 1, dtype, d, nullptr, 0, stream);
 }
 
 int moe_grouped_ffn_bwd(const void* dyp, const void* xp, const void* gu, const void* h,

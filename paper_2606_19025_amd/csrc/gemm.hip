@@ -55,9 +55,16 @@ struct GemmArgs {
   const int32_t* offsets;
   long lda, ldb, ldc;
   long b_gs, c_gs;  // per-group strides (elements) of B and C
-  long c_split;     // K-ragged kinds: stride between the split-K partial outputs
+  long c_split;     // stride (elements) between the split-K partial outputs
   int n_groups, cap, M, N, K, H, accumulate;
   int ksplit;       // K-ragged kinds: each group's rows split in ksplit parts (0 = 1)
+  // DOWN_FWD and DX_BWD (bf16): the kernel may cut K into up to ksplit_max
+  // parts (its choice from the device-side group sizes); part p's fp32
+  // partial goes to part + p c_split ([cap, N] each) and the choice to
+  // *ksplit_used, for splitk_rows_reduce_kernel.  ksplit_max <= 1: no split.
+  int ksplit_max;
+  float* part;
+  int* ksplit_used;
 };
 
 struct Tile {
@@ -620,18 +627,22 @@ DEVI int m_tile_count(const GemmArgs& a, const GroupTable& t) {
 // (32 / GROUP_M) rectangle and share GROUP_M A panels and 32 / GROUP_M B
 // panels in L2.  The m-tile's group is found by all lanes of the wave at once
 // (the number of groups whose m-tiles all lie before it).
+// M-ragged kinds cut into `parts` K parts: m_tiles counts (m-tile, part)
+// pairs, part fastest.
 template <int KIND>
 DEVI void tile_decode(const GemmArgs& a, const GroupTable& gt, int t, int m_tiles, int n_tiles,
-                      Tile& tl, int& tile_n) {
+                      int parts, Tile& tl, int& tile_n) {
   constexpr int BM = Cfg<KIND>::BM, GROUP_M = Cfg<KIND>::GROUP;
   const int band = t / (GROUP_M * n_tiles);
   const int first_m = band * GROUP_M;
   const int band_m = min(GROUP_M, m_tiles - first_m);
   const int r = t - band * GROUP_M * n_tiles;
-  const int q = first_m + r % band_m;  // m-tile
+  int q = first_m + r % band_m;  // m-tile (and part)
   tile_n = r / band_m;
   tl.n0 = tile_n * GT;
   if constexpr (Kind<KIND>::MRAG) {
+    const int part = q % parts;
+    q /= parts;
     const int lane = threadIdx.x & 63;
     int g = 0;
     for (int g0 = 0; g0 < a.n_groups; g0 += 64) {
@@ -643,7 +654,7 @@ DEVI void tile_decode(const GemmArgs& a, const GroupTable& gt, int t, int m_tile
     tl.row0 = gt.b[g] + (q - gt.p[g]) * BM;
     tl.rows = min(BM, gt.b[g + 1] - tl.row0);
     tl.m0 = 0;
-    tl.split = 0;
+    tl.split = part;
   } else {
     // (group, split part, m-tile); part p of a group of rows [b, e) is
     // [b + len p / S, b + len (p + 1) / S)
@@ -692,6 +703,7 @@ struct TileCtx {
   bool kb;  // of kind KB
   Tile tl;
   int tile_n, nk, n_full;
+  int parts;  // K parts of an M-ragged tile (1: whole K, bf16 output)
   unsigned a_step, b_step;
   u32x4_t rs_a, rs_b;
   DmaPtrs<4> da, db;
@@ -731,25 +743,51 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
   __syncthreads();
   // per set: m-tiles, n-tiles, this XCD's first tile and its reduction
   // length per tile (rows per group for the K-ragged kinds, from the table)
-  int mt[kMaxSets], ntl[kMaxSets], lo[kMaxSets], cnt[kMaxSets], kpt[kMaxSets];
+  int mt[kMaxSets], ntl[kMaxSets], lo[kMaxSets], cnt[kMaxSets], kpt[kMaxSets], prt[kMaxSets];
+  long work = 0;  // sum over tiles of their reduction lengths
 #pragma unroll
   for (int q = 0; q < kMaxSets; ++q) {
-    int tot = 0;
     mt[q] = ntl[q] = kpt[q] = 0;
+    prt[q] = 1;
     if (q < L.n_sets) {
       for_kind(L.kind_b[q] != 0, [&](auto kc) {
         constexpr int KIND = decltype(kc)::value;
         const GemmArgs& a = L.s[q];
         ntl[q] = col_tiles<KIND>(a);
         mt[q] = __builtin_amdgcn_readfirstlane(m_tile_count<KIND>(a, gtab[q]));
-        if constexpr (KA != KB)
-          kpt[q] = Kind<KIND>::MRAG
-                       ? a.K
-                       : __builtin_amdgcn_readfirstlane(gtab[q].b[a.n_groups] - gtab[q].b[0]) /
-                             max(1, a.n_groups) / max(1, a.ksplit);
+        kpt[q] = Kind<KIND>::MRAG
+                     ? a.K
+                     : __builtin_amdgcn_readfirstlane(gtab[q].b[a.n_groups] - gtab[q].b[0]) /
+                           max(1, a.n_groups) / max(1, a.ksplit);
       });
-      tot = mt[q] * ntl[q];
+      work += (long)mt[q] * ntl[q] * kpt[q];
     }
+  }
+  // K parts of the linear M-ragged kinds: a tile whose reduction is longer
+  // than the launch's average load per block (work / blocks) would finish
+  // last with most CUs idle (few tiles: small groups, narrow N), so it is cut
+  // into parts of about that load (at most ksplit_max, at least two k-steps
+  // each).  Every block derives the same choice from the group table.
+#pragma unroll
+  for (int q = 0; q < kMaxSets; ++q) {
+    if (q < L.n_sets && L.s[q].ksplit_max > 1) {
+      for_kind(L.kind_b[q] != 0, [&](auto kc) {
+        constexpr int KIND = decltype(kc)::value;
+        if constexpr (KIND == DOWN_FWD || KIND == DX_BWD) {
+          const GemmArgs& a = L.s[q];
+          const long want = work > 0 ? ((long)a.K * gridDim.x + work - 1) / work : 1;
+          const int most = max(1, a.K / (2 * Cfg<KIND>::GK));
+          prt[q] = (int)max(1L, min(want, (long)min(a.ksplit_max, most)));
+          prt[q] = __builtin_amdgcn_readfirstlane(prt[q]);
+          kpt[q] = a.K / prt[q];
+          if (blockIdx.x == 0 && threadIdx.x == 0) *a.ksplit_used = prt[q];
+        }
+      });
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kMaxSets; ++q) {
+    const int tot = q < L.n_sets ? mt[q] * prt[q] * ntl[q] : 0;
     lo[q] = (int)((long)tot * xcd / N_XCD);
     cnt[q] = (int)((long)tot * (xcd + 1) / N_XCD) - lo[q];
   }
@@ -806,7 +844,7 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
         pos = r;
         first = pre[r];
       }
-    int q = 0, t = 0, m_t = 0, n_t = 0;
+    int q = 0, t = 0, m_t = 0, n_t = 0, p_t = 1;
 #pragma unroll
     for (int x = 0; x < kMaxSets; ++x)
       if (rank[x] == pos) {
@@ -814,6 +852,7 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
         t = lo[x] + (it - first);
         m_t = mt[x];
         n_t = ntl[x];
+        p_t = prt[x];
       }
     c.set = q;
     c.kb = L.kind_b[q] != 0;
@@ -822,7 +861,8 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
       using K_ = Kind<KIND>;
       constexpr int GK = Cfg<KIND>::GK;
       const GemmArgs& a = L.s[q];
-      tile_decode<KIND>(a, gtab[q], t, m_t, n_t, c.tl, c.tile_n);
+      tile_decode<KIND>(a, gtab[q], t, m_t * p_t, n_t, p_t, c.tl, c.tile_n);
+      c.parts = p_t;
       const Tile tl = c.tl;
       const int tile_n = c.tile_n;
       const bf16_t* A = static_cast<const bf16_t*>(a.A);
@@ -830,6 +870,9 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
       const int Kd = K_::MRAG ? a.K : tl.rows;
       c.nk = (Kd + GK - 1) / GK;
       c.n_full = Kd / GK;  // k-steps without a ragged tail
+      // K part tl.split of p_t: k-steps [ks0, ks1) (M-ragged kinds only)
+      const int ks0 = c.nk * tl.split / p_t;
+      if constexpr (K_::MRAG) c.nk = c.nk * (tl.split + 1) / p_t - ks0;
       const int last_row = tl.row0 + (tl.rows > 0 ? tl.rows - 1 : 0);
       // operand pointers; out-of-range M/N indices are clamped to valid
       // memory (outputs not stored), out-of-range k-rows read zeros
@@ -886,6 +929,14 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
       c.rs_b = make_rsrc(B);
       c.a_step = 2u * (K_::A_KC ? GK : (unsigned)GK * a.lda);
       c.b_step = 2u * (K_::B_KC ? GK : (unsigned)GK * a.ldb);
+      if constexpr (K_::MRAG) {
+        if (ks0 > 0) {
+#pragma unroll
+          for (int x = 0; x < DA; ++x) c.da.p[x] += (unsigned)ks0 * c.a_step;
+#pragma unroll
+          for (int x = 0; x < DB; ++x) c.db.p[x] += (unsigned)ks0 * c.b_step;
+        }
+      }
     });
   };
 
@@ -1037,13 +1088,19 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
       const Tile tl = cur.tl;
       const int row_lim = tl.rows - wm * WM;  // rows of this wave's sub-tile to store
       char* reg = lds + wave * C_::EPI_WAVE;
+      // the lane index, opaque to the compiler from here on: the epilogue's
+      // lane-dependent addresses are then computed per tile rather than
+      // hoisted out of the tile loop, where they would hold registers across
+      // the main loop (or spill)
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
       if constexpr (KIND == DWD || KIND == DWGU) {
         late = !a.accumulate;
         if (a.accumulate) {
           // fp32 weight gradient added to the caller's values, 16 bytes per
           // lane straight from the accumulators, before the next tile's loads
-          const int r_in = lane & 15;
-          const int c_in = 4 * (lane >> 4);
+          const int r_in = ln & 15;
+          const int c_in = 4 * (ln >> 4);
 #pragma unroll
           for (int ii = 0; ii < MI; ++ii) {
             const int row = wm * WM + ii * 16 + r_in;
@@ -1056,6 +1113,26 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
                          (size_t)tl.split * a.c_split + (size_t)(tl.m0 + row) * a.ldc + col;
               *reinterpret_cast<f32x4_t*>(c) = acc[ii][j] + *reinterpret_cast<const f32x4_t*>(c);
             }
+          }
+        }
+      } else if ((KIND == DOWN_FWD || KIND == DX_BWD) && cur.parts > 1) {
+        // a K part: its fp32 partial ([cap, N], rows as the output's),
+        // straight from the accumulators (here, so that the accumulators
+        // and the staged bf16 results of part 2 are never live together)
+        const __amdgpu_buffer_rsrc_t rc = store_rsrc(a.part + (size_t)tl.split * a.c_split);
+        const int r_in = ln & 15;
+        const int c_in = 4 * (ln >> 4);
+#pragma unroll
+        for (int ii = 0; ii < MI; ++ii) {
+          const int row = wm * WM + ii * 16 + r_in;
+          const bool rok = row < tl.rows;
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            const int col = tl.n0 + wn * 128 + j * 16 + c_in;
+            const unsigned off = rok && col < a.N
+                                     ? 4u * ((unsigned)(tl.row0 + row) * (unsigned)a.N + (unsigned)col)
+                                     : kOOB;
+            store16<false>(rc, off, __builtin_bit_cast(u32x4_t, acc[ii][j]));
           }
         }
       } else {
@@ -1073,29 +1150,29 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
         for (int ii = 0; ii < MI; ++ii)
 #pragma unroll
           for (int j = 0; j < NJ; ++j) {
-            const int row = ii * 16 + (lane & 15);
-            const int u = 4 * j + (lane >> 4);
+            const int row = ii * 16 + (ln & 15);
+            const int u = 4 * j + (ln >> 4);
             epi_put(reg, row, u, acc[ii][j][0], acc[ii][j][1], acc[ii][j][2], acc[ii][j][3]);
           }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region is wave-private
         if constexpr (KIND == GU_FWD) {
           // region row: [G h0..31 | U h0..31 | G h32..63 | U h32..63] of the
           // wave's 64 hidden units; lane -> (row, 8 hidden units)
-          const int cg = 8 * ((lane & 7) >> 2) + (lane & 3);
+          const int cg = 8 * ((ln & 7) >> 2) + (ln & 3);
 #pragma unroll
           for (int it = 0; it < WM / 8; ++it) {
-            const int row = it * 8 + (lane >> 3);
+            const int row = it * 8 + (ln >> 3);
             out[it] = epi_get(reg, row, cg);
             out[8 + it] = epi_get(reg, row, cg + 4);
           }
           late = true;
         } else if constexpr (KIND == DOWN_FWD || KIND == DX_BWD || KIND == UP_FWD) {
-          const int c = lane & 15;
+          const int c = ln & 15;
 #pragma unroll
-          for (int it = 0; it < WM / 4; ++it) out[it] = epi_get(reg, it * 4 + (lane >> 4), c);
+          for (int it = 0; it < WM / 4; ++it) out[it] = epi_get(reg, it * 4 + (ln >> 4), c);
           late = true;
         } else {
-          const int c = lane & 15;
+          const int c = ln & 15;
           const int col = tl.n0 + wn * 128 + 8 * c;
           if (col < a.N) {
             if constexpr (KIND == DHH_BWD) {
@@ -1109,14 +1186,14 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
                 bf16x8_t G[8], U[8];
 #pragma unroll
                 for (int b = 0; b < 8; ++b) {
-                  const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
+                  const int row = min((it0 + b) * 4 + (ln >> 4), row_lim - 1);
                   const size_t m = (size_t)(tl.row0 + wm * WM + row);
                   G[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + col));
                   U[b] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(gu + m * 2 * a.H + a.H + col));
                 }
 #pragma unroll
                 for (int b = 0; b < 8; ++b) {
-                  const int row = (it0 + b) * 4 + (lane >> 4);
+                  const int row = (it0 + b) * 4 + (ln >> 4);
                   const bf16x8_t v = epi_get(reg, row, c);
                   bf16x8_t dG, dU;
 #pragma unroll
@@ -1143,13 +1220,13 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
                 bf16x8_t Av[8];
 #pragma unroll
                 for (int b = 0; b < 8; ++b) {
-                  const int row = min((it0 + b) * 4 + (lane >> 4), row_lim - 1);
+                  const int row = min((it0 + b) * 4 + (ln >> 4), row_lim - 1);
                   Av[b] = *reinterpret_cast<const bf16x8_t*>(
                       Ab + (size_t)(tl.row0 + wm * WM + row) * a.H + col);
                 }
 #pragma unroll
                 for (int b = 0; b < 8; ++b) {
-                  const int row = (it0 + b) * 4 + (lane >> 4);
+                  const int row = (it0 + b) * 4 + (ln >> 4);
                   const bf16x8_t v = epi_get(reg, row, c);
                   bf16x8_t dA;
 #pragma unroll
@@ -1174,8 +1251,8 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
         // the accumulators (64 contiguous bytes of 16 rows per instruction)
         const __amdgpu_buffer_rsrc_t rc = store_rsrc(
             static_cast<float*>(a.C) + (size_t)tl.g * a.c_gs + (size_t)tl.split * a.c_split);
-        const int r_in = lane & 15;
-        const int c_in = 4 * (lane >> 4);
+        const int r_in = ln & 15;
+        const int c_in = 4 * (ln >> 4);
 #pragma unroll
         for (int ii = 0; ii < MI; ++ii) {
           const int row = wm * WM + ii * 16 + r_in;
@@ -1190,12 +1267,12 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
           }
         }
       } else if constexpr (KIND == GU_FWD) {
-        const int h = cur.tile_n * (GT / 2) + wn * 64 + 32 * ((lane & 7) >> 2) + 8 * (lane & 3);
+        const int h = cur.tile_n * (GT / 2) + wn * 64 + 32 * ((ln & 7) >> 2) + 8 * (ln & 3);
         const __amdgpu_buffer_rsrc_t rg = store_rsrc(a.C), rh = store_rsrc(a.out2);
         const unsigned H = (unsigned)a.H;
 #pragma unroll
         for (int it = 0; it < WM / 8; ++it) {
-          const int row = it * 8 + (lane >> 3);
+          const int row = it * 8 + (ln >> 3);
           const bool ok = row < row_lim && h < a.H;
           const unsigned m = (unsigned)(tl.row0 + wm * WM + row);
           const bf16x8_t G = out[it], U = out[8 + it];
@@ -1207,12 +1284,12 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
           store16<true>(rh, ok ? 2u * (m * H + h) : kOOB, __builtin_bit_cast(u32x4_t, Hv));
         }
       } else if constexpr (KIND == DOWN_FWD || KIND == DX_BWD || KIND == UP_FWD) {
-        const int c = lane & 15;
+        const int c = ln & 15;
         const int col = tl.n0 + wn * 128 + 8 * c;
         const __amdgpu_buffer_rsrc_t rc = store_rsrc(a.C);
 #pragma unroll
         for (int it = 0; it < WM / 4; ++it) {
-          const int row = it * 4 + (lane >> 4);
+          const int row = it * 4 + (ln >> 4);
           const bool ok = row < row_lim && col < a.N;
           const unsigned m = (unsigned)(tl.row0 + wm * WM + row);
           store16<true>(rc, ok ? 2u * (m * (unsigned)a.ldc + col) : kOOB,
@@ -1269,8 +1346,9 @@ template <int KIND>
 long max_tiles(const GemmArgs& a) {
   constexpr int BM = Cfg<KIND>::BM;
   const long n_tiles = ceil_div((KIND == GU_FWD) ? 2 * a.H : a.N, GT);
-  return Kind<KIND>::MRAG ? (ceil_div(a.cap, BM) + (long)a.n_groups) * n_tiles
-                          : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, BM) * n_tiles;
+  return Kind<KIND>::MRAG
+             ? (ceil_div(a.cap, BM) + (long)a.n_groups) * n_tiles * std::max(1, a.ksplit_max)
+             : (long)a.n_groups * std::max(1, a.ksplit) * ceil_div(a.M, BM) * n_tiles;
 }
 
 constexpr const char* kGemmNames[] = {"gemm_gu_fwd", "gemm_down_fwd", "gemm_dhh_bwd",
@@ -1365,6 +1443,62 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(float* dst, const fl
   }
 }
 
+// Rows of the set's groups (clamped to [0, cap] as the GEMM's group table
+// does) of the bf16 output: out[r, :] = bf16(part_0[r, :] + ... +
+// part_{S-1}[r, :]) in that order, S = *parts_used (the K parts the GEMM
+// chose; nothing to do when it chose 1).  N % 8 == 0.
+__global__ __launch_bounds__(256) void splitk_rows_reduce_kernel(
+    bf16_t* out, long ldo, const float* part, long stride, const int* parts_used,
+    const int32_t* offsets, int n_groups, int cap, int N) {
+  const int S = *parts_used;
+  if (S <= 1) return;
+  __shared__ int s_hi;
+  if (threadIdx.x == 0) s_hi = 0;
+  __syncthreads();
+  const int lo = clamp_row(offsets[0], cap);
+  for (int g = threadIdx.x; g <= n_groups; g += 256) atomicMax(&s_hi, clamp_row(offsets[g], cap));
+  __syncthreads();
+  const int hi = max(lo, s_hi);
+  const int c8 = N / 8;
+  const long n = (long)(hi - lo) * c8;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const long r = lo + i / c8;
+    const int c = (int)(i % c8) * 8;
+    f32x4_t q[8][2];  // every part's loads first (S <= 8)
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+      if (p < S) {
+        const f32x4_t* src = reinterpret_cast<const f32x4_t*>(part + p * stride + r * N + c);
+        q[p][0] = __builtin_nontemporal_load(src);
+        q[p][1] = __builtin_nontemporal_load(src + 1);
+      }
+    f32x4_t v0 = q[0][0], v1 = q[0][1];
+#pragma unroll
+    for (int p = 1; p < 8; ++p)
+      if (p < S) {
+        v0 += q[p][0];
+        v1 += q[p][1];
+      }
+    bf16x8_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = (bf16_t)v0[e];
+      o[4 + e] = (bf16_t)v1[e];
+    }
+    *reinterpret_cast<bf16x8_t*>(out + r * ldo + c) = o;
+  }
+}
+
+// Largest K split of a DOWN_FWD / DX_BWD set whose fp32 partials ([cap, N]
+// each) fit kPartBudget bytes; 1 (no split) when two do not.
+constexpr size_t kPartBudget = (size_t)256 << 20;
+constexpr int kMaxRowParts = 8;
+int row_parts_max(int bf16, long cap, long N) {
+  if (!bf16 || cap <= 0) return 1;
+  const size_t per = (size_t)cap * N * sizeof(float);
+  return (int)std::min<size_t>(kMaxRowParts, kPartBudget / per);
+}
+
 // Split-K factor of the weight-gradient GEMM of one set.  A single large
 // group (the merged shared experts: one group over all T tokens) is cut into
 // parts of its rows, each part writing its own fp32 partial, summed
@@ -1397,14 +1531,65 @@ constexpr size_t kWsAlign = 256;
 constexpr int kCounterWords = 2 * N_XCD;  // per-XCD counters of the two backward launches
 size_t align_up(size_t v) { return (v + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
+// Workspace of the K-part partials of one launch's DOWN_FWD or DX_BWD sets
+// (N = d): one int per set (the parts the GEMM chose), then per set that may
+// split its row_parts_max [cap, d] fp32 partials.
+size_t row_parts_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
+  size_t b = 0;
+  for (int i = 0; i < n_sets; ++i) {
+    const int S = row_parts_max(bf16, sets[i].cap, d);
+    if (S > 1) b += align_up((size_t)S * sets[i].cap * d * sizeof(float));
+  }
+  return b ? align_up(kMaxSets * sizeof(int)) + b : 0;
+}
+
+// Point the DOWN_FWD / DX_BWD arguments of the sets at their partials in the
+// workspace region at `p` (row_parts_bytes of it).
+void assign_row_parts(GemmArgs* args, const moe_ffn_set* sets, int n_sets, int bf16, int d,
+                      char* p) {
+  if (!p || row_parts_bytes(sets, n_sets, bf16, d) == 0) return;
+  int* used = reinterpret_cast<int*>(p);
+  p += align_up(kMaxSets * sizeof(int));
+  for (int i = 0; i < n_sets; ++i) {
+    const int S = row_parts_max(bf16, sets[i].cap, d);
+    if (S <= 1) continue;
+    args[i].ksplit_max = S;
+    args[i].part = reinterpret_cast<float*>(p);
+    args[i].c_split = (long)sets[i].cap * d;
+    args[i].ksplit_used = used + i;
+    p += align_up((size_t)S * sets[i].cap * d * sizeof(float));
+  }
+}
+
+// Sum the K parts of the sets that may have split (after their GEMM launch).
+hipError_t reduce_row_parts(const GemmArgs* args, int n_sets, hipStream_t s) {
+  for (int i = 0; i < n_sets; ++i) {
+    const GemmArgs& a = args[i];
+    if (a.ksplit_max <= 1) continue;
+    const long n8 = (long)a.cap * a.N / 8;
+    const int blocks = (int)std::max<long>(1, std::min<long>(4096, (n8 + 255) / 256));
+    MOE_TIMED("splitk_rows_reduce", s,
+              splitk_rows_reduce_kernel<<<blocks, 256, 0, s>>>(
+                  static_cast<bf16_t*>(a.C), a.ldc, a.part, a.c_split, a.ksplit_used, a.offsets,
+                  a.n_groups, a.cap, a.N));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace
 
 // Rows of an expert's first weight per hidden unit: 2 (gate and up) for
 // SwiGLU, 1 for the SiLU expert.
 long first_rows(const moe_ffn_set& f) { return f.activation == MOE_ACT_SILU ? 1 : 2; }
 
+size_t ffn_fwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
+  return row_parts_bytes(sets, n_sets, bf16, d);
+}
+
 size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
-  size_t bytes = align_up(kCounterWords * sizeof(int));
+  size_t bytes = align_up(kCounterWords * sizeof(int)) + row_parts_bytes(sets, n_sets, bf16, d);
   for (int i = 0; i < n_sets; ++i) {
     const moe_ffn_set& f = sets[i];
     const long H = f.H, R1 = first_rows(f);
@@ -1416,7 +1601,7 @@ size_t ffn_bwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d) {
   return bytes;
 }
 
-hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d, void* ws,
                                hipStream_t s) {
   GemmArgs g[2]{}, o[2]{};
   const bool silu = sets[0].activation == MOE_ACT_SILU;  // the same for every set
@@ -1438,9 +1623,11 @@ hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     b.C = f.yp; b.ldc = d;
     b.N = d; b.K = f.H;
   }
+  if (bf16) assign_row_parts(o, sets, n_sets, bf16, d, static_cast<char*>(ws));
   hipError_t e = silu ? run_gemm<UP_FWD>(g, n_sets, bf16, s) : run_gemm<GU_FWD>(g, n_sets, bf16, s);
   if (e != hipSuccess) return e;
-  return run_gemm<DOWN_FWD>(o, n_sets, bf16, s);
+  if ((e = run_gemm<DOWN_FWD>(o, n_sets, bf16, s)) != hipSuccess) return e;
+  return reduce_row_parts(o, n_sets, s);
 }
 
 hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
@@ -1448,7 +1635,8 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
   GemmArgs hh[2]{}, dx[2]{}, wd[2]{}, wgu[2]{};
   // workspace: per-XCD counters, then the split-K partials
   int* counters = static_cast<int*>(ws);
-  char* part = static_cast<char*>(ws) + (ws ? align_up(kCounterWords * sizeof(int)) : 0);
+  char* rows_ws = static_cast<char*>(ws) + (ws ? align_up(kCounterWords * sizeof(int)) : 0);
+  char* part = rows_ws + (ws ? row_parts_bytes(sets, n_sets, bf16, d) : 0);
   struct Reduce { float* dst; const float* parts; int n_parts; size_t n; };
   Reduce red[4];
   int n_red = 0;
@@ -1498,6 +1686,7 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
       }
     }
   }
+  if (bf16 && ws) assign_row_parts(dx, sets, n_sets, bf16, d, rows_ws);
   hipError_t e;
   if (!bf16) {
     e = silu ? run_gemm<DH_BWD>(hh, n_sets, bf16, s) : run_gemm<DHH_BWD>(hh, n_sets, bf16, s);
@@ -1518,6 +1707,7 @@ hipError_t launch_ffn_bwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, in
     if (e != hipSuccess) return e;
     e = run_gemm_bf16<DX_BWD, DWGU>(dx, n_sets, wgu, n_sets, s, ws ? counters + N_XCD : nullptr);
     if (e != hipSuccess) return e;
+    if ((e = reduce_row_parts(dx, n_sets, s)) != hipSuccess) return e;
   }
   for (int r = 0; r < n_red; ++r) {
     const int blocks = (int)std::min<size_t>(8192, (red[r].n / 4 + 255) / 256);

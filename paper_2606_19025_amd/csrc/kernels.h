@@ -44,8 +44,10 @@ hipError_t launch_combine_bwd(const void* dy, const void* yp, int bf16, int T, i
                               float* dtw, hipStream_t s);
 
 // Grouped SwiGLU FFN over 1 or 2 expert sets (moe_ffn_set of the public
-// header), one launch per GEMM kind.
-hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d,
+// header), one launch per GEMM kind.  ws: NULL (no K parts) or
+// ffn_fwd_ws_bytes() bytes, 256-byte aligned; its contents on entry are ignored.
+size_t ffn_fwd_ws_bytes(const moe_ffn_set* sets, int n_sets, int bf16, int d);
+hipError_t launch_ffn_fwd_sets(const moe_ffn_set* sets, int n_sets, int bf16, int d, void* ws,
                                hipStream_t s);
 // ws: NULL (static tile dealing, no split-K) or ffn_bwd_ws_bytes() bytes,
 // 256-byte aligned; its contents on entry are ignored.

@@ -96,6 +96,7 @@ class ResidentMoELayer:
         self.ws_route_bytes = B.moe_route_bwd_workspace_size(T, d, E)
         self.ws_route = e(self.ws_route_bytes, dt=torch.uint8)
         self.ws_ffn, self.ws_ffn_bytes = None, 0  # sized on the first backward
+        self.ws_fwd, self.ws_fwd_bytes = None, 0  # sized on the first forward
         if self.Hs:
             Hs = self.Hs
             self.s_offsets = torch.tensor([0, T], dtype=i32, device=dev)
@@ -170,8 +171,12 @@ class ResidentMoELayer:
             sets.append(B.ffn_set(x, shared_gate_up, shared_down, self.s_offsets, T, self.Hs, 1,
                                   self.s_gu, self.s_h, yp=self.s_y, activation=self.act))
             y_add = self.s_y
+        if self.ws_fwd is None:
+            self.ws_fwd_bytes = B.moe_grouped_ffn_fwd_workspace_size(sets, dt, d)
+            self.ws_fwd = self._alloc(max(self.ws_fwd_bytes, 1), dt=torch.uint8)
         hook()
-        B.moe_grouped_ffn_fwd_sets(sets, dt, d, stream)
+        B.moe_grouped_ffn_fwd_sets(sets, dt, d, self.ws_fwd if self.ws_fwd_bytes else None,
+                                   self.ws_fwd_bytes, stream)
         hook()
         B.moe_combine_fwd(self.yp, dt, T, d, k, cap, self.topk_w, self.inv_perm, y_add, self.y,
                           stream)

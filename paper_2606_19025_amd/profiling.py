@@ -67,6 +67,7 @@ _SYMBOLS = [
     (r"unpermute_kernel", lambda m: "unpermute"),
     (r"expert_delta_kernel", lambda m: "expert_delta"),
     (r"splitk_reduce_kernel", lambda m: "splitk_reduce"),
+    (r"splitk_rows_reduce_kernel", lambda m: "splitk_rows_reduce"),
     (r"zero_counters_kernel", lambda m: "zero_counters"),
     (r"adamw_kernel", lambda m: "adamw_step"),
     (r"outer_nesterov_kernel", lambda m: "outer_nesterov"),

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert B.moe_abi_version() == 2
+    assert B.moe_abi_version() == 3
 
 
 def test_workspace_sizes_are_host_only(lib):
@@ -140,14 +140,14 @@ def test_expert_delta_rejects_too_many_peers(lib):
 def test_ffn_sets_reject_bad_arguments(lib):
     p = 256
     ok = B.ffn_set(p, p, p, p, 64, 128, 2, p, p, yp=p)
-    assert B.lib().moe_grouped_ffn_fwd_sets(None, 1, B.MOE_BF16, 128, None) == ERR_ARG
+    assert B.lib().moe_grouped_ffn_fwd_sets(None, 1, B.MOE_BF16, 128, None, 0, None) == ERR_ARG
     arr = (B.moe_ffn_set * 3)(ok, ok, ok)
-    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 3, B.MOE_BF16, 128, None) \
-        == ERR_ARG
+    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 3, B.MOE_BF16, 128, None, 0,
+                                            None) == ERR_ARG
     bad_h = B.ffn_set(p, p, p, p, 64, 100, 2, p, p, yp=p)
     arr = (B.moe_ffn_set * 2)(ok, bad_h)
-    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 2, B.MOE_BF16, 128, None) \
-        == ERR_UNSUPPORTED
+    assert B.lib().moe_grouped_ffn_fwd_sets(C.cast(arr, C.c_void_p), 2, B.MOE_BF16, 128, None, 0,
+                                            None) == ERR_UNSUPPORTED
     no_grad = B.ffn_set(p, p, p, p, 64, 128, 2, p, p, dyp=p, dgu=p, dxp=p)  # dW pointers NULL
     arr = (B.moe_ffn_set * 1)(no_grad)
     assert B.lib().moe_grouped_ffn_bwd_sets(C.cast(arr, C.c_void_p), 1, B.MOE_BF16, 128, 0,
@@ -184,3 +184,25 @@ def test_optimiser_entry_points_reject_bad_arguments(lib):
     assert call_status(lib.moe_replica_mean, p, arr, 17, 10, p) == ERR_ARG
     arr1 = (C.c_void_p * 1)(None)
     assert call_status(lib.moe_replica_mean, p, arr1, 1, 10, p) == ERR_ARG
+
+
+def test_ffn_forward_workspace_holds_the_down_projection_parts(lib):
+    """The forward workspace reserves up to 8 fp32 partials of [cap, d] per
+    set within 256 MiB (none when two do not fit, or in fp32), and a call with
+    a smaller workspace is rejected on the host."""
+    p = 256
+    d = 1024
+    small = B.ffn_set(p, p, p, p, 8192, 2816, 8, p, p, yp=p)     # 32 MiB per part: 8 parts
+    big = B.ffn_set(p, p, p, p, 49152, 1408, 16, p, p, yp=p)     # 192 MiB per part: none
+    one = B.moe_grouped_ffn_fwd_workspace_size([small], B.MOE_BF16, d)
+    assert one >= 8 * 8192 * d * 4
+    assert B.moe_grouped_ffn_fwd_workspace_size([big], B.MOE_BF16, d) == 0
+    assert B.moe_grouped_ffn_fwd_workspace_size([small], B.MOE_F32, d) == 0
+    assert B.moe_grouped_ffn_fwd_workspace_size([small, big], B.MOE_BF16, d) == one
+    arr = (B.moe_ffn_set * 1)(small)
+    assert call_status(lib.moe_grouped_ffn_fwd_sets, C.cast(arr, C.c_void_p), 1, B.MOE_BF16, d,
+                       p * 1024, one - 256) == ERR_ARG
+    assert "workspace" in B.moe_last_error()
+    # the backward's workspace holds dX's parts besides its counters
+    bwd = B.ffn_set(p, p, p, p, 8192, 2816, 8, p, p, dyp=p, dgu=p, dxp=p, dw_gate_up=p, dw_down=p)
+    assert B.moe_grouped_ffn_bwd_workspace_size([bwd], B.MOE_BF16, d) >= one

@@ -8,7 +8,9 @@ one below, at and above 128 rows (a wave pair's share of a tile) and the
 K extents (d, H, 2H) of one to several k-steps of 32 and 64 and ragged token
 counts for the weight-gradient kinds; the backward both without a workspace
 (static tile dealing, no split) and with one (dynamic dealing, split-K of a
-single large group, summed by splitk_reduce).  Both expert forms.
+single large group, summed by splitk_reduce); with workspaces, launches with
+far fewer tiles than CUs, whose down projection and dX cut their reduction
+into parts (summed by splitk_rows_reduce).  Both expert forms.
 
 Every output is compared with the oracle (Sec. 3.2 expert FFN per resident
 expert, App. B.3.1 for the SiLU form) at the bf16 tolerance, normwise.
@@ -43,6 +45,10 @@ CASES = {
     # gradients), so the load ring is never full
     "short-k": ([33, 64, 65, 96, 97, 0, 1, 31, 32], 64, 64, "swiglu", True, 0),
     "short-k-silu": ([33, 64, 65, 96, 97, 0, 1, 31, 32], 64, 64, "silu", False, 0),
+    # far fewer output tiles than CUs with long reductions: the down
+    # projection and dX cut K into parts (fp32 partial rows, then summed)
+    "few-tiles-long-k": ([300, 0, 257, 511], 256, 2048, "swiglu", True, 0),
+    "few-tiles-long-k-silu": ([129, 640], 512, 1536, "silu", True, 1),
 }
 
 
@@ -86,7 +92,11 @@ def test_grouped_ffn_tile_edges(gpu_lib, name):
     t_dwgu = (torch.from_numpy(dw_gu0).cuda() if acc else canary(G, r1 * H, d, dtype=torch.float32))
     t_dwd = (torch.from_numpy(dw_d0).cuda() if acc else canary(G, d, H, dtype=torch.float32))
     fset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, gu, h, yp=yp, activation=act)
-    B.moe_grouped_ffn_fwd_sets([fset], B.MOE_BF16, d)
+    fws, fws_bytes = None, 0
+    if use_ws:
+        fws_bytes = B.moe_grouped_ffn_fwd_workspace_size([fset], B.MOE_BF16, d)
+        fws = torch.full((max(fws_bytes, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+    B.moe_grouped_ffn_fwd_sets([fset], B.MOE_BF16, d, fws, fws_bytes)
     bset = B.ffn_set(t_xp, t_wgu, t_wd, t_off, cap, H, G, gu, h, dyp=t_dyp, dgu=dgu, dxp=dxp,
                      dw_gate_up=t_dwgu, dw_down=t_dwd, activation=act)
     ws, ws_bytes = None, 0
