@@ -20,7 +20,11 @@ Prints ONE JSON line.  Besides the contract fields it carries:
   kernels_cold  the HBM-bound kernels again with a 512 MiB read before every
                 library call (``--cold-steps`` steps), so that each call's first
                 kernel reads its inputs from HBM;
-  cpu_baseline  the CPU oracle on a bounded token sample of the same workload.
+  cpu_baseline  the CPU oracle on a bounded token sample of the same workload;
+  hbm_copy      a plain device copy of 1 GiB and, for each cold-timed kernel,
+                a cold copy moving that kernel's bytes (frac_of_copy_at_size);
+  blas_reference torch.matmul (hipBLASLt) on each GEMM launch's dense
+                equivalent (reference for the MFMA fractions, not in the step).
 
     python bench.py [--gpus 1] [--steps 64] [--warmup 10] [--workload 2]
 
@@ -84,6 +88,8 @@ def parse():
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="make one plain device-to-device copy of a known size before the "
                          "steps, the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
+    ap.add_argument("--no-blas-reference", dest="blas_reference", action="store_false",
+                    help="skip timing torch.matmul (hipBLASLt) on the GEMMs' dense equivalents")
     ap.add_argument("--no-copy-baseline", dest="copy_baseline", action="store_false",
                     help="skip timing torch's device-to-device copy and read-only sum of 1 GiB "
                          "(the HBM rates a plain streaming kernel reaches on the box; on by "
@@ -158,6 +164,49 @@ def survey_bytes(cfg, n, s):
             "combine_fwd": n * d * s + T * d * s,
             "combine_bwd": T * d * s + 2 * n * d * s + 8 * T * k,
             "unpermute": n * d * s + T * d * s}
+
+
+def blas_reference(cfg, n, expert="swiglu", reps=10):
+    """torch.matmul (hipBLASLt) time of each GEMM launch's work as dense bf16
+    GEMMs: every set as one GEMM over all its rows (routed: M = n executed
+    routes, as if no expert boundaries; shared: M = T), K-ragged kinds as one
+    GEMM with K = those rows.  A reference for the MFMA fractions, not part
+    of the step."""
+    import torch
+    T, d, H = cfg["T"], cfg["d"], cfg["H"]
+    Hs = cfg["n_shared"] * cfg["Hs"]
+    r1 = 1 if expert == "silu" else 2
+    sets = [(n, H)] + ([(T, Hs)] if Hs else [])
+    kinds = {  # launch -> [(M, N, K)]
+        "gemm_gu_fwd": [(m, r1 * h, d) for m, h in sets],
+        "gemm_down_fwd": [(m, d, h) for m, h in sets],
+        "gemm_dhh_dwd": [(m, h, d) for m, h in sets] + [(d, h, m) for m, h in sets],
+        "gemm_dx_dwgu": [(m, d, r1 * h) for m, h in sets] + [(r1 * h, d, m) for m, h in sets],
+    }
+    out = {}
+    for name, shapes in kinds.items():
+        tot_ms, flops = 0.0, 0.0
+        for M, N, K in shapes:
+            if min(M, N, K) <= 0:
+                continue
+            a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+            b = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+            c = a @ b
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                c = a @ b
+            e1.record()
+            e1.synchronize()
+            tot_ms += e0.elapsed_time(e1) / reps
+            flops += 2.0 * M * N * K
+            del a, b, c
+        if tot_ms > 0:
+            tf = flops / (tot_ms * 1e-3) / 1e12
+            out[name] = {"us": round(tot_ms * 1e3, 1), "tflops": round(tf, 1),
+                         "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+    return out
 
 
 def optimizer_work(n_step_params, n_round_params, n_peers):
@@ -563,8 +612,38 @@ def main():
         t_read = best_ms(lambda: src.sum())
         hbm_copy = {"bytes": nb, "copy_GBps": round(2 * nb / t_copy / 1e6, 1),
                     "read_GBps": round(nb / t_read / 1e6, 1), "peak": PEAK_HBM_GBS}
+        # the same copy at each cold-timed kernel's own size (half its bytes
+        # read, half written), the caches flushed before every timed call as
+        # in the cold pass: what a streaming kernel of that size reaches
+        if kernels_cold:
+            flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+            at_size = {}
+            for name, ent in kernels_cold.items():
+                moved = ent["achieved"] * 1e9 * ent["avg_us"] * 1e-6  # algorithmic bytes
+                half = max(int(moved / 2) // 16 * 4, 4)
+                a_, b_ = src[:half], dst[:half]
+                ts = []
+                for _ in range(6):
+                    flush.sum()
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    b_.copy_(a_)
+                    e1.record()
+                    e1.synchronize()
+                    ts.append(e0.elapsed_time(e1))
+                rate = 2 * 4 * half / min(ts[1:]) / 1e6
+                at_size[name] = {"bytes": 8 * half, "copy_GBps": round(rate, 1)}
+                ent["frac_of_copy_at_size"] = round(ent["achieved"] / rate, 4)
+            hbm_copy["cold_copy_at_kernel_size"] = at_size
+            del flush
         del src, dst
         log(f"[bench] copy baseline {hbm_copy}")
+
+    blas = None
+    if args.blas_reference and s_bytes == 2:
+        blas = blas_reference(cfg, n, args.expert)
+        log(f"[bench] hipBLASLt dense reference {blas}")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -617,6 +696,7 @@ def main():
         "kernels": kernels,
         "kernels_cold": kernels_cold,
         "hbm_copy": hbm_copy,
+        "blas_reference": blas,
     }
     print(json.dumps(out), flush=True)
 
