@@ -64,6 +64,7 @@ _SYMBOLS = [
     (r"dispatch_place_kernel", lambda m: "dispatch_place"),
     (r"combine_fwd_kernel", lambda m: "combine_fwd"),
     (r"combine_bwd_kernel", lambda m: "combine_bwd"),
+    (r"combine_bwd_rows_kernel", lambda m: "combine_bwd"),
     (r"unpermute_kernel", lambda m: "unpermute"),
     (r"expert_delta_kernel", lambda m: "expert_delta"),
     (r"splitk_reduce_kernel", lambda m: "splitk_reduce"),
@@ -120,6 +121,23 @@ def _is_copy(symbol: str) -> bool:
     return "copyBuffer" in symbol or "copy_kernel" in symbol
 
 
+def _mangled_kernel_name(sym: str) -> str:
+    """The *_kernel component of an Itanium-mangled nested name
+    (_ZN<len><id><len><id>...), or sym itself."""
+    i = sym.find("N") + 1 if sym.startswith("_ZN") else 2
+    found = sym
+    while i < len(sym) and sym[i].isdigit():
+        j = i
+        while j < len(sym) and sym[j].isdigit():
+            j += 1
+        n = int(sym[i:j])
+        comp = sym[j:j + n]
+        if comp.endswith("_kernel"):
+            found = comp
+        i = j + n
+    return found
+
+
 def kernel_stats(stats_csv: str, out: str, command: str) -> None:
     rows = list(csv.DictReader(open(stats_csv)))
     agg = collections.OrderedDict()
@@ -135,6 +153,8 @@ def kernel_stats(stats_csv: str, out: str, command: str) -> None:
         a[2] = min(a[2], mn)
         a[3] = max(a[3], mx)
         sym = r["Name"].replace("void ", "").replace("moe::(anonymous namespace)::", "")
+        if sym.startswith("_Z"):  # mangled (templates on bf16): the kernel's own name
+            sym = _mangled_kernel_name(sym)
         a[4].add(re.sub(r"\(.*", "", sym))
     total = sum(v[1] for v in agg.values())
     with open(out, "w") as f:

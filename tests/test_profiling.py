@@ -17,6 +17,10 @@ def test_symbols_map_to_timing_names():
         == "gemm_dhh_dwd"
     assert P.timing_name("_ZN3moe12_GLOBAL__N_118combine_fwd_kernelIDF16bEEvPKT_") == "combine_fwd"
     assert P.timing_name("moe::(anonymous namespace)::route_bwd_mfma_kernel(x)") == "route_bwd_mfma"
+    assert P.timing_name("_ZN3moe12_GLOBAL__N_123combine_bwd_rows_kernelIDF16bEEvPKT_S4_") \
+        == "combine_bwd"
+    assert P.timing_name("moe::(anonymous namespace)::splitk_rows_reduce_kernel(x)") \
+        == "splitk_rows_reduce"
     assert P.timing_name("__amd_rocclr_copyBuffer") is None
     assert P.source_digest("gemm_gu_fwd") != P.source_digest("route_fwd")
 
@@ -52,3 +56,25 @@ def test_digest_ignores_comments_and_layout():
     c = "int f(int x) { return 3 * x; }"
     assert P._code_only(a) == P._code_only(b)
     assert P._code_only(a) != P._code_only(c)
+
+
+def test_every_kernel_of_the_library_has_a_timing_name():
+    """Each __global__ kernel in csrc/ maps to a name, so that no kernel is
+    missing from the committed summaries."""
+    import glob
+    import os
+    import re
+    names = set()
+    for f in glob.glob(os.path.join(P.CSRC, "*.hip")):
+        src = open(f).read()
+        names |= set(re.findall(r"__global__\s+(?:__launch_bounds__\([^)]*\)\s+)?void\s+(\w+_kernel)\s*\(", src))
+    assert len(names) >= 15
+    for n in sorted(names):
+        # (template arguments as a templated kernel would carry them)
+        assert P.timing_name(f"void moe::(anonymous namespace)::{n}<0, 0>(x)") is not None, n
+
+
+def test_mangled_names_shorten_to_the_kernel():
+    assert P._mangled_kernel_name(
+        "_ZN3moe12_GLOBAL__N_123combine_bwd_rows_kernelIDF16bEEvPKT_S4_") == "combine_bwd_rows_kernel"
+    assert P._mangled_kernel_name("not_mangled") == "not_mangled"
