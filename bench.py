@@ -620,7 +620,8 @@ def main():
             at_size = {}
             for name, ent in kernels_cold.items():
                 moved = ent["achieved"] * 1e9 * ent["avg_us"] * 1e-6  # algorithmic bytes
-                half = max(int(moved / 2) // 16 * 4, 4)
+                # fp32 elements of each half, at most the 1 GiB buffers
+                half = min(max(int(moved / 8) // 4 * 4, 4), src.numel())
                 a_, b_ = src[:half], dst[:half]
                 ts = []
                 for _ in range(6):
