@@ -17,11 +17,11 @@
 // The first four are ragged in M (tiles are laid over the groups from the
 // device-side offsets; no host read-back), the last two ragged in K.
 //
-// bf16: v_mfma_f32_32x32x16_bf16 with fp32 accumulation in a persistent
+// bf16: v_mfma_f32_16x16x32_bf16 with fp32 accumulation in a persistent
 // kernel with 256 x 256 block tiles of 8 waves fed from an LDS ring by
-// global -> LDS DMA (details at gemm_bf16_kernel and Cfg).  One launch per
-// GEMM kind
-// covers up to two expert sets (routed and shared experts).
+// global -> LDS DMA (details at gemm_bf16_kernel and Cfg).  One launch
+// covers up to two expert sets (routed and shared experts) of one kind, or
+// in the backward two independent kinds (dHh with dW_d, dX with dW_gu).
 // fp32: a plain 64x64 SIMT tile (4x4 outputs per thread) with the same
 // epilogues; used for fp32 layers.
 #include <type_traits>
@@ -261,35 +261,29 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 //
-// Persistent: one 512-thread block per CU loops over output tiles.  Block tile
-// 256 x 256; the 8 waves (two per SIMD) form a 4 x 2 grid and each owns a
-// 64 x 128 sub-tile = 2 x 4 v_mfma_f32_32x32x16_bf16 tiles (128 fp32
-// accumulators per lane), reading 6 fragments (6 KB per wave) per 8 MFMAs.
+// Persistent: one 512-thread block per CU loops over output tiles, of up to
+// two GEMM kinds KA and KB (GemmLaunch).  Block tile 256 x 256; the 8 waves
+// (two per SIMD) form a 4 x 2 grid and each owns a 64 x 128 sub-tile = 4 x 8
+// v_mfma_f32_16x16x32_bf16 tiles (128 fp32 accumulators per lane).
 //
 // Operands stream through a ring of NS LDS stages of one k-step (GK) each,
 // filled with 16-byte global -> LDS DMA: M-ragged kinds NS = 2 stages of
 // GK = 64 (64 KB each), weight-gradient kinds NS = 4 stages of GK = 32
-// (32 KB each).  A k-step is GK / 16 k16-steps; per k-step and wave:
-//   k16-steps 0 .. GK/16 - 2: 8 MFMAs each, interleaved with the LDS reads of
-//   the next k16-step
-//   wait for own DMA of k-step kt+1 (vmcnt leaves the later k-steps' loads in
-//   flight) and for the LDS reads, barrier (stage kt+1 complete, stage kt
-//   free)
-//   last k16-step: its MFMAs, interleaved with the LDS reads of k-step kt+1's
-//   k16-step 0 and the DMA of k-step kt+NS into stage kt
-// So every load has NS - 1 k-steps less one k16-step to land.
-// Every k-step issues the same number of DMA loads (past the last k-step the
-// last one is loaded again into an unused stage) so vmcnt counting is uniform;
-// the ring is drained (vmcnt(0)) before a block moves to its next tile.
+// (32 KB each).  A k-step is GK / 32 k32-steps; a k32-step is 8 chunks of 4
+// MFMAs (k32step).  The last k32-step of k-step kt waits for the wave's DMA
+// of k-step kt+1 (vmcnt leaves the later k-steps' loads in flight), takes the
+// barrier after which stage kt is free, and refills it with k-step kt+NS (if
+// the tile has one).
 //
 // Tile order (see tile_decode): bands of GROUP_M m-tiles (2 to 8, per kind,
-// see Cfg).  Workgroups are dealt to the 8 XCDs round-robin by id, so block b
-// works on tiles of the ranges assigned to XCD b % 8 (an eighth of each set's
-// tiles): the 32 tiles an XCD runs at a time form a band rectangle whose
-// operand panels its L2 serves.  Output tiles
-// end in an epilogue: bf16 results are staged through the drained ring so
-// global accesses are whole 16-byte chunks; fp32 weight gradients are stored
-// (or added) straight from the accumulators.
+// see Cfg).  Each XCD takes an equal share of every set's tile range (blocks
+// are placed on the 8 XCDs round-robin by id): the 32 tiles an XCD runs at a
+// time form a band rectangle whose operand panels its L2 serves.  With
+// counters the blocks of an XCD take its tiles one at a time.  Output tiles
+// end in an epilogue: bf16 results are staged through a wave-private region
+// of the ring so global accesses are whole 16-byte chunks; fp32 weight
+// gradients and K-part partials are stored (or added) straight from the
+// accumulators.
 //
 // LDS layouts (per operand and stage):
 //  k-contiguous operand (rows = M or N index): row r holds GK k (2 GK bytes);
@@ -301,9 +295,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 //    chunk c sits at position c ^ (2 * (k & 3)).  A fragment is two
 //    ds_read_b64_tr_b16: in each 16-lane group, lane j points at (k0 + j/4,
 //    m0 + 4*(j%4)) and lane i receives m0 + i for k0..k0+3.
-// The MFMA is issued with the B fragment as its first operand, so lane l
-// accumulates C[m0 + l%32][n0 + 8q + 4(l/32) + t] in register 4q + t: four
-// consecutive output columns per lane, stored with 8- or 16-byte vectors.
+// The MFMA is issued with the B fragment as its first operand, so for each
+// 16 x 16 tile lane l accumulates C[m0 + l%16][n0 + 4(l/16) + t] in register
+// t: four consecutive output columns per lane.
 // Out-of-range M/N rows are clamped to valid memory (their outputs are not
 // stored); k-rows past a group's last row (ragged K) are loaded with an
 // offset past the buffer resource's range, which reads zeros, so they
@@ -314,7 +308,7 @@ constexpr int N_XCD = 8;
 
 // Tile configuration per kind.  Every kind runs 256 x 256 block tiles with 8
 // waves (two per SIMD), one block per CU; each wave owns 64 x 128 of the tile
-// (2 x 4 MFMA tiles, 128 accumulators).  Measured on the fine-grained
+// (4 x 8 MFMA tiles of 16 x 16, 128 accumulators).  Measured on the fine-grained
 // workload against 4 waves of 128 x 128 (one per SIMD): DOWN_FWD and DX_BWD
 // 9 % faster, the weight-gradient kinds level; and against 128 x 256 tiles at
 // two blocks per CU (which padded ragged groups less): GU_FWD 9 % and DHH_BWD
