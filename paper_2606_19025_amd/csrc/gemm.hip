@@ -1561,7 +1561,9 @@ hipError_t reduce_row_parts(const GemmArgs* args, int n_sets, hipStream_t s) {
     const GemmArgs& a = args[i];
     if (a.ksplit_max <= 1) continue;
     const long n8 = (long)a.cap * a.N / 8;
-    const int blocks = (int)std::max<long>(1, std::min<long>(4096, (n8 + 255) / 256));
+    // grid-stride: 4 blocks per CU stream the partials at full rate, and a call
+    // that chose one part (every block returns at once) stays short
+    const int blocks = (int)std::max<long>(1, std::min<long>(4L * num_cus(), (n8 + 255) / 256));
     MOE_TIMED("splitk_rows_reduce", s,
               splitk_rows_reduce_kernel<<<blocks, 256, 0, s>>>(
                   static_cast<bf16_t*>(a.C), a.ldc, a.part, a.c_split, a.ksplit_used, a.offsets,
