@@ -11,6 +11,7 @@ resident in HBM; the timed region holds exactly ``--steps`` steps bracketed by
 torch.cuda.synchronize().
 
 Prints ONE JSON line.  Besides the contract fields it carries:
+  step_spread   median, p10 and p90 of single steps, timed again one by one;
   roofline      the dominant kernel's achieved rate vs the MI355X peak, from
                 algorithmic flops (or bytes) per launch and its average launch
                 duration measured with HIP events in a second pass of the same
@@ -183,6 +184,8 @@ def blas_reference(cfg, n, expert="swiglu", reps=10):
         "gemm_dhh_dwd": [(m, h, d) for m, h in sets] + [(d, h, m) for m, h in sets],
         "gemm_dx_dwgu": [(m, d, r1 * h) for m, h in sets] + [(r1 * h, d, m) for m, h in sets],
     }
+    # and one large square GEMM: what the library reaches at its best shape
+    kinds["dense_8192_cubed"] = [(8192, 8192, 8192)]
     out = {}
     for name, shapes in kinds.items():
         tot_ms, flops = 0.0, 0.0
@@ -489,6 +492,21 @@ def main():
     t_act = int((local >= 0).any(axis=1).sum())
     log(f"[bench] {ms_per_step:.3f} ms/step ({wall:.2f} s wall), n={n}, tokens/s={value:.4g}")
 
+    # the spread of single steps: the same steps again, an event pair around
+    # each (a round-boundary step includes the expert delta)
+    import numpy as np
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for i in range(args.steps):
+        evs[i][0].record()
+        step(i)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) for a, b in evs])
+    step_spread = {"median_ms": round(float(np.median(per)), 4),
+                   "p10_ms": round(float(np.percentile(per, 10)), 4),
+                   "p90_ms": round(float(np.percentile(per, 90)), 4)}
+
     kernels = {}
     roofline = None
     if not args.no_kernel_timing:
@@ -681,6 +699,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "step_spread": step_spread,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
