@@ -102,11 +102,13 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   };
   // the lane's 32 consecutive elements of a slice feed the 4 k16 MFMA steps
   // in the same order for the token and the expert operand
-  auto load_slice = [&](int kb, bf16x8_t* av, bf16x8_t (*bv)[4], int u) {
-    const int c0 = kb * 64 + half * 32;
+  auto read_x = [&](bf16x8_t* av, int u) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       av[q] = *reinterpret_cast<const bf16x8_t*>(&xst[wave][u][xswz(row, half * 4 + q)]);
+  };
+  auto load_w = [&](int kb, bf16x8_t (*bv)[4]) {
+    const int c0 = kb * 64 + half * 32;
 #pragma unroll
     for (int eb = 0; eb < NEB; ++eb) {
       const int e = eb * 32 + row;
@@ -122,12 +124,16 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   for (int kb = wave; kb < n_slices; kb += UNR * RT_WAVES) {
     bf16x8_t av[UNR][4], bv[UNR][NEB][4];
     u32x4_t xv[UNR][4];
+    // the W_r fragments (L2) are requested with the x rows (HBM), not after
+    // the x rows have been staged
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) load_w(kb + u * RT_WAVES, bv[u]);
 #pragma unroll
     for (int u = 0; u < UNR; ++u) load_x(kb + u * RT_WAVES, xv[u]);  // zeros past the end
 #pragma unroll
     for (int u = 0; u < UNR; ++u) store_x(u, xv[u]);
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) load_slice(kb + u * RT_WAVES, av[u], bv[u], u);
+    for (int u = 0; u < UNR; ++u) read_x(av[u], u);
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
 #pragma unroll
