@@ -758,10 +758,13 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
     }
   }
   // K parts of the linear M-ragged kinds: a tile whose reduction is longer
-  // than the launch's average load per block (work / blocks) would finish
-  // last with most CUs idle (few tiles: small groups, narrow N), so it is cut
-  // into parts of about that load (at most ksplit_max, at least two k-steps
-  // each).  Every block derives the same choice from the group table.
+  // than 4/3 of the launch's average load per block (work / blocks) would
+  // finish last with most CUs idle (few tiles: small groups, narrow N), so it
+  // is cut into parts of about that length (at most ksplit_max, at least two
+  // k-steps each): the parts then fill about three quarters of the blocks.
+  // (Filling all of them was slower: each part writes a whole fp32 partial
+  // tile, and more parts moved more bytes than they saved in time.)  Every
+  // block derives the same choice from the group table.
 #pragma unroll
   for (int q = 0; q < kMaxSets; ++q) {
     if (q < L.n_sets && L.s[q].ksplit_max > 1) {
@@ -769,7 +772,7 @@ __global__ __launch_bounds__(512, 2) void gemm_bf16_kernel(GemmLaunch L) {
         constexpr int KIND = decltype(kc)::value;
         if constexpr (KIND == DOWN_FWD || KIND == DX_BWD) {
           const GemmArgs& a = L.s[q];
-          const long want = work > 0 ? ((long)a.K * gridDim.x + work - 1) / work : 1;
+          const long want = work > 0 ? ((long)a.K * gridDim.x * 3 / 4 + work - 1) / work : 1;
           const int most = max(1, a.K / (2 * Cfg<KIND>::GK));
           prt[q] = (int)max(1L, min(want, (long)min(a.ksplit_max, most)));
           prt[q] = __builtin_amdgcn_readfirstlane(prt[q]);
