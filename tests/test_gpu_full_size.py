@@ -16,6 +16,8 @@ hold at any size:
 * exact skip-token outputs of every fully skipped token;
 * the round-boundary delta of the fine-grained workload at its full parameter
   count, bit-exact.
+* run-to-run determinism of the mid-size and fine-grained layers (K parts,
+  dynamically dealt tiles), bit-exact.
 """
 import numpy as np
 import pytest
@@ -25,8 +27,8 @@ from oracle import moe_oracle as O
 from paper_2606_19025_amd import inputs as I
 from paper_2606_19025_amd.layer import expert_delta
 
-from .parity_helpers import (TOL, assert_close, host, make_layer, record_errors, run_gpu_layer,
-                             say)
+from .parity_helpers import (TOL, assert_close, gpu_outputs, host, make_layer, record_errors,
+                             run_gpu_layer, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -165,3 +167,21 @@ def test_full_size_expert_delta(gpu_lib, wl):
     assert torch.equal(dl.cpu().view(torch.int32), torch.from_numpy(dl_ref).view(torch.int32))
     assert torch.equal(avg.cpu().view(torch.int32), torch.from_numpy(avg_ref).view(torch.int32))
     say(f"[full] expert delta over {n} parameters bit-exact")
+
+
+@pytest.mark.parametrize("wl", [1, 2])
+def test_full_size_layer_is_deterministic(gpu_lib, wl):
+    """Three steps of the mid-size layer (its down projection and dX cut into K
+    parts) and of the fine-grained one (shared expert, merged backward
+    launches) give bit-identical outputs and gradients, whichever blocks the
+    dynamically dealt tiles ran on."""
+    say(f"[determinism] workload {wl}: inputs")
+    inp = I.make_layer_inputs(wl)
+    L, _ = run_gpu_layer(inp)
+    first = gpu_outputs(L)
+    for rep in (1, 2):
+        say(f"[determinism] workload {wl}: repeat {rep}")
+        run_gpu_layer(inp, layer=L)
+        again = gpu_outputs(L)
+        for key, v in first.items():
+            assert np.array_equal(v, again[key]), f"{key} differs on repeat {rep}"
