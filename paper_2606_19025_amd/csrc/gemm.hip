@@ -309,8 +309,8 @@ constexpr int N_XCD = 8;
 // Tile configuration per kind.  Every kind runs 256 x 256 block tiles with 8
 // waves (two per SIMD), one block per CU; each wave owns 64 x 128 of the tile
 // (4 x 8 MFMA tiles of 16 x 16, 128 accumulators).  Measured on the fine-grained
-// workload against 4 waves of 128 x 128 (one per SIMD): DOWN_FWD and DX_BWD
-// 9 % faster, the weight-gradient kinds level; and against 128 x 256 tiles at
+// workload against 4 waves of 128 x 128 (one per SIMD, 256 accumulators in
+// AGPRs): every launch 6-12 % faster; and against 128 x 256 tiles at
 // two blocks per CU (which padded ragged groups less): GU_FWD 9 % and DHH_BWD
 // 3 % faster.  The second wave of a SIMD issues MFMAs while the first waits
 // on its operand loads; the 1.5x fragment reads per MFMA of the narrower wave
