@@ -432,7 +432,7 @@ def main():
             # every expert at its own step count; restarted experts warm up
             # over one round
             o["steps"] = o["steps"] + 1
-            lrs = np.array([lr * min(1.0, t / args.round_every) for t in o["steps"]], np.float32)
+            lrs = B.moe_warmup_lr(o["steps"], lr, args.round_every)
             for p, grad in ((0, L.dw_gate_up), (1, L.dw_down)):
                 b, e, row = o["rows"][p]
                 B.moe_adamw_step_rows(th1[b:e], grad, o["m"][b:e], o["v"][b:e], Er, row,

@@ -406,6 +406,20 @@ int moe_copy_expert_rows(const float* src, const int32_t* src_row, float* dst,
                          hipStream_t stream);
 
 /*
+ * moe_warmup_lr (host only): the learning rate of each resident expert under
+ * the warm-up that Sec. 3.4 prescribes for experts new to a worker.  The
+ * paper gives no shape; this library's reading is linear over warmup_steps
+ * local steps counted from the (re)start of the expert's optimiser state, so
+ * lr_out[r] = (float)(lr * min(1, steps[r] / warmup_steps)), evaluated in
+ * double and rounded once; warmup_steps <= 0 gives lr to every row.  Experts
+ * kept across a migration keep their count and so leave the warm-up on
+ * schedule.  steps (each >= 0) and lr_out are HOST arrays of n_rows (>= 0);
+ * MOE_ERR_ARG on a NULL array, a negative count or a non-finite lr.  The
+ * rates feed moe_adamw_step_rows.
+ */
+int moe_warmup_lr(const int* steps, int n_rows, double lr, int warmup_steps, float* lr_out);
+
+/*
  * moe_adamw_step_rows: moe_adamw_step over n_rows experts of row_len
  * parameters each, with expert r at its own step count steps[r] >= 1 (its
  * steps since its state was (re)started) and learning rate lr[r] (the

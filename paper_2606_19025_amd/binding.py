@@ -27,8 +27,8 @@ EXPORTS = [
     "moe_grouped_ffn_bwd_workspace_size", "moe_grouped_ffn_bwd_sets", "moe_combine_fwd",
     "moe_combine_bwd",
     "moe_expert_delta", "moe_adamw_step", "moe_outer_nesterov", "moe_replica_mean",
-    "moe_gen_placement", "moe_migration_map", "moe_copy_expert_rows", "moe_adamw_step_rows",
-    "moe_timing_enable", "moe_timing_collect",
+    "moe_gen_placement", "moe_migration_map", "moe_copy_expert_rows", "moe_warmup_lr",
+    "moe_adamw_step_rows", "moe_timing_enable", "moe_timing_collect",
 ]
 
 
@@ -72,6 +72,7 @@ _SIGS = {
     "moe_gen_placement": (_I, [_I, _I, _I, _P, _P, _P]),
     "moe_migration_map": (_I, [_P, _I, _P, _I, _P]),
     "moe_copy_expert_rows": (_I, [_P, _P, _P, _P, _I, _Z, _P, _P]),
+    "moe_warmup_lr": (_I, [_P, _I, C.c_double, _I, _P]),
     "moe_adamw_step_rows": (_I, [_P, _P, _P, _P, _I, _Z, _P, _P, _F, _F, _F, _F, _P, _P]),
     "moe_timing_enable": (_I, [_I]),
     "moe_timing_collect": (_I, [_P, _I, C.POINTER(C.c_int)]),
@@ -312,6 +313,16 @@ def moe_migration_map(prev_set, new_set):
     _check("moe_migration_map", lib().moe_migration_map(
         pp, len(prev), npp, len(new), out.ctypes.data_as(C.c_void_p)))
     return out[:len(new)]
+
+
+def moe_warmup_lr(steps, lr, warmup_steps):
+    """fp32 learning rate per expert row from its steps since its state (re)started."""
+    import numpy as np
+    st, sp = _host_i32(steps)
+    out = np.zeros(max(len(st), 1), np.float32)
+    _check("moe_warmup_lr", lib().moe_warmup_lr(sp, len(st), float(lr), int(warmup_steps),
+                                                out.ctypes.data_as(C.c_void_p)))
+    return out[:len(st)]
 
 
 def moe_copy_expert_rows(src, src_row, dst, n_rows, row_len, dst_row=None, dst_bf16=None,

@@ -553,6 +553,18 @@ int moe_copy_expert_rows(const float* src, const int32_t* src_row, float* dst,
                     "moe_copy_expert_rows");
 }
 
+int moe_warmup_lr(const int* steps, int n_rows, double lr, int warmup_steps, float* lr_out) {
+  REQUIRE(n_rows >= 0, "n_rows = %d must be >= 0", n_rows);
+  REQUIRE(n_rows == 0 || (steps && lr_out), "steps and lr_out must not be NULL");
+  REQUIRE(std::isfinite(lr), "lr must be finite");
+  for (int r = 0; r < n_rows; ++r) REQUIRE(steps[r] >= 0, "steps[%d] = %d must be >= 0", r, steps[r]);
+  for (int r = 0; r < n_rows; ++r) {
+    const double f = warmup_steps > 0 ? std::min(1.0, (double)steps[r] / (double)warmup_steps) : 1.0;
+    lr_out[r] = (float)(lr * f);
+  }
+  return MOE_OK;
+}
+
 int moe_adamw_step_rows(float* theta, const float* grad, float* m, float* v, int n_rows,
                         size_t row_len, const int* steps, const float* lr, float beta1,
                         float beta2, float eps, float weight_decay, void* theta_bf16,

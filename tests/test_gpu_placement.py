@@ -93,8 +93,11 @@ def test_random_placement_round_boundary(gpu_lib):
     # per-expert AdamW: kept experts continue their count, new ones restart
     # with the warm-up
     steps = steps + 1
-    lr = np.array([1e-3 * (1.0 if mig[r] >= 0 else O.warmup_scale(steps[r], WARMUP))
-                   for r in range(N_le)], np.float32)
+    lr = B.moe_warmup_lr(steps, 1e-3, WARMUP)
+    assert np.array_equal(lr, np.array([1e-3 * O.warmup_scale(int(s), WARMUP) for s in steps],
+                                       np.float32))
+    # the kept experts are past their warm-up, the new ones start it
+    assert np.all(lr[mig >= 0] == np.float32(1e-3)) and np.all(lr[mig < 0] < np.float32(1e-3))
     grad = L.dw_gate_up.reshape(N_le, gu_len)
     th_before, m_before, v_before = (t.cpu().numpy().copy() for t in (theta_gu, m_new, v_new))
     g_host = grad.cpu().numpy()

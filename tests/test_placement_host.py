@@ -40,3 +40,26 @@ def test_migration_map_matches_oracle(lib):
         assert np.array_equal(B.moe_migration_map(prev, new), O.migration_map(prev, new))
     with pytest.raises(B.MoeError):
         B.moe_migration_map([1, 2], [3, 3])  # not strictly ascending
+
+
+def test_warmup_lr_matches_oracle(lib):
+    """The warm-up of experts new to a worker (Sec. 3.4; linear over W local
+    steps from the restart of the expert's state) against the oracle's
+    schedule, bit for bit, and its closed form."""
+    g = np.random.default_rng(11)
+    for W in (0, 1, 4, 32, 1000):
+        steps = g.integers(0, 3 * max(W, 1) + 2, 64)
+        for lr in (1e-3, 3e-4, 0.7):
+            got = B.moe_warmup_lr(steps, lr, W)
+            ref = np.array([lr * O.warmup_scale(int(s), W) for s in steps], np.float32)
+            assert np.array_equal(got, ref), (W, lr)
+    assert np.array_equal(B.moe_warmup_lr([0, 1, 2, 4, 9], 1.0, 4),
+                          np.float32([0.0, 0.25, 0.5, 1.0, 1.0]))
+    assert B.moe_warmup_lr([], 1e-3, 4).size == 0
+
+
+def test_warmup_lr_rejects_bad_arguments(lib):
+    with pytest.raises(B.MoeError):
+        B.moe_warmup_lr([1, -1], 1e-3, 4)
+    with pytest.raises(B.MoeError):
+        B.moe_warmup_lr([1], float("nan"), 4)
