@@ -215,12 +215,33 @@ DEVI uint32_t sel_key(float v) {
 
 constexpr int RT_KSEL = 8;
 
+// Lane permutations within a row of 16 lanes (DPP), applied to a 64-bit value
+// (its two halves moved alike): xor 1 and xor 2 inside each quad, then lane
+// i <- 7 - i inside each half-row and lane i <- 15 - i inside the row.  After
+// taking the maximum with each in turn, every lane of the row holds the row's
+// maximum.
+template <int CTRL>
+DEVI uint64_t row_perm64(uint64_t v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+DEVI uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+DEVI uint64_t row16_max64(uint64_t m) {
+  m = max64(m, row_perm64<0xB1>(m));   // quad_perm [1, 0, 3, 2]
+  m = max64(m, row_perm64<0x4E>(m));   // quad_perm [2, 3, 0, 1]
+  m = max64(m, row_perm64<0x141>(m));  // row_half_mirror
+  m = max64(m, row_perm64<0x140>(m));  // row_mirror
+  return m;
+}
+
 // Top-k (k <= RT_KSEL), gate weights and local ids of the block's tokens, 16
 // lanes per token (all RT_WAVES waves: wave w takes tokens 4w .. 4w+3): lane
 // s of a group holds experts s, s + 16, ... as 64-bit keys (order-preserving
 // logit key, then the inverted expert id, so that equal logits rank the lower
-// id first; 0 = taken or absent).  Round j takes the group's largest key by
-// xor shuffles and lane j keeps it, so the selections come out in rank order.
+// id first; 0 = taken or absent).  Round j takes the group's largest key (a
+// row of 16 lanes, by DPP moves) and lane j keeps it, so the selections come
+// out in rank order.
 template <int LDZ, int NE>
 DEVI void select_groups(const RouteFwdArgs& a, const float* zl, int t0, const int* lmap) {
   const int lane = threadIdx.x & 63;
@@ -240,12 +261,7 @@ DEVI void select_groups(const RouteFwdArgs& a, const float* zl, int t0, const in
     uint64_t m = 0ull;
 #pragma unroll
     for (int q = 0; q < NE; ++q) m = cand[q] > m ? cand[q] : m;
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      const uint64_t om = ((uint64_t)(uint32_t)__shfl_xor((int)(m >> 32), o, 64) << 32) |
-                          (uint32_t)__shfl_xor((int)(uint32_t)m, o, 64);
-      m = om > m ? om : m;
-    }
+    m = row16_max64(m);
 #pragma unroll
     for (int q = 0; q < NE; ++q)
       if (cand[q] == m) cand[q] = 0ull;
