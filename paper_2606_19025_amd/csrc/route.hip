@@ -144,7 +144,8 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   }
   // deterministic cross-wave sum (wave order).  Up to 64 experts: every wave
   // stores its partial tile, then each thread adds its entries' RT_WAVES
-  // partials; wider expert sets add wave by wave into zl.
+  // partials and finishes z (bias, temperature, logits store); wider expert
+  // sets add wave by wave into zl and the caller finishes z.
   if constexpr (NEB <= 2) {
     __shared__ float part[RT_WAVES][RT_TOK * NEB * 32];
 #pragma unroll
@@ -161,7 +162,14 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
       float v = part[0][p];
 #pragma unroll
       for (int wv = 1; wv < RT_WAVES; ++wv) v += part[wv][p];
-      if (e < a.E) zl[i * ldz + e] = v;
+      if (e < a.E) {
+        // z = (dot + bias) * inv_tau, stored as it is summed
+        if (a.bias) v += a.bias[e];
+        v *= a.inv_tau;
+        zl[i * ldz + e] = v;
+        const int t = t0 + i;
+        if (a.logits && t < a.T) a.logits[(size_t)t * a.E + e] = v;
+      }
     }
     __syncthreads();
   } else {
@@ -306,8 +314,9 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   if (wave == 0) build_local_map(a.resident, a.E, lmap);
   if constexpr (BF16) logits_mfma<NEB>(a, t0, zl, LDZ);
   else logits_f32(a, t0, zl, LDZ);
-  // z = (dot + bias) * inv_tau
-  for (int p = threadIdx.x; p < RT_TOK * a.E; p += RT_THREADS) {
+  // z = (dot + bias) * inv_tau (logits_mfma finishes it for up to 64 experts)
+  constexpr bool z_done = BF16 && NEB <= 2;
+  for (int p = threadIdx.x; !z_done && p < RT_TOK * a.E; p += RT_THREADS) {
     const int i = p / a.E, e = p % a.E;
     float v = zl[i * LDZ + e];
     if (a.bias) v += a.bias[e];
@@ -316,7 +325,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
     const int t = t0 + i;
     if (a.logits && t < a.T) a.logits[(size_t)t * a.E + e] = v;
   }
-  __syncthreads();
+  if constexpr (!z_done) __syncthreads();  // (logits_mfma ends with one)
 
   if (a.k <= RT_KSEL) {
     static_assert(RT_TOK == 4 * RT_WAVES, "16 lanes per token in every wave");
