@@ -193,6 +193,113 @@ DEVI void logits_mfma(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   }
 }
 
+// bf16 logits for up to 64 experts and d <= 64 XS RT_WAVES.  Wave w reduces
+// the slices w + RT_WAVES u (u < XS) of d.  The x rows and W_r rows of a
+// slice are read whole (8 lanes per 128-byte row piece, two slices ahead of
+// their use, into registers) and staged in the wave's own LDS region, from
+// which the MFMA fragments are read.  (Read in fragment order instead, 32
+// rows per load, W_r took twice as long to arrive.)  The per-wave partial
+// sums are then added in wave order through LDS and z is finished as in
+// logits_mfma.
+template <int NEB, int XS>
+DEVI void logits_mfma_staged(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
+  static_assert(NEB <= 2 && XS >= 2, "up to 64 experts, at least two slices per wave");
+  const bf16_t* x = static_cast<const bf16_t*>(a.x);
+  const bf16_t* w = static_cast<const bf16_t*>(a.w);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int row = lane & 31;
+  const int half = lane >> 5;
+  constexpr int XR = RT_TOK, WR = NEB * 32;  // x and W_r rows of a slice
+  constexpr int SLOT = (XR + WR) * 128;
+  constexpr int STG = RT_WAVES * SLOT;
+  constexpr int PART = RT_WAVES * RT_TOK * NEB * 32 * 4;
+  __shared__ __attribute__((aligned(16))) char lbuf[STG > PART ? STG : PART];
+  char* slot = lbuf + wave * SLOT;
+  // 16-byte chunk c of staged row r at chunk position c ^ ((r >> 1) & 7): the
+  // fragment reads (16 consecutive rows, one chunk) are free of bank conflicts
+  auto swz = [](int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); };
+  const int n_slices = (a.d + 63) / 64;
+  const u32x4_t zero4 = {0u, 0u, 0u, 0u};
+  struct Piece {
+    u32x4_t x[XR / 8], w[WR / 8];
+  };
+  auto load = [&](int kb, Piece& p) {
+    const int c = kb * 64 + (lane & 7) * 8;
+    const bool ok = kb < n_slices && c + 8 <= a.d;
+#pragma unroll
+    for (int j = 0; j < XR / 8; ++j) {
+      const int t = t0 + j * 8 + (lane >> 3);
+      p.x[j] = ok && t < a.T ? *reinterpret_cast<const u32x4_t*>(x + (size_t)t * a.d + c) : zero4;
+    }
+#pragma unroll
+    for (int j = 0; j < WR / 8; ++j) {
+      const int e = j * 8 + (lane >> 3);
+      p.w[j] = ok && e < a.E ? *reinterpret_cast<const u32x4_t*>(w + (size_t)e * a.d + c) : zero4;
+    }
+  };
+  f32x16_t acc[NEB];
+#pragma unroll
+  for (int eb = 0; eb < NEB; ++eb) acc[eb] = f32x16_t{};
+  Piece pc[XS];
+  load(wave, pc[0]);
+  load(wave + RT_WAVES, pc[1]);
+#pragma unroll
+  for (int u = 0; u < XS; ++u) {
+    const int kb = wave + u * RT_WAVES;
+    if (kb >= n_slices) break;
+    // a wave's LDS accesses run in order: the previous slice's fragment
+    // reads are done before these stores overwrite them
+#pragma unroll
+    for (int j = 0; j < XR / 8; ++j)
+      *reinterpret_cast<u32x4_t*>(slot + swz(j * 8 + (lane >> 3), lane & 7)) = pc[u].x[j];
+#pragma unroll
+    for (int j = 0; j < WR / 8; ++j)
+      *reinterpret_cast<u32x4_t*>(slot + XR * 128 + swz(j * 8 + (lane >> 3), lane & 7)) = pc[u].w[j];
+    if (u + 2 < XS) load(kb + 2 * RT_WAVES, pc[u + 2]);
+    bf16x8_t av[4], bv[NEB][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      av[q] = *reinterpret_cast<const bf16x8_t*>(slot + swz(row, half * 4 + q));
+#pragma unroll
+    for (int eb = 0; eb < NEB; ++eb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        bv[eb][q] = *reinterpret_cast<const bf16x8_t*>(slot + XR * 128 + swz(eb * 32 + row, half * 4 + q));
+#pragma unroll
+    for (int eb = 0; eb < NEB; ++eb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        acc[eb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[q], bv[eb][q], acc[eb], 0, 0, 0);
+  }
+  __syncthreads();  // every wave is done with its staging region: the partial sums reuse it
+  float* part = reinterpret_cast<float*>(lbuf);
+#pragma unroll
+  for (int eb = 0; eb < NEB; ++eb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = (r >> 2) * 8 + half * 4 + (r & 3);
+      part[wave * (RT_TOK * NEB * 32) + i * NEB * 32 + eb * 32 + row] = acc[eb][r];
+    }
+  }
+  __syncthreads();
+  for (int p = threadIdx.x; p < RT_TOK * NEB * 32; p += RT_THREADS) {
+    const int i = p / (NEB * 32), e = p % (NEB * 32);
+    float v = part[p];
+#pragma unroll
+    for (int wv = 1; wv < RT_WAVES; ++wv) v += part[wv * (RT_TOK * NEB * 32) + p];
+    if (e < a.E) {
+      // z = (dot + bias) * inv_tau, stored as it is summed
+      if (a.bias) v += a.bias[e];
+      v *= a.inv_tau;
+      zl[i * ldz + e] = v;
+      const int t = t0 + i;
+      if (a.logits && t < a.T) a.logits[(size_t)t * a.E + e] = v;
+    }
+  }
+  __syncthreads();
+}
+
 DEVI void logits_f32(const RouteFwdArgs& a, int t0, float* zl, int ldz) {
   const float* x = static_cast<const float*>(a.x);
   const float* w = static_cast<const float*>(a.w);
@@ -302,7 +409,8 @@ DEVI void select_groups(const RouteFwdArgs& a, const float* zl, int t0, const in
   }
 }
 
-template <int NEB, bool BF16>
+// XS > 0: bf16 with up to 64 experts and d <= 64 XS RT_WAVES (logits_mfma_staged)
+template <int NEB, bool BF16, int XS>
 __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   constexpr int LDZ = NEB * 32 + 1;
   constexpr int NQ = (NEB * 32 + 63) / 64;  // logits (and selections) per lane
@@ -312,7 +420,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   if (wave == 0) build_local_map(a.resident, a.E, lmap);
-  if constexpr (BF16) logits_mfma<NEB>(a, t0, zl, LDZ);
+  if constexpr (XS > 0) logits_mfma_staged<NEB, XS>(a, t0, zl, LDZ);
+  else if constexpr (BF16) logits_mfma<NEB>(a, t0, zl, LDZ);
   else logits_f32(a, t0, zl, LDZ);
   // z = (dot + bias) * inv_tau (logits_mfma finishes it for up to 64 experts)
   constexpr bool z_done = BF16 && NEB <= 2;
@@ -840,13 +949,33 @@ hipError_t launch_route_fwd(const void* x, const void* w, const float* bias, int
   if (T == 0) return hipSuccess;
   const dim3 grid(ceil_div(T, RT_TOK));
   const int neb = E <= 32 ? 1 : E <= 64 ? 2 : E <= 128 ? 4 : 8;
-#define ROUTE_CASE(N)                                                                 \
-  case N:                                                                             \
-    if (bf16) MOE_TIMED("route_fwd", s, route_fwd_kernel<N, true><<<grid, RT_THREADS, 0, s>>>(a)); \
-    else MOE_TIMED("route_fwd", s, route_fwd_kernel<N, false><<<grid, RT_THREADS, 0, s>>>(a));     \
-    break;
-  switch (neb) { ROUTE_CASE(1) ROUTE_CASE(2) ROUTE_CASE(4) ROUTE_CASE(8) }
-#undef ROUTE_CASE
+  // slices of d per wave for the staged bf16 path (0: not taken)
+  const int xs = (!bf16 || neb > 2) ? 0 : d <= 64 * 4 * RT_WAVES ? 4 : d <= 64 * 8 * RT_WAVES ? 8 : 0;
+#define ROUTE_LAUNCH(N, B, X) \
+  MOE_TIMED("route_fwd", s, route_fwd_kernel<N, B, X><<<grid, RT_THREADS, 0, s>>>(a))
+  switch (neb) {
+    case 1:
+      if (xs == 4) ROUTE_LAUNCH(1, true, 4);
+      else if (xs == 8) ROUTE_LAUNCH(1, true, 8);
+      else if (bf16) ROUTE_LAUNCH(1, true, 0);
+      else ROUTE_LAUNCH(1, false, 0);
+      break;
+    case 2:
+      if (xs == 4) ROUTE_LAUNCH(2, true, 4);
+      else if (xs == 8) ROUTE_LAUNCH(2, true, 8);
+      else if (bf16) ROUTE_LAUNCH(2, true, 0);
+      else ROUTE_LAUNCH(2, false, 0);
+      break;
+    case 4:
+      if (bf16) ROUTE_LAUNCH(4, true, 0);
+      else ROUTE_LAUNCH(4, false, 0);
+      break;
+    default:
+      if (bf16) ROUTE_LAUNCH(8, true, 0);
+      else ROUTE_LAUNCH(8, false, 0);
+      break;
+  }
+#undef ROUTE_LAUNCH
   return hipGetLastError();
 }
 
