@@ -5,10 +5,12 @@
 // unpartitioned under skip-token, routes to non-resident experts are masked):
 //   one block = 32 tokens, 8 waves.  bf16 logits use v_mfma_f32_32x32x16_bf16
 //   (tokens x experts tiles, the d reduction split over the 8 waves and summed
-//   in a fixed order through LDS); fp32 logits use plain FMA loops.  For
+//   in a fixed order through LDS; x and, for up to 64 experts, W_r rows are
+//   read whole and staged in LDS); fp32 logits use plain FMA loops.  For
 //   k <= 8 every wave then selects for 4 tokens, 16 lanes per token
-//   (select_groups); for larger k each wave takes tokens one at a time, lane
-//   = expert, with k wave-wide (max logit, min id) reductions.
+//   (select_groups, row maxima by DPP); for larger k each wave takes tokens
+//   one at a time, lane = expert, with k wave-wide (max logit, min id)
+//   reductions.
 #include "common.h"
 #include "kernels.h"
 #include "timing.h"
