@@ -192,6 +192,44 @@ def test_topk_selection_special_logits(gpu_lib, name):
     np.testing.assert_allclose(host(tw)[fin], wr[fin], rtol=2e-6, atol=1e-7)
 
 
+# The router forward's bf16 logits paths: x and W_r rows staged in LDS for up
+# to 64 experts with d <= 2048 (one to four slices of d per wave) or d <= 4096
+# (up to eight), W_r fragments read directly beyond that or for more experts;
+# ragged d (a partial last slice) and ragged T.  Logits within fp32 rounding
+# of the fp64 oracle; the selection, local ids and gate weights from the
+# GPU's own logits exactly as the oracle makes them.
+ROUTE_SHAPES = [(96, 64, 32), (90, 1096, 64), (80, 2056, 64), (70, 2056, 32), (64, 4104, 64),
+                (64, 520, 200)]
+
+
+@pytest.mark.parametrize("T,d,E", ROUTE_SHAPES)
+def test_router_forward_logits_paths(gpu_lib, T, d, E):
+    k = 4
+    g = np.random.default_rng([T, d, E])
+    say(f"[router] T={T} d={d} E={E}")
+    x = I.bf16_round(g.standard_normal((T, d)).astype(np.float32))
+    w = I.bf16_round((g.standard_normal((E, d)) * 0.05).astype(np.float32))
+    bias = (g.standard_normal(E) * 0.1).astype(np.float32)
+    res = np.zeros(E, np.uint8)
+    res[g.choice(E, max(1, E // 2), replace=False)] = 1
+    logits = torch.full((T, E), float("nan"), dtype=torch.float32, device="cuda")
+    idx = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    loc = torch.full_like(idx, -7)
+    tw = torch.full((T, k), float("nan"), dtype=torch.float32, device="cuda")
+    B.moe_route_mask(dev(x, torch.bfloat16), dev(w, torch.bfloat16), dev(bias, torch.float32),
+                     B.MOE_BF16, T, d, E, k, 0.8, B.GATES["softmax_topk"],
+                     torch.from_numpy(res).cuda(), logits, idx, tw, loc)
+    torch.cuda.synchronize()
+    z = host(logits)
+    e = assert_close("logits", z, O.router_logits(x, w, 0.8, bias), TOL["f32"])
+    record_errors(f"router_forward T={T} d={d} E={E}", {"logits": e})
+    ref = O.topk_select(z, k)
+    assert np.array_equal(host(idx), ref)
+    rank = np.cumsum(res.astype(np.int64)) - 1
+    assert np.array_equal(host(loc), np.where(res[ref] == 1, rank[ref], -1))
+    np.testing.assert_allclose(host(tw), O.gate_weights(z, ref), rtol=2e-6, atol=1e-7)
+
+
 def test_layer_is_deterministic(gpu_lib):
     inp = synth_inputs(600, 128, 12, 3, 128, [0, 3, 5, 8], "bf16", seed=5, shared_hidden=64)
     L1, _ = run_gpu_layer(inp)
