@@ -341,10 +341,8 @@ struct Cfg {
   static constexpr int DMA_MAX = DMA_A > DMA_B ? DMA_A : DMA_B;
   static constexpr int EPI_WAVE = WM * 256;        // epilogue staging per wave
   // m-tiles per band of the tile order, measured per kind on the
-  // fine-grained workload (bands of 2, 4, 8 and 16 tried)
-  static constexpr int GROUP = (KIND == GU_FWD || KIND == UP_FWD || KIND == DOWN_FWD) ? 8
-                               : (KIND == DHH_BWD || KIND == DH_BWD || KIND == DX_BWD) ? 4
-                                                                                        : 2;
+  // fine-grained workload (bands of 1, 2, 4, 8 and 16 tried)
+  static constexpr int GROUP = KIND == DOWN_FWD || KIND == DX_BWD ? 8 : 2;
   static_assert(NW * EPI_WAVE <= LDS, "epilogue staging exceeds the ring");
 };
 
