@@ -620,11 +620,18 @@ __global__ __launch_bounds__(256) void combine_bwd_rows_kernel(const T* dy, cons
       }
     }
   }
-  // the routes' dot products, reduced together (fixed xor order)
+  // the resident routes' dot products, reduced together (fixed xor order),
+  // over as many as the token has (rounded up to 2, 4 or 8)
+  auto reduce = [&](auto n_tag) {
+    constexpr int N = decltype(n_tag)::value;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1)
+    for (int off = 32; off > 0; off >>= 1)
 #pragma unroll
-    for (int s = 0; s < 8; ++s) dot[s] += __shfl_xor(dot[s], off, 64);
+      for (int s = 0; s < N; ++s) dot[s] += __shfl_xor(dot[s], off, 64);
+  };
+  if (nr > 4) reduce(std::integral_constant<int, 8>{});
+  else if (nr > 2) reduce(std::integral_constant<int, 4>{});
+  else if (nr > 0) reduce(std::integral_constant<int, 2>{});
   if (lane < k) {
     float r = 0.f;
     if (my_p >= 0) {
