@@ -425,7 +425,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
   if constexpr (XS > 0) logits_mfma_staged<NEB, XS>(a, t0, zl, LDZ);
   else if constexpr (BF16) logits_mfma<NEB>(a, t0, zl, LDZ);
   else logits_f32(a, t0, zl, LDZ);
-  // z = (dot + bias) * inv_tau (logits_mfma finishes it for up to 64 experts)
+  // z = (dot + bias) * inv_tau (the bf16 logits paths finish it for up to 64 experts)
   constexpr bool z_done = BF16 && NEB <= 2;
   for (int p = threadIdx.x; !z_done && p < RT_TOK * a.E; p += RT_THREADS) {
     const int i = p / a.E, e = p % a.E;
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_fwd_kernel(RouteFwdArgs a) {
     const int t = t0 + i;
     if (a.logits && t < a.T) a.logits[(size_t)t * a.E + e] = v;
   }
-  if constexpr (!z_done) __syncthreads();  // (logits_mfma ends with one)
+  if constexpr (!z_done) __syncthreads();  // (those paths end with one)
 
   if (a.k <= RT_KSEL) {
     static_assert(RT_TOK == 4 * RT_WAVES, "16 lanes per token in every wave");
